@@ -1,0 +1,211 @@
+"""Benchmark of the replicated-encoder step on one MI355X.
+
+One step = one pass of the whole hot path over one synthetic micro-batch of the
+Qwen2-VL-ViT-shaped workload (24 images, sides log-uniform in [224, 1344]):
+trained forward with tape -> merge scatter into the LLM input buffer -> merge
+gather of the upstream gradient -> backward with fp32 weight-gradient
+accumulation.  Inputs are resident in HBM before the timed region.
+
+Prints one JSON line (rank 0).  See the design doc for the FLOP model, the roofline
+figures and the CPU-baseline sample."""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import platform
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2516.6     # MI355X dense bf16 MFMA (256 CU x 4096 FLOP/clk x 2.4 GHz)
+PEAK_F32_TFLOPS = 157.3
+PEAK_HBM_GBPS = 8000.0
+METRIC = "encoder patch-tokens/sec fwd+bwd on 1 MI355X; % bf16 MFMA peak"
+
+
+def log(msg: str):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def model_flops(cfg, n_patches: int, sum_len2: int, trainable: bool) -> float:
+    """Algorithmic FLOPs of one step (recompute and padding excluded).
+
+    forward F = 2 N Kpe h + L (8 N h^2 + 4 N h m + 4 h sum_i L_i^2) + 8 N h^2 + 2 N h H;
+    trained = 3 F minus the patch-gradient GEMM (2 N Kpe h), which the trainable
+    source does not compute (nothing is sent upstream); frozen = F."""
+    N, h, m, H, L = n_patches, cfg.hidden, cfg.mlp, cfg.llm_hidden, cfg.layers
+    kpe = cfg.k_pe
+    F = (2 * N * kpe * h + L * (8 * N * h * h + 4 * N * h * m + 4 * h * sum_len2)
+         + 8 * N * h * h + 2 * N * h * H)
+    return float(3 * F - 2 * N * kpe * h) if trainable else float(F)
+
+
+def cpu_baseline(seconds_hint: float = 20.0):
+    """Time the CPU oracle on a bounded sample of the same workload shape: one
+    224x224 image (256 patches) through the full-depth encoder, forward and
+    backward (trained) or forward only (frozen)."""
+    import oracle
+    import workload as W
+    cfg = W.CONFIGS["c4_qwen2vl_trained"].cfg
+    wl = W.make_workload("c4_qwen2vl_trained", 0, grid_thw=np.array([[1, 16, 16]]))
+    w, X = wl.weights(), wl.patches()
+    dM = np.random.default_rng(0).standard_normal((wl.n_merged, cfg.llm_hidden))
+    t0 = time.perf_counter()
+    oracle.encoder(cfg, w, X, wl.cu_seqlens, wl.grid_thw, True, d_merged=dM)
+    dt = time.perf_counter() - t0
+    return {"value": wl.n_patches / dt, "unit": "patch-tokens/s", "cores": oracle.num_threads(),
+            "kind": "oracle",
+            "sample": ("one 224x224 image (256 patches), Qwen2-VL-ViT shape, all 32 layers, "
+                       "fp64 forward+backward incl. merger; " f"{dt:.1f} s"),
+            "cpu": platform.processor() or _cpu_model()}
+
+
+def _cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="c4_qwen2vl_trained")
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-profile", action="store_true",
+                    help="skip the per-kernel event timing (roofline figures)")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py measures one MI355X only: the encoder step runs on one GPU "
+              "(see DESIGN.md for how the transpose schedule shards it).", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2607_03229_amd as mp
+    import workload as W
+
+    dev = torch.device("cuda:0")
+    wl = W.make_workload(args.workload, args.seed)
+    cfg = wl.cfg
+    trainable = wl.trainable
+    tdt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
+    log(f"workload {wl.name}: {wl.n_items} items, {wl.n_patches} patches, {wl.n_merged} merged")
+
+    enc = mp.Encoder(cfg)
+    sz = enc.sizes(wl.cu_seqlens, wl.grid_thw, trainable)
+    t0 = time.perf_counter()
+    weights = torch.from_numpy(wl.weights()).to(dev).to(tdt)
+    patches = torch.from_numpy(wl.patches()).to(dev).to(tdt)
+    idx = torch.from_numpy(wl.placeholders()).to(dev)
+    emb = torch.from_numpy(wl.emb_init()).to(dev).to(tdt)
+    d_emb = torch.from_numpy(wl.d_emb()).to(dev).to(tdt)
+    log(f"inputs resident ({time.perf_counter() - t0:.1f} s); workspace "
+        f"{sz['workspace'] / 2**30:.2f} GiB, tape {sz['tape'] / 2**30:.2f} GiB")
+    merged = torch.empty((sz["n_merged"], cfg.llm_hidden), dtype=tdt, device=dev)
+    d_merged = torch.empty_like(merged)
+    ws = torch.empty(sz["workspace"], dtype=torch.uint8, device=dev)
+    tape = torch.empty(max(sz["tape"], 1), dtype=torch.uint8, device=dev) if trainable else None
+    d_w = torch.zeros(weights.numel(), dtype=torch.float32, device=dev) if trainable else None
+    stream = torch.cuda.current_stream()
+
+    def step():
+        enc.fwd(weights, patches, wl.cu_seqlens, wl.grid_thw, trainable, merged, tape, ws)
+        mp.merge_scatter(merged, idx, emb)
+        if trainable:
+            mp.merge_gather(d_emb, idx, d_merged)
+            enc.bwd(weights, patches, wl.cu_seqlens, wl.grid_thw, True, tape, d_merged, d_w,
+                    None, ws)
+
+    for i in range(args.warmup):
+        step()
+        torch.cuda.synchronize()
+        log(f"warmup step {i + 1}/{args.warmup} done")
+    profile = not args.no_profile
+    if profile:
+        enc.profile(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    log(f"timed {args.steps} steps: {elapsed * 1e3 / args.steps:.1f} ms/step")
+    kern = enc.profile_read(stream) if profile else {}
+    enc.profile(False)
+
+    # scatter bandwidth, timed on its own
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    reps = 20
+    ev0.record(stream)
+    for _ in range(reps):
+        mp.merge_scatter(merged, idx, emb)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    esz = 2 if cfg.dtype == "bf16" else 4
+    scat_bytes = 2 * wl.n_merged * cfg.llm_hidden * esz + 8 * wl.n_merged
+    scat_ms = ev0.elapsed_time(ev1) / reps
+    scatter_gbps = scat_bytes / (scat_ms * 1e-3) / 1e9
+
+    sum_len2 = int(np.sum(np.diff(wl.cu_seqlens).astype(np.int64) ** 2))
+    flops = model_flops(cfg, wl.n_patches, sum_len2, trainable)
+    ms_step = elapsed * 1e3 / args.steps
+    achieved = flops / (ms_step * 1e-3) / 1e12
+    peak = PEAK_BF16_TFLOPS if cfg.dtype == "bf16" else PEAK_F32_TFLOPS
+
+    roofline = None
+    kernels = {}
+    if kern:
+        for name, (n, ms, fl) in sorted(kern.items(), key=lambda kv: -kv[1][1]):
+            kernels[name] = {"launches": n, "ms_total": round(ms, 3),
+                             "ms_avg": round(ms / max(n, 1), 4),
+                             "tflops": round(fl / (ms * 1e-3) / 1e12, 1) if ms > 0 and fl > 0 else None}
+        dom = max((k for k in kern if kern[k][2] > 0), key=lambda k: kern[k][1])
+        n, ms, fl = kern[dom]
+        ach = fl / n / (ms / n * 1e-3) / 1e12
+        roofline = {"kernel": dom, "bound": "mfma", "achieved": round(ach, 1), "peak": peak,
+                    "unit": "TFLOP/s", "frac": round(ach / peak, 4), "traffic": None,
+                    "launches": n, "avg_ms": round(ms / n, 4),
+                    "flop_per_launch": fl / n}
+
+    result = {
+        "metric": METRIC,
+        "value": round(wl.n_patches / (ms_step * 1e-3), 1),
+        "unit": "patch-tokens/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 3),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": cfg.dtype, "data": "synthetic",
+        "config": {"workload": wl.name, "seed": args.seed, "mode": "trained" if trainable else "frozen",
+                   "n_items": wl.n_items, "n_patches": wl.n_patches, "n_merged": wl.n_merged,
+                   "sum_seg_len2": sum_len2,
+                   "encoder": f"h{cfg.hidden} L{cfg.layers} heads{cfg.heads} mlp{cfg.mlp} "
+                              f"T{cfg.temporal_patch} merge->{cfg.llm_hidden}",
+                   "parallelism": "1 GPU (one pipeline rank's encoder share)"},
+        "model_tflop_per_step": round(flops / 1e12, 3),
+        "achieved_tflops": round(achieved, 1),
+        "mfma_pct_of_peak": round(100 * achieved / peak, 2),
+        "peak_tflops": peak,
+        "scatter_GBps": round(scatter_gbps, 1),
+        "scatter_pct_of_hbm": round(100 * scatter_gbps / PEAK_HBM_GBPS, 1),
+        "roofline": roofline,
+        "kernels": kernels,
+    }
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle on its bounded sample")
+        result["cpu_baseline"] = cpu_baseline()
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,303 @@
+"""ctypes binding of libmpipe (include/mpipe.h, include/mpipe_ops.h).
+
+Argument marshalling only: torch tensors provide device memory and the current
+HIP stream; every step of the encoder runs in the library's kernels."""
+from __future__ import annotations
+
+import ctypes as C
+import os
+from typing import Dict, List, Optional, Sequence, Tuple
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB_PATH = os.path.join(_HERE, "libmpipe.so")
+
+F32, BF16 = 0, 1
+OK, NOOP_FROZEN = 0, 1
+_STATUS = {0: "OK", 1: "NOOP_FROZEN", -1: "INVALID_ARG", -2: "BAD_METADATA", -3: "WORKSPACE",
+           -4: "NO_TAPE", -5: "UNSUPPORTED", -6: "HIP"}
+
+
+class MpipeError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"mpipe status {status} ({_STATUS.get(status, '?')}): {msg}")
+        self.status = status
+
+
+class EncoderCfg(C.Structure):
+    _fields_ = [("in_chans", C.c_int32), ("patch", C.c_int32), ("temporal_patch", C.c_int32),
+                ("hidden", C.c_int32), ("layers", C.c_int32), ("heads", C.c_int32),
+                ("mlp", C.c_int32), ("merge", C.c_int32), ("llm_hidden", C.c_int32),
+                ("dtype", C.c_int32), ("ln_eps", C.c_float), ("rope_theta", C.c_float)]
+
+    @classmethod
+    def from_config(cls, cfg) -> "EncoderCfg":
+        """From any object with the encoder-config attributes (e.g. workload.EncoderConfig)."""
+        dt = BF16 if getattr(cfg, "dtype", "bf16") in ("bf16", BF16) else F32
+        return cls(cfg.in_chans, cfg.patch, cfg.temporal_patch, cfg.hidden, cfg.layers,
+                   cfg.heads, cfg.mlp, cfg.merge, cfg.llm_hidden, dt, float(cfg.ln_eps),
+                   float(cfg.rope_theta))
+
+
+_lib = None
+
+
+def lib_path() -> str:
+    return _LIB_PATH
+
+
+def load():
+    """Load libmpipe.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB_PATH):
+        raise MpipeError(-6, f"{_LIB_PATH} is missing: build it with paper_2607_03229_amd/build.py")
+    L = C.CDLL(_LIB_PATH)
+    P, i32, i64, sz = C.c_void_p, C.c_int32, C.c_int64, C.c_size_t
+    st = C.c_int
+    sig = {
+        "mpipe_encoder_create": (st, [P, P]),
+        "mpipe_encoder_destroy": (None, [P]),
+        "mpipe_param_count": (i64, [P]),
+        "mpipe_param_tensors": (i32, [P]),
+        "mpipe_param_info": (st, [P, i32, C.c_char_p, i32, P, P, P]),
+        "mpipe_encoder_sizes": (st, [P, P, i32, P, i32, i32, P, P, P, P]),
+        "mpipe_encoder_fwd": (st, [P, P, P, P, i32, P, i32, i32, P, P, sz, P, sz, P]),
+        "mpipe_encoder_bwd": (st, [P, P, P, P, i32, P, i32, i32, P, sz, P, P, P, P, sz, P]),
+        "mpipe_merge_scatter": (st, [P, i64, i32, i32, P, P, i64, P]),
+        "mpipe_merge_gather": (st, [P, i64, i32, i32, P, i64, P, P]),
+        "mpipe_merge_check_indices": (st, [P, i64, i64, P, P, P]),
+        "mpipe_last_error": (C.c_char_p, []),
+        "mpipe_profile_enable": (st, [P, i32]),
+        "mpipe_profile_read": (i32, [P, P, i32, P, i32, P, P, P]),
+        "mpipe_op_gemm": (st, [i32, i32, i32, i32, i32, i32, P, i64, P, i64, P, i64, P, P, i64,
+                               P, i64, i32, i32, i64, P]),
+        "mpipe_op_layernorm_fwd": (st, [i32, P, i64, i32, P, P, C.c_float, P, P, P, P]),
+        "mpipe_op_layernorm_bwd": (st, [i32, P, P, P, P, P, i64, i32, P, P, P, P, P, P, sz, P]),
+        "mpipe_op_rope": (st, [i32, P, i64, i32, i32, P, i32, C.c_float, i32, P, sz, P]),
+        "mpipe_op_attention_fwd": (st, [i32, P, i64, i32, i32, P, i32, P, P, P, sz, P]),
+        "mpipe_op_attention_bwd": (st, [i32, P, P, P, P, i64, i32, i32, P, i32, P, P, sz, P]),
+        "mpipe_op_scratch_bytes": (sz, [i64, i32, i32, i32]),
+    }
+    for name, (res, args) in sig.items():
+        f = getattr(L, name)
+        f.restype = res
+        f.argtypes = args
+    _lib = L
+    return L
+
+
+def last_error() -> str:
+    v = load().mpipe_last_error()
+    return v.decode() if v else ""
+
+
+def _check(status: int, allow=(OK,)) -> int:
+    if status not in allow:
+        raise MpipeError(status, last_error())
+    return status
+
+
+def _ptr(t) -> Optional[int]:
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    return t.data_ptr()
+
+
+def _stream(stream=None) -> int:
+    import torch
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return s.cuda_stream
+
+
+def _host_i32(a) -> Tuple[np.ndarray, C.c_void_p]:
+    arr = np.ascontiguousarray(np.asarray(a, dtype=np.int32))
+    return arr, arr.ctypes.data_as(C.c_void_p)
+
+
+# --------------------------------------------------------------------------
+# Encoder handle
+# --------------------------------------------------------------------------
+
+class Encoder:
+    """Handle over mpipe_encoder_*; all tensors are torch device tensors."""
+
+    def __init__(self, cfg):
+        self.L = load()
+        self.ccfg = cfg if isinstance(cfg, EncoderCfg) else EncoderCfg.from_config(cfg)
+        h = C.c_void_p()
+        _check(self.L.mpipe_encoder_create(C.byref(self.ccfg), C.byref(h)))
+        self._h = h
+
+    def close(self):
+        if getattr(self, "_h", None) is not None and self._h.value:
+            self.L.mpipe_encoder_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    # -- parameter table --
+    def param_count(self) -> int:
+        return int(self.L.mpipe_param_count(C.byref(self.ccfg)))
+
+    def param_table(self) -> List[Tuple[str, int, int, int]]:
+        n = self.L.mpipe_param_tensors(C.byref(self.ccfg))
+        buf = C.create_string_buffer(128)
+        off, r, c = C.c_int64(), C.c_int64(), C.c_int64()
+        out = []
+        for i in range(n):
+            _check(self.L.mpipe_param_info(C.byref(self.ccfg), i, buf, 128, C.byref(off),
+                                           C.byref(r), C.byref(c)))
+            out.append((buf.value.decode(), off.value, r.value, c.value))
+        return out
+
+    # -- sizes --
+    def sizes(self, cu_seqlens, grid_thw, trainable: bool) -> Dict[str, int]:
+        cu, cup = _host_i32(cu_seqlens)
+        g, gp = _host_i32(np.asarray(grid_thw).reshape(-1, 3))
+        ws, tp, nm, npch = C.c_size_t(), C.c_size_t(), C.c_int64(), C.c_int64()
+        _check(self.L.mpipe_encoder_sizes(self._h, cup, max(len(cu) - 1, 0), gp, g.shape[0],
+                                          int(trainable), C.byref(ws), C.byref(tp),
+                                          C.byref(nm), C.byref(npch)))
+        return {"workspace": ws.value, "tape": tp.value, "n_merged": nm.value,
+                "n_patches": npch.value}
+
+    # -- fwd / bwd --
+    def fwd(self, weights, patches, cu_seqlens, grid_thw, trainable: bool, merged, tape,
+            workspace, stream=None) -> int:
+        cu, cup = _host_i32(cu_seqlens)
+        g, gp = _host_i32(np.asarray(grid_thw).reshape(-1, 3))
+        tb = 0 if tape is None else tape.numel() * tape.element_size()
+        wb = 0 if workspace is None else workspace.numel() * workspace.element_size()
+        return _check(self.L.mpipe_encoder_fwd(
+            self._h, _ptr(weights), _ptr(patches), cup, max(len(cu) - 1, 0), gp, g.shape[0],
+            int(trainable), _ptr(merged), _ptr(tape), tb, _ptr(workspace), wb, _stream(stream)))
+
+    def bwd(self, weights, patches, cu_seqlens, grid_thw, trainable: bool, tape, d_merged,
+            d_weights, d_patches, workspace, stream=None) -> int:
+        cu, cup = _host_i32(cu_seqlens)
+        g, gp = _host_i32(np.asarray(grid_thw).reshape(-1, 3))
+        tb = 0 if tape is None else tape.numel() * tape.element_size()
+        wb = 0 if workspace is None else workspace.numel() * workspace.element_size()
+        return _check(self.L.mpipe_encoder_bwd(
+            self._h, _ptr(weights), _ptr(patches), cup, max(len(cu) - 1, 0), gp, g.shape[0],
+            int(trainable), _ptr(tape), tb, _ptr(d_merged), _ptr(d_weights), _ptr(d_patches),
+            _ptr(workspace), wb, _stream(stream)), allow=(OK, NOOP_FROZEN))
+
+    # -- kernel timing --
+    def profile(self, enable: bool):
+        _check(self.L.mpipe_profile_enable(self._h, int(enable)))
+
+    def profile_read(self, stream=None) -> Dict[str, Tuple[int, float, float]]:
+        cap, stride = 64, 64
+        names = C.create_string_buffer(cap * stride)
+        la = (C.c_int64 * cap)()
+        ms = (C.c_double * cap)()
+        fl = (C.c_double * cap)()
+        n = self.L.mpipe_profile_read(self._h, _stream(stream), cap, names, stride, la, ms, fl)
+        if n < 0:
+            raise MpipeError(-6, "profile read failed")
+        out = {}
+        for i in range(n):
+            nm = names.raw[i * stride:(i + 1) * stride].split(b"\0", 1)[0].decode()
+            out[nm] = (int(la[i]), float(ms[i]), float(fl[i]))
+        return out
+
+
+# --------------------------------------------------------------------------
+# Seam scatter / gather
+# --------------------------------------------------------------------------
+
+def _dt(t) -> int:
+    import torch
+    if t.dtype == torch.bfloat16:
+        return BF16
+    if t.dtype == torch.float32:
+        return F32
+    raise MpipeError(-1, f"unsupported dtype {t.dtype}")
+
+
+def merge_scatter(merged, placeholder_idx, embeds, stream=None) -> None:
+    """embeds.view(-1, H)[idx[j]] = merged[j] (bit-exact, in place)."""
+    H = merged.shape[-1]
+    n_rows = embeds.numel() // H
+    _check(load().mpipe_merge_scatter(_ptr(merged), merged.shape[0], H, _dt(merged),
+                                      _ptr(placeholder_idx), _ptr(embeds), n_rows,
+                                      _stream(stream)))
+
+
+def merge_gather(d_embeds, placeholder_idx, d_merged, stream=None) -> None:
+    """d_merged[j] = d_embeds.view(-1, H)[idx[j]]."""
+    H = d_merged.shape[-1]
+    n_rows = d_embeds.numel() // H
+    _check(load().mpipe_merge_gather(_ptr(d_embeds), n_rows, H, _dt(d_embeds),
+                                     _ptr(placeholder_idx), d_merged.shape[0], _ptr(d_merged),
+                                     _stream(stream)))
+
+
+def merge_check_indices(placeholder_idx, n_rows: int, marks, status, stream=None) -> None:
+    _check(load().mpipe_merge_check_indices(_ptr(placeholder_idx), placeholder_idx.numel(),
+                                            n_rows, _ptr(marks), _ptr(status), _stream(stream)))
+
+
+# --------------------------------------------------------------------------
+# Kernel-level ops
+# --------------------------------------------------------------------------
+
+def op_scratch_bytes(N: int, heads: int, n: int, n_seg: int) -> int:
+    return int(load().mpipe_op_scratch_bytes(N, heads, n, n_seg))
+
+
+def op_gemm(dtype: int, layout: int, epilogue: int, M: int, N: int, K: int, A, lda: int, B,
+            ldb: int, Cout, ldc: int, bias=None, aux=None, ld_aux: int = 0, C2=None,
+            ldc2: int = 0, beta: int = 0, k_per_split: int = 0, split_stride: int = 0,
+            stream=None) -> None:
+    _check(load().mpipe_op_gemm(dtype, layout, epilogue, M, N, K, _ptr(A), lda, _ptr(B), ldb,
+                                _ptr(Cout), ldc, _ptr(bias), _ptr(aux), ld_aux, _ptr(C2), ldc2,
+                                beta, k_per_split, split_stride, _stream(stream)))
+
+
+def op_layernorm_fwd(dtype, X, rows, n, g, b, eps, Y, mean=None, rstd=None, stream=None):
+    _check(load().mpipe_op_layernorm_fwd(dtype, _ptr(X), rows, n, _ptr(g), _ptr(b), eps, _ptr(Y),
+                                         _ptr(mean), _ptr(rstd), _stream(stream)))
+
+
+def op_layernorm_bwd(dtype, dY, X, mean, rstd, g, rows, n, dres, dX, dXt, grad_g, grad_b,
+                     scratch, stream=None):
+    _check(load().mpipe_op_layernorm_bwd(dtype, _ptr(dY), _ptr(X), _ptr(mean), _ptr(rstd), _ptr(g),
+                                         rows, n, _ptr(dres), _ptr(dX), _ptr(dXt), _ptr(grad_g),
+                                         _ptr(grad_b), _ptr(scratch),
+                                         scratch.numel() * scratch.element_size(),
+                                         _stream(stream)))
+
+
+def op_rope(dtype, qkv, rows, heads, head_dim, grid_thw, theta, inverse, scratch, stream=None):
+    g, gp = _host_i32(np.asarray(grid_thw).reshape(-1, 3))
+    _check(load().mpipe_op_rope(dtype, _ptr(qkv), rows, heads, head_dim, gp, g.shape[0], theta,
+                                int(inverse), _ptr(scratch),
+                                scratch.numel() * scratch.element_size(), _stream(stream)))
+
+
+def op_attention_fwd(dtype, qkv, N, heads, head_dim, cu_seqlens, o, lse, scratch, stream=None):
+    cu, cup = _host_i32(cu_seqlens)
+    _check(load().mpipe_op_attention_fwd(dtype, _ptr(qkv), N, heads, head_dim, cup,
+                                         max(len(cu) - 1, 0), _ptr(o), _ptr(lse), _ptr(scratch),
+                                         scratch.numel() * scratch.element_size(),
+                                         _stream(stream)))
+
+
+def op_attention_bwd(dtype, qkv, o, d_o, lse, N, heads, head_dim, cu_seqlens, dqkv, scratch,
+                     stream=None):
+    cu, cup = _host_i32(cu_seqlens)
+    _check(load().mpipe_op_attention_bwd(dtype, _ptr(qkv), _ptr(o), _ptr(d_o), _ptr(lse), N,
+                                         heads, head_dim, cup, max(len(cu) - 1, 0), _ptr(dqkv),
+                                         _ptr(scratch), scratch.numel() * scratch.element_size(),
+                                         _stream(stream)))

@@ -1,0 +1,649 @@
+// Block-diagonal variable-length attention for the packed patch sequence.
+//
+// Each item (or temporal slice) of the micro-batch is one attention segment
+// [s0, s1) of the packed rows; a query attends to every key of its own segment
+// and to no other (non-causal softmax attention, scale 1/sqrt(d)).  Segment
+// tables and tile work lists come from the host planner, longest segments
+// first, heads innermost, so that the longest-running blocks start first.
+//
+// bf16 kernels (gfx950 MFMA):
+//   forward  S^T = K Q^T, online softmax in fp32 (exp2 domain), O^T += V^T P^T.
+//            Working on S^T puts one query per lane column, so the per-query
+//            max/sum need only a 4-lane reduction and the P^T fragment is
+//            already in B-operand layout for the PV product (keys are taken in
+//            the permuted order {4g..4g+3, 16+4g..16+4g+3} on both operands).
+//   backward two deterministic kernels that recompute P from Q, K and the LSE:
+//            dK/dV per 128-key tile looping over query tiles, and dQ per
+//            128-query tile looping over key tiles.  No atomics.
+// head_dim 80 = 2 MFMA K-steps of 32 + one 16x16x16 step; output d-tiles of 16.
+// fp32 kernels (the small fp32 configuration): plain per-row loops.
+#include "common.h"
+#include "internal.h"
+
+namespace mpipe {
+namespace {
+
+constexpr int NTHR = 256;
+
+template <int D> struct AD {
+  static constexpr int NC = D / 8;                          // 16-byte chunks per row
+  static constexpr int PC = (NC % 2 == 0) ? NC + 1 : NC;    // odd pitch: conflict-free reads
+  static constexpr int NF = D / 32;                         // full 32-wide K steps over d
+  static constexpr bool REM = (D % 32) != 0;                // one 16-wide remainder step
+  static constexpr int NDT = D / 16;                        // 16-wide output d tiles
+};
+
+// ---- LDS tile helpers ------------------------------------------------------------
+
+// Load rows [r0, r0+64) x D of a head from X (row stride ld) into a row tile with
+// pitch PC chunks, zero-filling rows >= rend.  Optionally also write the
+// transposed tile [D][64] (128-byte rows, swizzled chunks).
+template <int D, bool ROW, bool TR>
+__device__ __forceinline__ void load_tile(uint4* rowt, uint4* trt, const bf16* X, int64_t ld,
+                                          int r0, int rend) {
+  constexpr int NC = AD<D>::NC, PC = AD<D>::PC;
+  const int t = threadIdx.x;
+  if constexpr (TR) {
+    // 16 row-quads x NC d-chunks sub-blocks of 4 rows x 8 d
+    for (int sb = t; sb < 16 * NC; sb += NTHR) {
+      const int rq = sb % 16, dc = sb / 16;
+      uint4 v[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int row = r0 + 4 * rq + j;
+        v[j] = row < rend ? *reinterpret_cast<const uint4*>(X + (int64_t)row * ld + 8 * dc)
+                          : make_uint4(0, 0, 0, 0);
+        if constexpr (ROW) rowt[(4 * rq + j) * PC + dc] = v[j];
+      }
+      const uint32_t* w0 = reinterpret_cast<const uint32_t*>(&v[0]);
+      const uint32_t* w1 = reinterpret_cast<const uint32_t*>(&v[1]);
+      const uint32_t* w2 = reinterpret_cast<const uint32_t*>(&v[2]);
+      const uint32_t* w3 = reinterpret_cast<const uint32_t*>(&v[3]);
+      uint2* t2 = reinterpret_cast<uint2*>(trt);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const int pw = i >> 1;
+        uint2 o;
+        if (i & 1) {
+          o.x = pack_hi(w0[pw], w1[pw]);
+          o.y = pack_hi(w2[pw], w3[pw]);
+        } else {
+          o.x = pack_lo(w0[pw], w1[pw]);
+          o.y = pack_lo(w2[pw], w3[pw]);
+        }
+        const int drow = 8 * dc + i;
+        t2[swz(drow, rq >> 1) * 2 + (rq & 1)] = o;
+      }
+    }
+  } else {
+    for (int c = t; c < 64 * NC; c += NTHR) {
+      const int rr = c / NC, dc = c % NC;
+      const int row = r0 + rr;
+      rowt[rr * PC + dc] = row < rend ? *reinterpret_cast<const uint4*>(X + (int64_t)row * ld + 8 * dc)
+                                      : make_uint4(0, 0, 0, 0);
+    }
+  }
+}
+
+// A/B fragment of a 16x16x32 MFMA from a row tile: row `row`, d in [32f + 8g, +8)
+template <int D>
+__device__ __forceinline__ bf16x8 frag_row(const uint4* rowt, int row, int f, int g) {
+  uint4 v = rowt[row * AD<D>::PC + 4 * f + g];
+  return *reinterpret_cast<bf16x8*>(&v);
+}
+// 16x16x16 remainder fragment: d in [32 NF + 4g, +4)
+template <int D>
+__device__ __forceinline__ s16x4 frag_row_rem(const uint4* rowt, int row, int g) {
+  const uint2* p = reinterpret_cast<const uint2*>(rowt);
+  uint2 v = p[(row * AD<D>::PC + 4 * AD<D>::NF) * 2 + g];
+  return *reinterpret_cast<s16x4*>(&v);
+}
+// fragment from a transposed tile: row `row` (a d index), columns {c0..c0+3, c0+16..c0+19}
+__device__ __forceinline__ bf16x8 frag_tr(const uint4* trt, int row, int c0) {
+  const uint2* p = reinterpret_cast<const uint2*>(trt);
+  uint2 a = p[swz(row, c0 >> 3) * 2 + ((c0 >> 2) & 1)];
+  const int c1 = c0 + 16;
+  uint2 b = p[swz(row, c1 >> 3) * 2 + ((c1 >> 2) & 1)];
+  uint4 v = make_uint4(a.x, a.y, b.x, b.y);
+  return *reinterpret_cast<bf16x8*>(&v);
+}
+
+// register fragments of one row (query/key) straight from global memory
+template <int D> struct RowFrag {
+  bf16x8 f[AD<D>::NF > 0 ? AD<D>::NF : 1];
+  s16x4 rem;
+};
+template <int D>
+__device__ __forceinline__ void load_rowfrag(RowFrag<D>& R, const bf16* X, int64_t ld, int row,
+                                             int g) {
+  const bf16* base = X + (int64_t)row * ld;
+#pragma unroll
+  for (int f = 0; f < AD<D>::NF; ++f) {
+    uint4 v = *reinterpret_cast<const uint4*>(base + 32 * f + 8 * g);
+    R.f[f] = *reinterpret_cast<bf16x8*>(&v);
+  }
+  if constexpr (AD<D>::REM) {
+    uint2 v = *reinterpret_cast<const uint2*>(base + 32 * AD<D>::NF + 4 * g);
+    R.rem = *reinterpret_cast<s16x4*>(&v);
+  }
+}
+
+// acc += A(row tile, rows arow..) x B(register fragment) over d.
+// The 16-wide remainder MFMA gets its own zero-initialised accumulator and is
+// added with a VALU add: an MFMA must never take the result of an MFMA of a
+// different shape as its accumulator input (the generated code then reads a
+// stale accumulator, because no wait states separate the two).
+template <int D>
+__device__ __forceinline__ f32x4 dot_d(const uint4* rowt, int arow, const RowFrag<D>& B, int g,
+                                       f32x4 acc) {
+#pragma unroll
+  for (int f = 0; f < AD<D>::NF; ++f)
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(frag_row<D>(rowt, arow, f, g), B.f[f], acc, 0, 0, 0);
+  if constexpr (AD<D>::REM) {
+    const f32x4 r = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(frag_row_rem<D>(rowt, arow, g), B.rem,
+                                                              f32x4{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
+    acc += r;
+  }
+  return acc;
+}
+
+__device__ __forceinline__ bf16x8 pack8(const f32x4& a, const f32x4& b) {
+  bf16x8 r;
+  r[0] = (bf16)a[0]; r[1] = (bf16)a[1]; r[2] = (bf16)a[2]; r[3] = (bf16)a[3];
+  r[4] = (bf16)b[0]; r[5] = (bf16)b[1]; r[6] = (bf16)b[2]; r[7] = (bf16)b[3];
+  return r;
+}
+
+// ---- forward ----------------------------------------------------------------------
+
+template <int D>
+__global__ __launch_bounds__(NTHR, 2) void attn_fwd_kernel(AttnArgs p) {
+  constexpr int PC = AD<D>::PC, NDT = AD<D>::NDT;
+  __shared__ uint4 kt_s[64 * PC];   // K tile [key][d]
+  __shared__ uint4 vt_s[D * 8];     // V^T tile [d][key]
+  const int work = blockIdx.x / p.heads, head = blockIdx.x % p.heads;
+  const int4 wk = p.work[work];
+  const int q0 = wk.x, s0 = wk.y, s1 = wk.z;
+  const int w = threadIdx.x >> 6, l = threadIdx.x & 63, g = l >> 4, r = l & 15;
+  const bf16* Q = reinterpret_cast<const bf16*>(p.q) + head * D;
+  const bf16* K = reinterpret_cast<const bf16*>(p.k) + head * D;
+  const bf16* V = reinterpret_cast<const bf16*>(p.v) + head * D;
+  const float sl2 = p.scale * kLog2e;
+
+  RowFrag<D> qf[2];
+  int qrow[2];
+#pragma unroll
+  for (int qs = 0; qs < 2; ++qs) {
+    qrow[qs] = q0 + 32 * w + 16 * qs + r;
+    load_rowfrag<D>(qf[qs], Q, p.ld, min(qrow[qs], s1 - 1), g);
+  }
+  float m[2] = {-INFINITY, -INFINITY}, lsum[2] = {0.f, 0.f};
+  f32x4 o[2][NDT];
+#pragma unroll
+  for (int qs = 0; qs < 2; ++qs)
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt) o[qs][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  for (int k0 = s0; k0 < s1; k0 += 64) {
+    __syncthreads();
+    load_tile<D, true, false>(kt_s, nullptr, K, p.ld, k0, s1);
+    load_tile<D, false, true>(nullptr, vt_s, V, p.ld, k0, s1);
+    __syncthreads();
+    f32x4 s[4][2];
+#pragma unroll
+    for (int kq = 0; kq < 4; ++kq)
+#pragma unroll
+      for (int qs = 0; qs < 2; ++qs)
+        s[kq][qs] = dot_d<D>(kt_s, 16 * kq + r, qf[qs], g, f32x4{0.f, 0.f, 0.f, 0.f});
+    bf16x8 pb[2][2];
+#pragma unroll
+    for (int qs = 0; qs < 2; ++qs) {
+      float mx = -INFINITY;
+#pragma unroll
+      for (int kq = 0; kq < 4; ++kq)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const int key = k0 + 16 * kq + 4 * g + v;
+          const float x = key < s1 ? s[kq][qs][v] * sl2 : -INFINITY;
+          s[kq][qs][v] = x;
+          mx = fmaxf(mx, x);
+        }
+      mx = fmaxf(mx, __shfl_xor(mx, 16));
+      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      const float mn = fmaxf(m[qs], mx);
+      const float alpha = exp2f(m[qs] - mn);
+      m[qs] = mn;
+      float ps = 0.f;
+#pragma unroll
+      for (int kq = 0; kq < 4; ++kq)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const float e = exp2f(s[kq][qs][v] - mn);
+          s[kq][qs][v] = e;
+          ps += e;
+        }
+      lsum[qs] = lsum[qs] * alpha + ps;
+#pragma unroll
+      for (int dt = 0; dt < NDT; ++dt) o[qs][dt] *= alpha;
+      pb[qs][0] = pack8(s[0][qs], s[1][qs]);
+      pb[qs][1] = pack8(s[2][qs], s[3][qs]);
+    }
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk) {
+        const bf16x8 a = frag_tr(vt_s, 16 * dt + r, 32 * kk + 4 * g);
+#pragma unroll
+        for (int qs = 0; qs < 2; ++qs)
+          o[qs][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb[qs][kk], o[qs][dt], 0, 0, 0);
+      }
+  }
+  bf16* O = reinterpret_cast<bf16*>(p.out) + head * D;
+#pragma unroll
+  for (int qs = 0; qs < 2; ++qs) {
+    float tot = lsum[qs];
+    tot += __shfl_xor(tot, 16);
+    tot += __shfl_xor(tot, 32);
+    const int q = qrow[qs];
+    if (q < s1) {
+      const float inv = 1.0f / tot;
+#pragma unroll
+      for (int dt = 0; dt < NDT; ++dt) {
+        bf16 v4[4];
+#pragma unroll
+        for (int v = 0; v < 4; ++v) v4[v] = (bf16)(o[qs][dt][v] * inv);
+        *reinterpret_cast<uint2*>(O + (int64_t)q * p.ldo + 16 * dt + 4 * g) =
+            *reinterpret_cast<uint2*>(v4);
+      }
+      if (g == 0 && p.lse) p.lse[(int64_t)head * p.N + q] = (m[qs] + log2f(tot)) * kLn2;
+    }
+  }
+}
+
+// ---- backward: dK, dV ------------------------------------------------------------
+
+template <int D>
+__global__ __launch_bounds__(NTHR, 1) void attn_bwd_dkdv_kernel(AttnArgs p) {
+  constexpr int PC = AD<D>::PC, NDT = AD<D>::NDT;
+  __shared__ uint4 q_s[64 * PC], do_s[64 * PC];   // [query][d]
+  __shared__ uint4 qT_s[D * 8], doT_s[D * 8];     // [d][query]
+  __shared__ float lse_s[64], del_s[64];
+  const int work = blockIdx.x / p.heads, head = blockIdx.x % p.heads;
+  const int4 wk = p.work[work];
+  const int k0 = wk.x, s0 = wk.y, s1 = wk.z;
+  const int w = threadIdx.x >> 6, l = threadIdx.x & 63, g = l >> 4, r = l & 15;
+  const bf16* Q = reinterpret_cast<const bf16*>(p.q) + head * D;
+  const bf16* K = reinterpret_cast<const bf16*>(p.k) + head * D;
+  const bf16* V = reinterpret_cast<const bf16*>(p.v) + head * D;
+  const bf16* O = reinterpret_cast<const bf16*>(p.o) + head * D;
+  (void)O;
+  const bf16* dO = reinterpret_cast<const bf16*>(p.d_o) + head * D;
+  const float sl2 = p.scale * kLog2e;
+
+  RowFrag<D> kf[2], vf[2];
+#pragma unroll
+  for (int ks = 0; ks < 2; ++ks) {
+    const int key = min(k0 + 32 * w + 16 * ks + r, s1 - 1);
+    load_rowfrag<D>(kf[ks], K, p.ld, key, g);
+    load_rowfrag<D>(vf[ks], V, p.ld, key, g);
+  }
+  f32x4 dk[2][NDT], dv[2][NDT];
+#pragma unroll
+  for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt) dk[ks][dt] = dv[ks][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  for (int q0 = s0; q0 < s1; q0 += 64) {
+    __syncthreads();
+    load_tile<D, true, true>(q_s, qT_s, Q, p.ld, q0, s1);
+    load_tile<D, true, true>(do_s, doT_s, dO, p.ldo, q0, s1);
+    if (threadIdx.x < 64) {
+      const int q = q0 + threadIdx.x;
+      lse_s[threadIdx.x] = q < s1 ? p.lse[(int64_t)head * p.N + q] * kLog2e : INFINITY;
+      del_s[threadIdx.x] = q < s1 ? p.delta[(int64_t)head * p.N + q] : 0.f;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+      // S and dP for queries [32kk, 32kk+32) of the tile, keys of this wave
+      f32x4 P[2][2], dS[2][2];   // [qs-in-half][ks]
+#pragma unroll
+      for (int h2 = 0; h2 < 2; ++h2) {
+        const int qrow = 16 * (2 * kk + h2) + r;   // A-operand row (query) for this lane
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+          f32x4 s = dot_d<D>(q_s, qrow, kf[ks], g, f32x4{0.f, 0.f, 0.f, 0.f});
+          f32x4 dp = dot_d<D>(do_s, qrow, vf[ks], g, f32x4{0.f, 0.f, 0.f, 0.f});
+#pragma unroll
+          for (int v = 0; v < 4; ++v) {
+            const int qi = 16 * (2 * kk + h2) + 4 * g + v;   // query of output element v
+            const float pp = exp2f(s[v] * sl2 - lse_s[qi]);
+            P[h2][ks][v] = pp;
+            dS[h2][ks][v] = pp * (dp[v] - del_s[qi]);
+          }
+        }
+      }
+#pragma unroll
+      for (int ks = 0; ks < 2; ++ks) {
+        const bf16x8 ap = pack8(P[0][ks], P[1][ks]);
+        const bf16x8 ads = pack8(dS[0][ks], dS[1][ks]);
+#pragma unroll
+        for (int dt = 0; dt < NDT; ++dt) {
+          const bf16x8 bdo = frag_tr(doT_s, 16 * dt + r, 32 * kk + 4 * g);
+          const bf16x8 bq = frag_tr(qT_s, 16 * dt + r, 32 * kk + 4 * g);
+          dv[ks][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ap, bdo, dv[ks][dt], 0, 0, 0);
+          dk[ks][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ads, bq, dk[ks][dt], 0, 0, 0);
+        }
+      }
+    }
+  }
+  bf16* dK = reinterpret_cast<bf16*>(p.dk) + head * D;
+  bf16* dV = reinterpret_cast<bf16*>(p.dv) + head * D;
+#pragma unroll
+  for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int key = k0 + 32 * w + 16 * ks + 4 * g + v;
+      if (key >= s1) continue;
+#pragma unroll
+      for (int dt = 0; dt < NDT; ++dt) {
+        dK[(int64_t)key * p.ldd + 16 * dt + r] = (bf16)(dk[ks][dt][v] * p.scale);
+        dV[(int64_t)key * p.ldd + 16 * dt + r] = (bf16)(dv[ks][dt][v]);
+      }
+    }
+}
+
+// ---- backward: dQ -----------------------------------------------------------------
+
+template <int D>
+__global__ __launch_bounds__(NTHR, 2) void attn_bwd_dq_kernel(AttnArgs p) {
+  constexpr int PC = AD<D>::PC, NDT = AD<D>::NDT;
+  __shared__ uint4 k_s[64 * PC], v_s[64 * PC];   // [key][d]
+  __shared__ uint4 kT_s[D * 8];                  // [d][key]
+  const int work = blockIdx.x / p.heads, head = blockIdx.x % p.heads;
+  const int4 wk = p.work[work];
+  const int q0 = wk.x, s0 = wk.y, s1 = wk.z;
+  const int w = threadIdx.x >> 6, l = threadIdx.x & 63, g = l >> 4, r = l & 15;
+  const bf16* Q = reinterpret_cast<const bf16*>(p.q) + head * D;
+  const bf16* K = reinterpret_cast<const bf16*>(p.k) + head * D;
+  const bf16* V = reinterpret_cast<const bf16*>(p.v) + head * D;
+  const bf16* dO = reinterpret_cast<const bf16*>(p.d_o) + head * D;
+  const float sl2 = p.scale * kLog2e;
+
+  RowFrag<D> qf[2], dof[2];
+  int qrow[2];
+  float lse2[2], del[2];
+#pragma unroll
+  for (int qs = 0; qs < 2; ++qs) {
+    qrow[qs] = q0 + 32 * w + 16 * qs + r;
+    const int qc = min(qrow[qs], s1 - 1);
+    load_rowfrag<D>(qf[qs], Q, p.ld, qc, g);
+    load_rowfrag<D>(dof[qs], dO, p.ldo, qc, g);
+    lse2[qs] = p.lse[(int64_t)head * p.N + qc] * kLog2e;
+    del[qs] = p.delta[(int64_t)head * p.N + qc];
+  }
+  f32x4 dq[2][NDT];
+#pragma unroll
+  for (int qs = 0; qs < 2; ++qs)
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt) dq[qs][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  for (int k0 = s0; k0 < s1; k0 += 64) {
+    __syncthreads();
+    load_tile<D, true, true>(k_s, kT_s, K, p.ld, k0, s1);
+    load_tile<D, true, false>(v_s, nullptr, V, p.ld, k0, s1);
+    __syncthreads();
+    f32x4 ds[4][2];
+#pragma unroll
+    for (int kq = 0; kq < 4; ++kq)
+#pragma unroll
+      for (int qs = 0; qs < 2; ++qs) {
+        f32x4 s = dot_d<D>(k_s, 16 * kq + r, qf[qs], g, f32x4{0.f, 0.f, 0.f, 0.f});
+        f32x4 dp = dot_d<D>(v_s, 16 * kq + r, dof[qs], g, f32x4{0.f, 0.f, 0.f, 0.f});
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const int key = k0 + 16 * kq + 4 * g + v;
+          const float pp = key < s1 ? exp2f(s[v] * sl2 - lse2[qs]) : 0.f;
+          ds[kq][qs][v] = pp * (dp[v] - del[qs]);
+        }
+      }
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+      bf16x8 b[2];
+#pragma unroll
+      for (int qs = 0; qs < 2; ++qs) b[qs] = pack8(ds[2 * kk][qs], ds[2 * kk + 1][qs]);
+#pragma unroll
+      for (int dt = 0; dt < NDT; ++dt) {
+        const bf16x8 a = frag_tr(kT_s, 16 * dt + r, 32 * kk + 4 * g);
+#pragma unroll
+        for (int qs = 0; qs < 2; ++qs)
+          dq[qs][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b[qs], dq[qs][dt], 0, 0, 0);
+      }
+    }
+  }
+  bf16* dQ = reinterpret_cast<bf16*>(p.dq) + head * D;
+#pragma unroll
+  for (int qs = 0; qs < 2; ++qs) {
+    const int q = qrow[qs];
+    if (q >= s1) continue;
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt) {
+      bf16 v4[4];
+#pragma unroll
+      for (int v = 0; v < 4; ++v) v4[v] = (bf16)(dq[qs][dt][v] * p.scale);
+      *reinterpret_cast<uint2*>(dQ + (int64_t)q * p.ldd + 16 * dt + 4 * g) =
+          *reinterpret_cast<uint2*>(v4);
+    }
+  }
+}
+
+// ---- delta = rowsum(dO o O) per (head, query) ----------------------------------------
+
+template <class T>
+__global__ void attn_delta_kernel(const T* O, const T* dO, int64_t ldo, int64_t N, int heads,
+                                  int d, float* delta) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= N * heads) return;
+  const int64_t q = i / heads;
+  const int hd = (int)(i % heads);
+  float s = 0.f;
+  for (int e = 0; e < d; ++e)
+    s += to_f(O[q * ldo + hd * d + e]) * to_f(dO[q * ldo + hd * d + e]);
+  delta[(int64_t)hd * N + q] = s;
+}
+
+// ---- fp32 kernels: one thread per query (forward, dQ) or per key (dK, dV) -------------
+
+template <int D>
+__global__ void attn_fwd_f32_kernel(AttnArgs p) {
+  const int work = blockIdx.x / p.heads, head = blockIdx.x % p.heads;
+  const int4 wk = p.work[work];
+  const int q = wk.x + threadIdx.x, s0 = wk.y, s1 = wk.z;
+  if (q >= s1) return;
+  const float* Q = reinterpret_cast<const float*>(p.q) + head * D;
+  const float* K = reinterpret_cast<const float*>(p.k) + head * D;
+  const float* V = reinterpret_cast<const float*>(p.v) + head * D;
+  float qv[D], o[D];
+  for (int e = 0; e < D; ++e) {
+    qv[e] = Q[(int64_t)q * p.ld + e];
+    o[e] = 0.f;
+  }
+  float m = -INFINITY, lsum = 0.f;
+  for (int k = s0; k < s1; ++k) {
+    float s = 0.f;
+    for (int e = 0; e < D; ++e) s += qv[e] * K[(int64_t)k * p.ld + e];
+    s *= p.scale;
+    const float mn = fmaxf(m, s);
+    const float a = expf(m - mn), e1 = expf(s - mn);
+    lsum = lsum * a + e1;
+    for (int e = 0; e < D; ++e) o[e] = o[e] * a + e1 * V[(int64_t)k * p.ld + e];
+    m = mn;
+  }
+  float* Ot = reinterpret_cast<float*>(p.out) + head * D;
+  for (int e = 0; e < D; ++e) Ot[(int64_t)q * p.ldo + e] = o[e] / lsum;
+  if (p.lse) p.lse[(int64_t)head * p.N + q] = m + logf(lsum);
+}
+
+template <int D>
+__global__ void attn_bwd_dq_f32_kernel(AttnArgs p) {
+  const int work = blockIdx.x / p.heads, head = blockIdx.x % p.heads;
+  const int4 wk = p.work[work];
+  const int q = wk.x + threadIdx.x, s0 = wk.y, s1 = wk.z;
+  if (q >= s1) return;
+  const float* Q = reinterpret_cast<const float*>(p.q) + head * D;
+  const float* K = reinterpret_cast<const float*>(p.k) + head * D;
+  const float* V = reinterpret_cast<const float*>(p.v) + head * D;
+  const float* dO = reinterpret_cast<const float*>(p.d_o) + head * D;
+  float qv[D], dov[D], dq[D];
+  for (int e = 0; e < D; ++e) {
+    qv[e] = Q[(int64_t)q * p.ld + e];
+    dov[e] = dO[(int64_t)q * p.ldo + e];
+    dq[e] = 0.f;
+  }
+  const float L = p.lse[(int64_t)head * p.N + q], del = p.delta[(int64_t)head * p.N + q];
+  for (int k = s0; k < s1; ++k) {
+    float s = 0.f, dp = 0.f;
+    for (int e = 0; e < D; ++e) {
+      s += qv[e] * K[(int64_t)k * p.ld + e];
+      dp += dov[e] * V[(int64_t)k * p.ld + e];
+    }
+    const float ds = expf(s * p.scale - L) * (dp - del);
+    for (int e = 0; e < D; ++e) dq[e] += ds * K[(int64_t)k * p.ld + e];
+  }
+  float* dQ = reinterpret_cast<float*>(p.dq) + head * D;
+  for (int e = 0; e < D; ++e) dQ[(int64_t)q * p.ldd + e] = dq[e] * p.scale;
+}
+
+template <int D>
+__global__ void attn_bwd_dkdv_f32_kernel(AttnArgs p) {
+  const int work = blockIdx.x / p.heads, head = blockIdx.x % p.heads;
+  const int4 wk = p.work[work];
+  const int k = wk.x + threadIdx.x, s0 = wk.y, s1 = wk.z;
+  if (k >= s1) return;
+  const float* Q = reinterpret_cast<const float*>(p.q) + head * D;
+  const float* K = reinterpret_cast<const float*>(p.k) + head * D;
+  const float* V = reinterpret_cast<const float*>(p.v) + head * D;
+  const float* dO = reinterpret_cast<const float*>(p.d_o) + head * D;
+  float kv[D], vv[D], dk[D], dv[D];
+  for (int e = 0; e < D; ++e) {
+    kv[e] = K[(int64_t)k * p.ld + e];
+    vv[e] = V[(int64_t)k * p.ld + e];
+    dk[e] = dv[e] = 0.f;
+  }
+  for (int q = s0; q < s1; ++q) {
+    float s = 0.f, dp = 0.f;
+    for (int e = 0; e < D; ++e) {
+      s += Q[(int64_t)q * p.ld + e] * kv[e];
+      dp += dO[(int64_t)q * p.ldo + e] * vv[e];
+    }
+    const float pp = expf(s * p.scale - p.lse[(int64_t)head * p.N + q]);
+    const float ds = pp * (dp - p.delta[(int64_t)head * p.N + q]);
+    for (int e = 0; e < D; ++e) {
+      dv[e] += pp * dO[(int64_t)q * p.ldo + e];
+      dk[e] += ds * Q[(int64_t)q * p.ld + e];
+    }
+  }
+  float* dK = reinterpret_cast<float*>(p.dk) + head * D;
+  float* dV = reinterpret_cast<float*>(p.dv) + head * D;
+  for (int e = 0; e < D; ++e) {
+    dK[(int64_t)k * p.ldd + e] = dk[e] * p.scale;
+    dV[(int64_t)k * p.ldd + e] = dv[e];
+  }
+}
+
+template <int D>
+hipError_t fwd_bf16(const AttnArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(attn_fwd_kernel<D>, dim3(a.n_work * a.heads), dim3(NTHR), 0, s, a);
+  return hipGetLastError();
+}
+template <int D>
+hipError_t dq_bf16(const AttnArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(attn_bwd_dq_kernel<D>, dim3(a.n_work * a.heads), dim3(NTHR), 0, s, a);
+  return hipGetLastError();
+}
+template <int D>
+hipError_t dkdv_bf16(const AttnArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(attn_bwd_dkdv_kernel<D>, dim3(a.n_work * a.heads), dim3(NTHR), 0, s, a);
+  return hipGetLastError();
+}
+template <int D>
+hipError_t fwd_f32(const AttnArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(attn_fwd_f32_kernel<D>, dim3(a.n_work * a.heads), dim3(ATTN_TILE), 0, s, a);
+  return hipGetLastError();
+}
+template <int D>
+hipError_t dq_f32(const AttnArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(attn_bwd_dq_f32_kernel<D>, dim3(a.n_work * a.heads), dim3(ATTN_TILE), 0, s, a);
+  return hipGetLastError();
+}
+template <int D>
+hipError_t dkdv_f32(const AttnArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(attn_bwd_dkdv_f32_kernel<D>, dim3(a.n_work * a.heads), dim3(ATTN_TILE), 0, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+bool attention_supported(int dtype, int head_dim) {
+  if (dtype == DT_BF16) return head_dim == 32 || head_dim == 64 || head_dim == 80;
+  return head_dim == 32 || head_dim == 64 || head_dim == 80;
+}
+
+hipError_t attention_fwd(int dtype, int head_dim, const AttnArgs& a, hipStream_t s) {
+  if (a.n_work == 0) return hipSuccess;
+  if (dtype == DT_BF16) {
+    switch (head_dim) {
+      case 32: return fwd_bf16<32>(a, s);
+      case 64: return fwd_bf16<64>(a, s);
+      case 80: return fwd_bf16<80>(a, s);
+    }
+  } else {
+    switch (head_dim) {
+      case 32: return fwd_f32<32>(a, s);
+      case 64: return fwd_f32<64>(a, s);
+      case 80: return fwd_f32<80>(a, s);
+    }
+  }
+  return hipErrorInvalidValue;
+}
+
+#define MPIPE_ATTN_DISPATCH(BF, FP)                  \
+  if (a.n_work == 0) return hipSuccess;              \
+  if (dtype == DT_BF16) {                            \
+    switch (head_dim) {                              \
+      case 32: return BF<32>(a, s);                  \
+      case 64: return BF<64>(a, s);                  \
+      case 80: return BF<80>(a, s);                  \
+    }                                                \
+  } else {                                           \
+    switch (head_dim) {                              \
+      case 32: return FP<32>(a, s);                  \
+      case 64: return FP<64>(a, s);                  \
+      case 80: return FP<80>(a, s);                  \
+    }                                                \
+  }                                                  \
+  return hipErrorInvalidValue;
+
+hipError_t attention_bwd_dq(int dtype, int head_dim, const AttnArgs& a, hipStream_t s) {
+  MPIPE_ATTN_DISPATCH(dq_bf16, dq_f32)
+}
+hipError_t attention_bwd_dkdv(int dtype, int head_dim, const AttnArgs& a, hipStream_t s) {
+  MPIPE_ATTN_DISPATCH(dkdv_bf16, dkdv_f32)
+}
+#undef MPIPE_ATTN_DISPATCH
+
+hipError_t attention_delta(int dtype, const void* O, const void* dO, int64_t ldo, int64_t N,
+                           int heads, int d, float* delta, hipStream_t s) {
+  const int64_t n = N * heads;
+  if (n == 0) return hipSuccess;
+  const int blocks = (int)((n + 255) / 256);
+  if (dtype == DT_BF16)
+    hipLaunchKernelGGL(attn_delta_kernel<bf16>, dim3(blocks), dim3(256), 0, s,
+                       (const bf16*)O, (const bf16*)dO, ldo, N, heads, d, delta);
+  else
+    hipLaunchKernelGGL(attn_delta_kernel<float>, dim3(blocks), dim3(256), 0, s,
+                       (const float*)O, (const float*)dO, ldo, N, heads, d, delta);
+  return hipGetLastError();
+}
+
+}  // namespace mpipe

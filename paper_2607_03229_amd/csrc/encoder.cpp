@@ -1,0 +1,692 @@
+// C ABI of libmpipe: handle, metadata validation, and the launch sequence of the
+// encoder forward / backward on the caller's stream.  See include/mpipe.h.
+#include "../../include/mpipe.h"
+#include "../../include/mpipe_ops.h"
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <tuple>
+#include <map>
+#include <string>
+#include <vector>
+
+#include "internal.h"
+#include "plan.h"
+
+using namespace mpipe;
+
+namespace {
+thread_local std::string g_err;
+
+mpipe_status fail(mpipe_status s, const std::string& m) {
+  g_err = m;
+  return s;
+}
+}  // namespace
+
+namespace mpipe {
+mpipe_status set_error(mpipe_status s, const std::string& m) { return fail(s, m); }
+}  // namespace mpipe
+
+namespace {
+
+struct Rec {
+  std::string cls;
+  hipEvent_t a, b;
+  double flops;
+};
+}  // namespace
+
+struct mpipe_encoder {
+  Cfg cfg;
+  std::vector<ParamEntry> params;
+  void* staging = nullptr;  // pinned host memory for the per-call metadata upload
+  size_t staging_cap = 0;
+  hipEvent_t staging_ev = nullptr;
+  bool staging_pending = false;
+  bool prof = false;
+  std::vector<Rec> recs;
+  std::vector<hipEvent_t> pool;
+
+  hipEvent_t event() {
+    if (!pool.empty()) {
+      hipEvent_t e = pool.back();
+      pool.pop_back();
+      return e;
+    }
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    return e;
+  }
+};
+
+namespace {
+
+// Bracket one launch with events when profiling is on.
+template <class F>
+hipError_t run(mpipe_encoder* e, hipStream_t s, const char* cls, double flops, F&& f) {
+  if (!e || !e->prof) return f();
+  hipEvent_t a = e->event(), b = e->event();
+  if (a) hipEventRecord(a, s);
+  hipError_t r = f();
+  if (b) hipEventRecord(b, s);
+  if (a && b) e->recs.push_back({cls, a, b, flops});
+  return r;
+}
+
+const char* gemm_name(int layout, int epi) {
+  static const char* L[] = {"NT", "NN", "TN"};
+  static const char* E[] = {"store", "gelu", "resid", "gelubwd", "f32"};
+  static std::map<int, std::string> names;
+  const int key = layout * 8 + epi;
+  auto it = names.find(key);
+  if (it == names.end())
+    it = names.emplace(key, std::string("gemm_") + L[layout] + "_" + E[epi]).first;
+  return it->second.c_str();
+}
+
+#define MP_CHECK(expr)                                                              \
+  do {                                                                              \
+    hipError_t _e = (expr);                                                         \
+    if (_e != hipSuccess)                                                           \
+      return fail(MPIPE_ERR_HIP, std::string(#expr) + ": " + hipGetErrorString(_e)); \
+  } while (0)
+
+Cfg to_cfg(const mpipe_encoder_cfg* c) {
+  Cfg o;
+  o.in_chans = c->in_chans;
+  o.patch = c->patch;
+  o.tpatch = c->temporal_patch;
+  o.hidden = c->hidden;
+  o.layers = c->layers;
+  o.heads = c->heads;
+  o.mlp = c->mlp;
+  o.merge = c->merge;
+  o.llm = c->llm_hidden;
+  o.dtype = c->dtype;
+  o.eps = c->ln_eps;
+  o.theta = c->rope_theta;
+  derive_cfg(o);
+  return o;
+}
+
+struct Ctx {
+  mpipe_encoder* e;
+  const Cfg& c;
+  const Plan& P;
+  hipStream_t s;
+  const char* w;   // weights (device)
+  char* ws;        // workspace (device)
+  int dt;
+  int64_t E;
+  const char* W(int i) const { return w + e->params[i].off * E; }
+  float* grad(float* dw, int i) const { return dw + e->params[i].off; }
+};
+
+mpipe_status gemm_call(Ctx& x, int layout, int epi, GemmArgs a) {
+  const double fl = 2.0 * a.M * a.N * (double)a.K;
+  MP_CHECK(run(x.e, x.s, gemm_name(layout, epi), fl, [&] { return gemm(x.dt, layout, epi, a, x.s); }));
+  return MPIPE_OK;
+}
+
+GemmArgs ga(const void* A, int64_t lda, const void* B, int64_t ldb, int64_t M, int64_t N,
+            int64_t K, void* C, int64_t ldc) {
+  GemmArgs a;
+  a.A = A;
+  a.lda = lda;
+  a.B = B;
+  a.ldb = ldb;
+  a.M = (int)M;
+  a.N = (int)N;
+  a.K = (int)K;
+  a.C = C;
+  a.ldc = ldc;
+  return a;
+}
+
+// dW[M][N] (+)= sum_k A[k][m] B[k][n]  (weight gradient, K = tokens)
+mpipe_status dw_gemm(Ctx& x, const void* A, int64_t lda, const void* B, int64_t ldb, int64_t M,
+                     int64_t N, int64_t K, float* out, int64_t ldo) {
+  GemmSplit sp = choose_split(M, N, K);
+  GemmArgs a = ga(A, lda, B, ldb, M, N, K, nullptr, 0);
+  if (sp.splits <= 1) {
+    a.C = out;
+    a.ldc = ldo;
+    a.beta = 1;
+    return gemm_call(x, GEMM_TN, EPI_F32, a);
+  }
+  float* part = reinterpret_cast<float*>(x.ws + x.P.ws_dwpart);
+  a.C = part;
+  a.ldc = N;
+  a.kps = sp.kps;
+  a.split_stride = M * N;
+  mpipe_status st = gemm_call(x, GEMM_TN, EPI_F32, a);
+  if (st) return st;
+  MP_CHECK(run(x.e, x.s, "splitk_reduce", 0, [&] { return splitk_reduce(part, sp.splits, M, N, out, ldo, x.s); }));
+  return MPIPE_OK;
+}
+
+mpipe_status colsum(Ctx& x, int dtype_in, const void* X, int64_t ld, int64_t rows, int n,
+                    float* out) {
+  float* part = reinterpret_cast<float*>(x.ws + x.P.ws_part);
+  MP_CHECK(run(x.e, x.s, "colsum", 0,
+               [&] { return colsum_accumulate(dtype_in, X, ld, rows, n, part, out, x.s); }));
+  return MPIPE_OK;
+}
+
+mpipe_status upload_meta(mpipe_encoder* e, const Plan& P, char* ws, hipStream_t s) {
+  const size_t bytes = P.meta_bytes;
+  if (bytes == 0) return MPIPE_OK;
+  if (e->staging_pending) {
+    MP_CHECK(hipEventSynchronize(e->staging_ev));
+    e->staging_pending = false;
+  }
+  if (bytes > e->staging_cap) {
+    if (e->staging) MP_CHECK(hipHostFree(e->staging));
+    e->staging = nullptr;
+    e->staging_cap = 0;
+    MP_CHECK(hipHostMalloc(&e->staging, bytes, hipHostMallocDefault));
+    e->staging_cap = bytes;
+  }
+  char* st = reinterpret_cast<char*>(e->staging);
+  std::memcpy(st + P.ws_pos, P.pos.data(), P.pos.size() * sizeof(int32_t));
+  std::memcpy(st + P.ws_qwork, P.q_work.data(), P.q_work.size() * sizeof(int32_t));
+  std::memcpy(st + P.ws_kwork, P.k_work.data(), P.k_work.size() * sizeof(int32_t));
+  std::memcpy(st + P.ws_freq, P.freq.data(), P.freq.size() * sizeof(float));
+  MP_CHECK(hipMemcpyAsync(ws, st, bytes, hipMemcpyHostToDevice, s));
+  if (!e->staging_ev) MP_CHECK(hipEventCreateWithFlags(&e->staging_ev, hipEventDisableTiming));
+  MP_CHECK(hipEventRecord(e->staging_ev, s));
+  e->staging_pending = true;
+  return MPIPE_OK;
+}
+
+AttnArgs attn_args(Ctx& x, const char* qkv, bool k_tiles) {
+  const Cfg& c = x.c;
+  AttnArgs a;
+  a.q = qkv;
+  a.k = qkv + (int64_t)c.hidden * x.E;
+  a.v = qkv + 2 * (int64_t)c.hidden * x.E;
+  a.ld = 3 * c.hidden;
+  a.heads = c.heads;
+  a.N = x.P.N;
+  a.scale = 1.0f / std::sqrt((float)c.d);
+  a.work = reinterpret_cast<const int4*>(x.ws + (k_tiles ? x.P.ws_kwork : x.P.ws_qwork));
+  a.n_work = (int)((k_tiles ? x.P.k_work.size() : x.P.q_work.size()) / 4);
+  return a;
+}
+
+// pointers of the padded patch matrix and patch-embedding weight
+void pe_operands(Ctx& x, const void* patches, const void*& Xp, const void*& Wpe, int64_t& ld) {
+  const Cfg& c = x.c;
+  if (c.kp != c.kpe) {
+    Xp = x.ws + x.P.ws_xp;
+    Wpe = x.ws + x.P.ws_wpe;
+    ld = c.kp;
+  } else {
+    Xp = patches;
+    Wpe = x.W(P_PE_W);
+    ld = c.kpe;
+  }
+}
+
+mpipe_status pad_pe(Ctx& x, const void* patches) {
+  const Cfg& c = x.c;
+  if (c.kp == c.kpe) return MPIPE_OK;
+  MP_CHECK(run(x.e, x.s, "pad", 0, [&] { return pad_cols(x.dt, patches, x.P.N, c.kpe, x.ws + x.P.ws_xp, c.kp, x.s); }));
+  MP_CHECK(run(x.e, x.s, "pad", 0, [&] { return pad_cols(x.dt, x.W(P_PE_W), c.hidden, c.kpe, x.ws + x.P.ws_wpe, c.kp, x.s); }));
+  return MPIPE_OK;
+}
+
+#define MP_RET(expr)                  \
+  do {                                \
+    mpipe_status _s = (expr);         \
+    if (_s != MPIPE_OK) return _s;    \
+  } while (0)
+
+mpipe_status forward(Ctx& x, const void* patches, void* merged, char* tape) {
+  const Cfg& c = x.c;
+  const Plan& P = x.P;
+  const int64_t N = P.N, h = c.hidden, m = c.mlp, H = c.llm, E = x.E;
+  const bool tr = P.trainable;
+  char* base = tr ? tape : x.ws;
+  auto act = [&](int l) -> const ActSet& { return tr ? P.tape_act[l] : P.ws_act; };
+  const MergerSet& MS = tr ? P.tape_mrg : P.ws_mrg;
+  const int32_t* pos = reinterpret_cast<const int32_t*>(x.ws + P.ws_pos);
+  const float* freq = reinterpret_cast<const float*>(x.ws + P.ws_freq);
+
+  MP_RET(pad_pe(x, patches));
+  const void *Xp, *Wpe;
+  int64_t ldx;
+  pe_operands(x, patches, Xp, Wpe, ldx);
+  const size_t h0 = c.layers > 0 ? act(0).hin : MS.hfin;
+  {
+    GemmArgs a = ga(Xp, ldx, Wpe, ldx, N, h, c.kp, base + h0, h);
+    a.bias = x.W(P_PE_B);
+    MP_RET(gemm_call(x, GEMM_NT, EPI_RESID, a));
+  }
+  for (int l = 0; l < c.layers; ++l) {
+    const ActSet& S = act(l);
+    float* hin = reinterpret_cast<float*>(base + S.hin);
+    float* hmid = reinterpret_cast<float*>(base + S.hmid);
+    float* hout = reinterpret_cast<float*>(base + (tr ? S.hout : S.hin));
+    char* A = base + S.a;
+    char* qkv = base + S.qkv;
+    char* O = base + S.o;
+    char* B = base + S.b;
+    char* G = base + S.g;
+    MP_CHECK(run(x.e, x.s, "layernorm", 0, [&] {
+      return layernorm_fwd(x.dt, hin, h, N, (int)h, x.W(blk_param(c, l, B_LN1G)),
+                           x.W(blk_param(c, l, B_LN1B)), c.eps, A, h,
+                           reinterpret_cast<float*>(base + S.mean1),
+                           reinterpret_cast<float*>(base + S.rstd1), x.s);
+    }));
+    {
+      GemmArgs a = ga(A, h, x.W(blk_param(c, l, B_QKVW)), h, N, 3 * h, h, qkv, 3 * h);
+      a.bias = x.W(blk_param(c, l, B_QKVB));
+      MP_RET(gemm_call(x, GEMM_NT, EPI_STORE, a));
+    }
+    MP_CHECK(run(x.e, x.s, "rope", 0, [&] {
+      return rope(x.dt, qkv, 3 * h, N, c.heads, c.d, (int)h, pos, freq, 0, x.s);
+    }));
+    {
+      AttnArgs a = attn_args(x, qkv, false);
+      a.out = O;
+      a.ldo = h;
+      a.lse = reinterpret_cast<float*>(base + S.lse);
+      const double fl = 4.0 * c.heads * c.d * (double)P.sum_len2;
+      MP_CHECK(run(x.e, x.s, "attn_fwd", fl, [&] { return attention_fwd(x.dt, c.d, a, x.s); }));
+    }
+    {
+      GemmArgs a = ga(O, h, x.W(blk_param(c, l, B_PROJW)), h, N, h, h, hmid, h);
+      a.bias = x.W(blk_param(c, l, B_PROJB));
+      a.aux = hin;
+      a.ld_aux = h;
+      MP_RET(gemm_call(x, GEMM_NT, EPI_RESID, a));
+    }
+    MP_CHECK(run(x.e, x.s, "layernorm", 0, [&] {
+      return layernorm_fwd(x.dt, hmid, h, N, (int)h, x.W(blk_param(c, l, B_LN2G)),
+                           x.W(blk_param(c, l, B_LN2B)), c.eps, B, h,
+                           reinterpret_cast<float*>(base + S.mean2),
+                           reinterpret_cast<float*>(base + S.rstd2), x.s);
+    }));
+    {
+      GemmArgs a = ga(B, h, x.W(blk_param(c, l, B_FC1W)), h, N, m, h, G, m);
+      a.bias = x.W(blk_param(c, l, B_FC1B));
+      a.C2 = tr ? base + S.u : nullptr;
+      a.ldc2 = m;
+      MP_RET(gemm_call(x, GEMM_NT, EPI_GELU, a));
+    }
+    {
+      GemmArgs a = ga(G, m, x.W(blk_param(c, l, B_FC2W)), m, N, h, m, hout, h);
+      a.bias = x.W(blk_param(c, l, B_FC2B));
+      a.aux = hmid;
+      a.ld_aux = h;
+      MP_RET(gemm_call(x, GEMM_NT, EPI_RESID, a));
+    }
+  }
+  // 2x2 merger: LN, the four window rows side by side ([Tm][4h] view), fc1+GELU, fc2
+  char* Z = base + MS.z;
+  char* Gm = base + MS.gm;
+  MP_CHECK(run(x.e, x.s, "layernorm", 0, [&] {
+    return layernorm_fwd(x.dt, reinterpret_cast<float*>(base + MS.hfin), h, N, (int)h,
+                         x.W(merger_param(c, M_LNG)), x.W(merger_param(c, M_LNB)), c.eps, Z, h,
+                         reinterpret_cast<float*>(base + MS.meanz),
+                         reinterpret_cast<float*>(base + MS.rstdz), x.s);
+  }));
+  {
+    GemmArgs a = ga(Z, 4 * h, x.W(merger_param(c, M_FC1W)), 4 * h, P.Tm, 4 * h, 4 * h, Gm, 4 * h);
+    a.bias = x.W(merger_param(c, M_FC1B));
+    a.C2 = tr ? base + MS.um : nullptr;
+    a.ldc2 = 4 * h;
+    MP_RET(gemm_call(x, GEMM_NT, EPI_GELU, a));
+  }
+  {
+    GemmArgs a = ga(Gm, 4 * h, x.W(merger_param(c, M_FC2W)), 4 * h, P.Tm, H, 4 * h, merged, H);
+    a.bias = x.W(merger_param(c, M_FC2B));
+    MP_RET(gemm_call(x, GEMM_NT, EPI_STORE, a));
+  }
+  (void)E;
+  return MPIPE_OK;
+}
+
+mpipe_status backward(Ctx& x, const void* patches, const char* tape, const void* dM, float* dw,
+                      void* d_patches) {
+  const Cfg& c = x.c;
+  const Plan& P = x.P;
+  const int64_t N = P.N, Tm = P.Tm, h = c.hidden, m = c.mlp, H = c.llm;
+  const char* base = tape;
+  const MergerSet& MS = P.tape_mrg;
+  const int32_t* pos = reinterpret_cast<const int32_t*>(x.ws + P.ws_pos);
+  const float* freq = reinterpret_cast<const float*>(x.ws + P.ws_freq);
+  float* dh = reinterpret_cast<float*>(x.ws + P.ws_dh);
+  char* dht = x.ws + P.ws_dht;
+  float* dhm = reinterpret_cast<float*>(x.ws + P.ws_dhm);
+  char* dhmt = x.ws + P.ws_dhmt;
+  float* dx32 = reinterpret_cast<float*>(x.ws + P.ws_dx32);
+  char* du = x.ws + P.ws_du;
+  char* dO = x.ws + P.ws_do;
+  float* delta = reinterpret_cast<float*>(x.ws + P.ws_delta);
+  char* dqkv = x.ws + P.ws_dqkv;
+  float* part = reinterpret_cast<float*>(x.ws + P.ws_part);
+  const int64_t part_half = ((N + 63) / 64 * 4) * std::max({3 * h, m, 4 * h, H, (int64_t)c.kpe});
+
+  MP_RET(pad_pe(x, patches));
+  const void *Xp, *Wpe;
+  int64_t ldx;
+  pe_operands(x, patches, Xp, Wpe, ldx);
+
+  // merger
+  {
+    GemmArgs a = ga(dM, H, x.W(merger_param(c, M_FC2W)), 4 * h, Tm, 4 * h, H, du, 4 * h);
+    a.aux = base + MS.um;
+    a.ld_aux = 4 * h;
+    MP_RET(gemm_call(x, GEMM_NN, EPI_GELU_BWD, a));
+  }
+  MP_RET(dw_gemm(x, dM, H, base + MS.gm, 4 * h, H, 4 * h, Tm, x.grad(dw, merger_param(c, M_FC2W)), 4 * h));
+  MP_RET(colsum(x, x.dt, dM, H, Tm, (int)H, x.grad(dw, merger_param(c, M_FC2B))));
+  {
+    GemmArgs a = ga(du, 4 * h, x.W(merger_param(c, M_FC1W)), 4 * h, Tm, 4 * h, 4 * h, dx32, 4 * h);
+    MP_RET(gemm_call(x, GEMM_NN, EPI_F32, a));
+  }
+  MP_RET(dw_gemm(x, du, 4 * h, base + MS.z, 4 * h, 4 * h, 4 * h, Tm, x.grad(dw, merger_param(c, M_FC1W)), 4 * h));
+  MP_RET(colsum(x, x.dt, du, 4 * h, Tm, (int)(4 * h), x.grad(dw, merger_param(c, M_FC1B))));
+  MP_CHECK(run(x.e, x.s, "layernorm_bwd", 0, [&] {
+    return layernorm_bwd(x.dt, dx32, h, reinterpret_cast<const float*>(base + MS.hfin), h,
+                         reinterpret_cast<const float*>(base + MS.meanz),
+                         reinterpret_cast<const float*>(base + MS.rstdz),
+                         x.W(merger_param(c, M_LNG)), N, (int)h, nullptr, dh, dht, part,
+                         part + part_half, x.grad(dw, merger_param(c, M_LNG)),
+                         x.grad(dw, merger_param(c, M_LNB)), x.s);
+  }));
+
+  for (int l = c.layers - 1; l >= 0; --l) {
+    const ActSet& S = P.tape_act[l];
+    const float* hin = reinterpret_cast<const float*>(base + S.hin);
+    const float* hmid = reinterpret_cast<const float*>(base + S.hmid);
+    // MLP: H_out = H_mid + GELU(B W1^T + b1) W2^T + b2
+    {
+      GemmArgs a = ga(dht, h, x.W(blk_param(c, l, B_FC2W)), m, N, m, h, du, m);
+      a.aux = base + S.u;
+      a.ld_aux = m;
+      MP_RET(gemm_call(x, GEMM_NN, EPI_GELU_BWD, a));
+    }
+    MP_RET(dw_gemm(x, dht, h, base + S.g, m, h, m, N, x.grad(dw, blk_param(c, l, B_FC2W)), m));
+    MP_RET(colsum(x, DT_F32, dh, h, N, (int)h, x.grad(dw, blk_param(c, l, B_FC2B))));
+    {
+      GemmArgs a = ga(du, m, x.W(blk_param(c, l, B_FC1W)), h, N, h, m, dx32, h);
+      MP_RET(gemm_call(x, GEMM_NN, EPI_F32, a));
+    }
+    MP_RET(dw_gemm(x, du, m, base + S.b, h, m, h, N, x.grad(dw, blk_param(c, l, B_FC1W)), h));
+    MP_RET(colsum(x, x.dt, du, m, N, (int)m, x.grad(dw, blk_param(c, l, B_FC1B))));
+    MP_CHECK(run(x.e, x.s, "layernorm_bwd", 0, [&] {
+      return layernorm_bwd(x.dt, dx32, h, hmid, h, reinterpret_cast<const float*>(base + S.mean2),
+                           reinterpret_cast<const float*>(base + S.rstd2),
+                           x.W(blk_param(c, l, B_LN2G)), N, (int)h, dh, dhm, dhmt, part,
+                           part + part_half, x.grad(dw, blk_param(c, l, B_LN2G)),
+                           x.grad(dw, blk_param(c, l, B_LN2B)), x.s);
+    }));
+    // attention: H_mid = H_in + O Wo^T + bo
+    {
+      GemmArgs a = ga(dhmt, h, x.W(blk_param(c, l, B_PROJW)), h, N, h, h, dO, h);
+      MP_RET(gemm_call(x, GEMM_NN, EPI_STORE, a));
+    }
+    MP_RET(dw_gemm(x, dhmt, h, base + S.o, h, h, h, N, x.grad(dw, blk_param(c, l, B_PROJW)), h));
+    MP_RET(colsum(x, DT_F32, dhm, h, N, (int)h, x.grad(dw, blk_param(c, l, B_PROJB))));
+    MP_CHECK(run(x.e, x.s, "attn_delta", 0, [&] {
+      return attention_delta(x.dt, base + S.o, dO, h, N, c.heads, c.d, delta, x.s);
+    }));
+    {
+      const char* qkv = base + S.qkv;
+      AttnArgs qa = attn_args(x, qkv, false), ka = attn_args(x, qkv, true);
+      for (AttnArgs* a : {&qa, &ka}) {
+        a->o = base + S.o;
+        a->d_o = dO;
+        a->ldo = h;
+        a->lse = const_cast<float*>(reinterpret_cast<const float*>(base + S.lse));
+        a->delta = delta;
+        a->dq = dqkv;
+        a->dk = dqkv + h * x.E;
+        a->dv = dqkv + 2 * h * x.E;
+        a->ldd = 3 * h;
+      }
+      const double f = 2.0 * c.heads * c.d * (double)P.sum_len2;
+      MP_CHECK(run(x.e, x.s, "attn_bwd_dq", f, [&] { return attention_bwd_dq(x.dt, c.d, qa, x.s); }));
+      MP_CHECK(run(x.e, x.s, "attn_bwd_dkdv", 3 * f, [&] { return attention_bwd_dkdv(x.dt, c.d, ka, x.s); }));
+    }
+    MP_CHECK(run(x.e, x.s, "rope", 0, [&] {
+      return rope(x.dt, dqkv, 3 * h, N, c.heads, c.d, (int)h, pos, freq, 1, x.s);
+    }));
+    {
+      GemmArgs a = ga(dqkv, 3 * h, x.W(blk_param(c, l, B_QKVW)), h, N, h, 3 * h, dx32, h);
+      MP_RET(gemm_call(x, GEMM_NN, EPI_F32, a));
+    }
+    MP_RET(dw_gemm(x, dqkv, 3 * h, base + S.a, h, 3 * h, h, N, x.grad(dw, blk_param(c, l, B_QKVW)), h));
+    MP_RET(colsum(x, x.dt, dqkv, 3 * h, N, (int)(3 * h), x.grad(dw, blk_param(c, l, B_QKVB))));
+    MP_CHECK(run(x.e, x.s, "layernorm_bwd", 0, [&] {
+      return layernorm_bwd(x.dt, dx32, h, hin, h, reinterpret_cast<const float*>(base + S.mean1),
+                           reinterpret_cast<const float*>(base + S.rstd1),
+                           x.W(blk_param(c, l, B_LN1G)), N, (int)h, dhm, dh, dht, part,
+                           part + part_half, x.grad(dw, blk_param(c, l, B_LN1G)),
+                           x.grad(dw, blk_param(c, l, B_LN1B)), x.s);
+    }));
+  }
+  // patch embedding (the trainable source: nothing goes upstream unless asked)
+  MP_RET(dw_gemm(x, dht, h, Xp, ldx, h, c.kpe, N, x.grad(dw, P_PE_W), c.kpe));
+  MP_RET(colsum(x, DT_F32, dh, h, N, (int)h, x.grad(dw, P_PE_B)));
+  if (d_patches) {
+    GemmArgs a = ga(dht, h, Wpe, ldx, N, c.kpe, h, d_patches, c.kpe);
+    MP_RET(gemm_call(x, GEMM_NN, EPI_STORE, a));
+  }
+  return MPIPE_OK;
+}
+
+mpipe_status check_handle(const mpipe_encoder* e) {
+  if (!e) return fail(MPIPE_ERR_INVALID_ARG, "null encoder handle");
+  return MPIPE_OK;
+}
+
+}  // namespace
+
+// =====================================================================================
+// C ABI
+// =====================================================================================
+extern "C" {
+
+mpipe_status mpipe_encoder_create(const mpipe_encoder_cfg* cfg, mpipe_encoder** out) {
+  if (!cfg || !out) return fail(MPIPE_ERR_INVALID_ARG, "null argument");
+  Cfg c = to_cfg(cfg);
+  const std::string why = check_cfg(c);
+  if (!why.empty()) return fail(MPIPE_ERR_UNSUPPORTED, why);
+  mpipe_encoder* e = new mpipe_encoder();
+  e->cfg = c;
+  e->params = param_table(c);
+  *out = e;
+  return MPIPE_OK;
+}
+
+void mpipe_encoder_destroy(mpipe_encoder* e) {
+  if (!e) return;
+  if (e->staging_pending && e->staging_ev) hipEventSynchronize(e->staging_ev);
+  if (e->staging) hipHostFree(e->staging);
+  if (e->staging_ev) hipEventDestroy(e->staging_ev);
+  for (auto& r : e->recs) {
+    hipEventDestroy(r.a);
+    hipEventDestroy(r.b);
+  }
+  for (auto ev : e->pool) hipEventDestroy(ev);
+  delete e;
+}
+
+int64_t mpipe_param_count(const mpipe_encoder_cfg* cfg) {
+  if (!cfg) return -1;
+  Cfg c = to_cfg(cfg);
+  auto t = param_table(c);
+  return t.empty() ? 0 : t.back().off + t.back().rows * t.back().cols;
+}
+
+int32_t mpipe_param_tensors(const mpipe_encoder_cfg* cfg) {
+  if (!cfg) return -1;
+  return (int32_t)param_table(to_cfg(cfg)).size();
+}
+
+mpipe_status mpipe_param_info(const mpipe_encoder_cfg* cfg, int32_t i, char* name, int32_t cap,
+                              int64_t* offset, int64_t* rows, int64_t* cols) {
+  if (!cfg) return fail(MPIPE_ERR_INVALID_ARG, "null cfg");
+  auto t = param_table(to_cfg(cfg));
+  if (i < 0 || i >= (int32_t)t.size()) return fail(MPIPE_ERR_INVALID_ARG, "tensor index out of range");
+  if (name && cap > 0) {
+    std::strncpy(name, t[i].name.c_str(), (size_t)cap - 1);
+    name[cap - 1] = 0;
+  }
+  if (offset) *offset = t[i].off;
+  if (rows) *rows = t[i].rows;
+  if (cols) *cols = t[i].cols;
+  return MPIPE_OK;
+}
+
+mpipe_status mpipe_encoder_sizes(const mpipe_encoder* e, const int32_t* cu, int32_t n_seg,
+                                 const int32_t* thw, int32_t n_items, int32_t trainable,
+                                 size_t* ws_bytes, size_t* tape_bytes, int64_t* n_merged,
+                                 int64_t* n_patches) {
+  MP_RET(check_handle(e));
+  Plan P;
+  std::string err;
+  const int rc = build_plan(e->cfg, cu, n_seg, thw, n_items, trainable != 0, P, err);
+  if (rc) return fail((mpipe_status)rc, err);
+  if (ws_bytes) *ws_bytes = P.ws_bytes;
+  if (tape_bytes) *tape_bytes = P.tape_bytes;
+  if (n_merged) *n_merged = P.Tm;
+  if (n_patches) *n_patches = P.N;
+  return MPIPE_OK;
+}
+
+mpipe_status mpipe_encoder_fwd(mpipe_encoder* e, const void* weights, const void* patches,
+                               const int32_t* cu, int32_t n_seg, const int32_t* thw,
+                               int32_t n_items, int32_t trainable, void* merged, void* tape,
+                               size_t tape_bytes, void* ws, size_t ws_bytes, void* stream) {
+  MP_RET(check_handle(e));
+  Plan P;
+  std::string err;
+  const int rc = build_plan(e->cfg, cu, n_seg, thw, n_items, trainable != 0, P, err);
+  if (rc) return fail((mpipe_status)rc, err);
+  if (P.N == 0) return MPIPE_OK;
+  if (!weights || !patches || !merged) return fail(MPIPE_ERR_INVALID_ARG, "null device buffer");
+  if (!ws || ws_bytes < P.ws_bytes)
+    return fail(MPIPE_ERR_WORKSPACE, "workspace needs " + std::to_string(P.ws_bytes) + " bytes");
+  if (trainable && (!tape || tape_bytes < P.tape_bytes))
+    return fail(MPIPE_ERR_NO_TAPE, "trainable forward needs a tape of " +
+                                       std::to_string(P.tape_bytes) + " bytes");
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  MP_RET(upload_meta(e, P, reinterpret_cast<char*>(ws), s));
+  Ctx x{e, e->cfg, P, s, reinterpret_cast<const char*>(weights), reinterpret_cast<char*>(ws),
+        e->cfg.dtype, e->cfg.esz};
+  return forward(x, patches, merged, reinterpret_cast<char*>(tape));
+}
+
+mpipe_status mpipe_encoder_bwd(mpipe_encoder* e, const void* weights, const void* patches,
+                               const int32_t* cu, int32_t n_seg, const int32_t* thw,
+                               int32_t n_items, int32_t trainable, const void* tape,
+                               size_t tape_bytes, const void* d_merged, float* d_weights,
+                               void* d_patches, void* ws, size_t ws_bytes, void* stream) {
+  MP_RET(check_handle(e));
+  if (!trainable) return fail(MPIPE_NOOP_FROZEN, "frozen encoder: no backward (Lemma 1)");
+  Plan P;
+  std::string err;
+  const int rc = build_plan(e->cfg, cu, n_seg, thw, n_items, true, P, err);
+  if (rc) return fail((mpipe_status)rc, err);
+  if (P.N == 0) return MPIPE_OK;
+  if (!weights || !patches || !d_merged || !d_weights)
+    return fail(MPIPE_ERR_INVALID_ARG, "null device buffer");
+  if (!tape || tape_bytes < P.tape_bytes)
+    return fail(MPIPE_ERR_NO_TAPE, "backward needs the forward's tape of " +
+                                       std::to_string(P.tape_bytes) + " bytes");
+  if (!ws || ws_bytes < P.ws_bytes)
+    return fail(MPIPE_ERR_WORKSPACE, "workspace needs " + std::to_string(P.ws_bytes) + " bytes");
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  MP_RET(upload_meta(e, P, reinterpret_cast<char*>(ws), s));
+  Ctx x{e, e->cfg, P, s, reinterpret_cast<const char*>(weights), reinterpret_cast<char*>(ws),
+        e->cfg.dtype, e->cfg.esz};
+  return backward(x, patches, reinterpret_cast<const char*>(tape), d_merged, d_weights, d_patches);
+}
+
+static mpipe_status rows_common(int32_t row_elems, int32_t dtype, int64_t n_merged, int64_t n_rows,
+                                const void* a, const void* b, const int64_t* idx) {
+  if (dtype != MPIPE_F32 && dtype != MPIPE_BF16) return fail(MPIPE_ERR_INVALID_ARG, "bad dtype");
+  if (row_elems <= 0 || n_merged < 0 || n_rows < 0)
+    return fail(MPIPE_ERR_INVALID_ARG, "negative size");
+  if (n_merged > 0 && (!a || !b || !idx)) return fail(MPIPE_ERR_INVALID_ARG, "null device buffer");
+  return MPIPE_OK;
+}
+
+mpipe_status mpipe_merge_scatter(const void* merged, int64_t n_merged, int32_t row_elems,
+                                 int32_t dtype, const int64_t* idx, void* embeds, int64_t n_rows,
+                                 void* stream) {
+  MP_RET(rows_common(row_elems, dtype, n_merged, n_rows, merged, embeds, idx));
+  const int64_t rb = (int64_t)row_elems * (dtype == MPIPE_BF16 ? 2 : 4);
+  MP_CHECK(rows_copy(true, merged, embeds, idx, n_merged, rb, n_rows,
+                     reinterpret_cast<hipStream_t>(stream)));
+  return MPIPE_OK;
+}
+
+mpipe_status mpipe_merge_gather(const void* d_embeds, int64_t n_rows, int32_t row_elems,
+                                int32_t dtype, const int64_t* idx, int64_t n_merged,
+                                void* d_merged, void* stream) {
+  MP_RET(rows_common(row_elems, dtype, n_merged, n_rows, d_embeds, d_merged, idx));
+  const int64_t rb = (int64_t)row_elems * (dtype == MPIPE_BF16 ? 2 : 4);
+  MP_CHECK(rows_copy(false, d_embeds, d_merged, idx, n_merged, rb, n_rows,
+                     reinterpret_cast<hipStream_t>(stream)));
+  return MPIPE_OK;
+}
+
+mpipe_status mpipe_merge_check_indices(const int64_t* idx, int64_t n_merged, int64_t n_rows,
+                                       int32_t* marks, int32_t* status, void* stream) {
+  if (n_merged < 0 || n_rows < 0) return fail(MPIPE_ERR_INVALID_ARG, "negative size");
+  if (!status || (n_rows > 0 && !marks) || (n_merged > 0 && !idx))
+    return fail(MPIPE_ERR_INVALID_ARG, "null device buffer");
+  MP_CHECK(check_indices(idx, n_merged, n_rows, marks, status, reinterpret_cast<hipStream_t>(stream)));
+  return MPIPE_OK;
+}
+
+const char* mpipe_last_error(void) { return g_err.c_str(); }
+
+mpipe_status mpipe_profile_enable(mpipe_encoder* e, int32_t enable) {
+  MP_RET(check_handle(e));
+  e->prof = enable != 0;
+  return MPIPE_OK;
+}
+
+int32_t mpipe_profile_read(mpipe_encoder* e, void* stream, int32_t cap, char* names,
+                           int32_t name_stride, int64_t* launches, double* ms, double* flops) {
+  if (!e) return -1;
+  if (hipStreamSynchronize(reinterpret_cast<hipStream_t>(stream)) != hipSuccess) return -1;
+  std::map<std::string, std::tuple<int64_t, double, double>> agg;
+  for (auto& r : e->recs) {
+    float t = 0.f;
+    hipEventElapsedTime(&t, r.a, r.b);
+    auto& v = agg[r.cls];
+    std::get<0>(v) += 1;
+    std::get<1>(v) += t;
+    std::get<2>(v) += r.flops;
+    e->pool.push_back(r.a);
+    e->pool.push_back(r.b);
+  }
+  e->recs.clear();
+  int32_t n = 0;
+  for (auto& kv : agg) {
+    if (n >= cap) break;
+    if (names && name_stride > 0) {
+      std::strncpy(names + (size_t)n * name_stride, kv.first.c_str(), (size_t)name_stride - 1);
+      names[(size_t)n * name_stride + name_stride - 1] = 0;
+    }
+    if (launches) launches[n] = std::get<0>(kv.second);
+    if (ms) ms[n] = std::get<1>(kv.second);
+    if (flops) flops[n] = std::get<2>(kv.second);
+    ++n;
+  }
+  return n;
+}
+
+}  // extern "C"

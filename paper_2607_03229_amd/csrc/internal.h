@@ -1,0 +1,91 @@
+// Internal launch interface between the host sequencer and the gfx950 kernels.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace mpipe {
+
+enum { DT_F32 = 0, DT_BF16 = 1 };
+enum { GEMM_NT = 0, GEMM_NN = 1, GEMM_TN = 2 };
+enum { EPI_STORE = 0, EPI_GELU = 1, EPI_RESID = 2, EPI_GELU_BWD = 3, EPI_F32 = 4 };
+constexpr int ATTN_TILE = 128;   // queries (forward, dQ) or keys (dK/dV) per attention work item
+
+// C[m][n] = sum_k A(m,k) B(n,k) + epilogue.
+//   NT: A[m*lda + k], B[n*ldb + k];  NN: A[m*lda + k], B[k*ldb + n];  TN: A[k*lda + m], B[k*ldb + n]
+//   kps: K range per split (multiple of the K step; <= 0 means no split); split s
+//        covers [s*kps, (s+1)*kps) and writes C + s*split_stride (EPI_F32 only).
+//   EPI_STORE     C(T)   = acc + bias
+//   EPI_GELU      C2(T)  = acc + bias (pre-activation, optional), C(T) = GELU(that)
+//   EPI_RESID     C(f32) = aux(f32, may alias C, may be null) + acc + bias
+//   EPI_GELU_BWD  C(T)   = acc * GELU'(aux(T))
+//   EPI_F32       C(f32) = acc (+ C if beta)
+struct GemmArgs {
+  const void* A = nullptr;
+  const void* B = nullptr;
+  int64_t lda = 0, ldb = 0;
+  int M = 0, N = 0, K = 0, kps = 0;
+  int tiles_m = 0, tiles_n = 0;
+  void* C = nullptr;
+  int64_t ldc = 0, split_stride = 0;
+  const void* bias = nullptr;
+  const void* aux = nullptr;
+  int64_t ld_aux = 0;
+  void* C2 = nullptr;
+  int64_t ldc2 = 0;
+  int beta = 0;
+};
+hipError_t gemm(int dtype, int layout, int epi, const GemmArgs& a, hipStream_t s);
+
+struct AttnArgs {
+  const void* q = nullptr;     // Q, K, V column blocks, row stride ld (head h at column h*d)
+  const void* k = nullptr;
+  const void* v = nullptr;
+  int64_t ld = 0;
+  const void* o = nullptr;     // O and dO, row stride ldo
+  const void* d_o = nullptr;
+  int64_t ldo = 0;
+  void* out = nullptr;         // forward output O (row stride ldo)
+  void* dq = nullptr;          // backward outputs, row stride ldd
+  void* dk = nullptr;
+  void* dv = nullptr;
+  int64_t ldd = 0;
+  float* lse = nullptr;        // [heads][N], natural log
+  const float* delta = nullptr;  // [heads][N]
+  const int4* work = nullptr;  // (tile start row, segment start, segment end, 0)
+  int n_work = 0;
+  int heads = 0;
+  int64_t N = 0;
+  float scale = 0.f;
+};
+bool attention_supported(int dtype, int head_dim);
+hipError_t attention_fwd(int dtype, int head_dim, const AttnArgs& a, hipStream_t s);
+// dQ over query tiles (work = query tiles); dK, dV over key tiles (work = key tiles)
+hipError_t attention_bwd_dq(int dtype, int head_dim, const AttnArgs& a, hipStream_t s);
+hipError_t attention_bwd_dkdv(int dtype, int head_dim, const AttnArgs& a, hipStream_t s);
+hipError_t attention_delta(int dtype, const void* O, const void* dO, int64_t ldo, int64_t N,
+                           int heads, int d, float* delta, hipStream_t s);
+
+hipError_t layernorm_fwd(int dtype, const float* X, int64_t ldx, int64_t rows, int n,
+                         const void* g, const void* b, float eps, void* Y, int64_t ldy,
+                         float* mean, float* rstd, hipStream_t s);
+int64_t layernorm_bwd_partial_rows(int64_t rows);
+// dX, dres and dXt use the row stride ldx of X.
+hipError_t layernorm_bwd(int dtype, const float* dY, int64_t ldd, const float* X, int64_t ldx,
+                         const float* mean, const float* rstd, const void* g, int64_t rows, int n,
+                         const float* dres, float* dX, void* dXt, float* part_g, float* part_b,
+                         float* grad_g, float* grad_b, hipStream_t s);
+int64_t colsum_partial_rows(int64_t rows);
+hipError_t colsum_accumulate(int dtype_in, const void* X, int64_t ld, int64_t rows, int n,
+                             float* part, float* out, hipStream_t s);
+hipError_t splitk_reduce(const float* part, int splits, int64_t M, int64_t N, float* out,
+                         int64_t ldo, hipStream_t s);
+hipError_t pad_cols(int dtype, const void* src, int64_t rows, int K, void* dst, int Kp,
+                    hipStream_t s);
+hipError_t rope(int dtype, void* qk, int64_t ld, int64_t rows, int heads, int d, int kcol,
+                const int32_t* pos, const float* freq, int inverse, hipStream_t s);
+hipError_t rows_copy(bool scatter, const void* src, void* dst, const int64_t* idx, int64_t n_idx,
+                     int64_t row_bytes, int64_t n_rows, hipStream_t s);
+hipError_t check_indices(const int64_t* idx, int64_t n, int64_t n_rows, int32_t* marks,
+                         int32_t* status, hipStream_t s);
+
+}  // namespace mpipe

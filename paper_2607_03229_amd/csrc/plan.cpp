@@ -1,0 +1,312 @@
+// Host planner for one micro-batch (see plan.h).
+#include "plan.h"
+
+#include <algorithm>
+#include <cmath>
+#include <numeric>
+
+namespace mpipe {
+
+namespace {
+constexpr int kTile = 128;      // attention rows per work item (matches ATTN_TILE)
+constexpr size_t kAlign = 256;
+
+struct Arena {
+  size_t top = 0;
+  size_t take(size_t bytes) {
+    const size_t off = (top + kAlign - 1) / kAlign * kAlign;
+    top = off + bytes;
+    return off;
+  }
+};
+}  // namespace
+
+void derive_cfg(Cfg& c) {
+  c.d = c.heads > 0 ? c.hidden / c.heads : 0;
+  c.kpe = c.in_chans * c.tpatch * c.patch * c.patch;
+  c.kp = (c.kpe + 63) / 64 * 64;
+  c.esz = c.dtype == 1 ? 2 : 4;
+}
+
+std::string check_cfg(const Cfg& c) {
+  if (c.in_chans <= 0 || c.patch <= 0 || c.tpatch <= 0 || c.layers < 0 || c.heads <= 0)
+    return "sizes must be positive";
+  if (c.dtype != 0 && c.dtype != 1) return "dtype must be MPIPE_F32 or MPIPE_BF16";
+  if (c.merge != 2) return "only the 2x2 spatial merge is supported";
+  if (c.hidden <= 0 || c.hidden % 64 || c.hidden > 2048) return "hidden must be a multiple of 64, <= 2048";
+  if (c.hidden % c.heads) return "hidden must be divisible by heads";
+  const int d = c.hidden / c.heads;
+  if (d != 32 && d != 64 && d != 80) return "head_dim must be 32, 64 or 80";
+  if (c.mlp <= 0 || c.mlp % 8) return "mlp must be a positive multiple of 8";
+  if (c.llm <= 0 || c.llm % 8) return "llm_hidden must be a positive multiple of 8";
+  if (!(c.eps > 0.f) || !(c.theta > 0.f)) return "ln_eps and rope_theta must be positive";
+  return "";
+}
+
+std::vector<ParamEntry> param_table(const Cfg& c) {
+  const int64_t h = c.hidden, m = c.mlp, H = c.llm, mh = 4 * h;
+  std::vector<ParamEntry> t;
+  int64_t off = 0;
+  auto add = [&](const std::string& n, int64_t r, int64_t cc) {
+    t.push_back({n, off, r, cc});
+    off += r * cc;
+  };
+  add("pe.w", h, c.kpe);
+  add("pe.b", h, 1);
+  for (int l = 0; l < c.layers; ++l) {
+    const std::string p = "blk" + std::to_string(l) + ".";
+    add(p + "ln1.g", h, 1);
+    add(p + "ln1.b", h, 1);
+    add(p + "qkv.w", 3 * h, h);
+    add(p + "qkv.b", 3 * h, 1);
+    add(p + "proj.w", h, h);
+    add(p + "proj.b", h, 1);
+    add(p + "ln2.g", h, 1);
+    add(p + "ln2.b", h, 1);
+    add(p + "fc1.w", m, h);
+    add(p + "fc1.b", m, 1);
+    add(p + "fc2.w", h, m);
+    add(p + "fc2.b", h, 1);
+  }
+  add("merger.ln.g", h, 1);
+  add("merger.ln.b", h, 1);
+  add("merger.fc1.w", mh, mh);
+  add("merger.fc1.b", mh, 1);
+  add("merger.fc2.w", H, mh);
+  add("merger.fc2.b", H, 1);
+  return t;
+}
+
+GemmSplit choose_split(int64_t M, int64_t N, int64_t K) {
+  // weight-gradient GEMMs have few output tiles and a long K (tokens): split K
+  // until there are about 1024 blocks, keeping each split >= 1024 rows of K.
+  const int64_t tiles = ((M + 127) / 128) * ((N + 127) / 128);
+  int64_t s = std::max<int64_t>(1, (1024 + tiles - 1) / tiles);
+  s = std::min<int64_t>(s, std::max<int64_t>(1, K / 1024));
+  s = std::min<int64_t>(s, 16);
+  GemmSplit g;
+  if (s <= 1) {
+    g.splits = 1;
+    g.kps = 0;
+    return g;
+  }
+  int64_t kps = (K + s - 1) / s;
+  kps = (kps + 63) / 64 * 64;
+  g.kps = (int)kps;
+  g.splits = (int)((K + kps - 1) / kps);
+  if (g.splits <= 1) {
+    g.splits = 1;
+    g.kps = 0;
+  }
+  return g;
+}
+
+int build_plan(const Cfg& c, const int32_t* cu, int n_seg, const int32_t* thw, int n_items,
+               bool trainable, Plan& p, std::string& err) {
+  p = Plan();
+  p.trainable = trainable;
+  if (n_items < 0 || n_seg < 0) {
+    err = "negative item or segment count";
+    return -1;
+  }
+  if (n_items > 0 && (!thw || !cu)) {
+    err = "grid_thw and cu_seqlens are required";
+    return -1;
+  }
+  // items
+  std::vector<int64_t> start(n_items + 1, 0);
+  int64_t N = 0, Tm = 0;
+  for (int i = 0; i < n_items; ++i) {
+    const int t = thw[3 * i], gh = thw[3 * i + 1], gw = thw[3 * i + 2];
+    if (t <= 0 || gh <= 0 || gw <= 0) {
+      err = "grid_thw entries must be positive (item " + std::to_string(i) + ")";
+      return -2;
+    }
+    if (gh % 2 || gw % 2) {
+      err = "grid height and width must be even for the 2x2 merge (item " + std::to_string(i) + ")";
+      return -2;
+    }
+    if (gh > 65534 || gw > 65534) {
+      err = "grid too large";
+      return -2;
+    }
+    start[i] = N;
+    N += (int64_t)t * gh * gw;
+    Tm += (int64_t)t * (gh / 2) * (gw / 2);
+  }
+  start[n_items] = N;
+  if (N > (int64_t)INT32_MAX / 4) {
+    err = "too many patches";
+    return -2;
+  }
+  p.N = N;
+  p.Tm = Tm;
+  p.n_items = n_items;
+  p.n_seg = n_seg;
+  if (n_items == 0) {
+    if (n_seg != 0 && !(cu && cu[n_seg] == 0)) {
+      err = "segments given for an empty micro-batch";
+      return -2;
+    }
+    p.n_seg = 0;
+    return 0;
+  }
+  if (n_seg <= 0 || cu[0] != 0 || cu[n_seg] != N) {
+    err = "cu_seqlens must start at 0 and end at the packed row count " + std::to_string(N);
+    return -2;
+  }
+  int it = 0;
+  for (int s = 0; s < n_seg; ++s) {
+    if (cu[s + 1] <= cu[s]) {
+      err = "cu_seqlens must be strictly increasing (segment " + std::to_string(s) + ")";
+      return -2;
+    }
+    while (it < n_items && cu[s] >= start[it + 1]) ++it;
+    if (it >= n_items || cu[s + 1] > start[it + 1]) {
+      err = "segment " + std::to_string(s) + " crosses an item boundary";
+      return -2;
+    }
+    const int64_t slice = (int64_t)thw[3 * it + 1] * thw[3 * it + 2];
+    if ((cu[s] - start[it]) % slice || (cu[s + 1] - start[it]) % slice) {
+      err = "segment " + std::to_string(s) + " does not start/end on a temporal slice";
+      return -2;
+    }
+  }
+
+  // positions (inverse of the window-major row order)
+  p.pos.resize(N);
+  for (int i = 0; i < n_items; ++i) {
+    const int gh = thw[3 * i + 1], gw = thw[3 * i + 2];
+    const int64_t n = start[i + 1] - start[i];
+    const int wpr = gw / 2, wpc = gh / 2;
+    for (int64_t r = 0; r < n; ++r) {
+      const int64_t w = r >> 2;
+      const int dh = (int)((r >> 1) & 1), dw = (int)(r & 1);
+      const int wb = (int)(w % wpr);
+      const int hb = (int)((w / wpr) % wpc);
+      p.pos[start[i] + r] = ((2 * hb + dh) << 16) | (2 * wb + dw);
+    }
+  }
+  // attention work lists: tiles of 128 rows, longest segments first
+  std::vector<int> order(n_seg);
+  std::iota(order.begin(), order.end(), 0);
+  std::stable_sort(order.begin(), order.end(), [&](int a, int b) {
+    return (cu[a + 1] - cu[a]) > (cu[b + 1] - cu[b]);
+  });
+  for (int s : order) {
+    const int s0 = cu[s], s1 = cu[s + 1];
+    p.sum_len2 += (int64_t)(s1 - s0) * (s1 - s0);
+    for (int r = s0; r < s1; r += kTile) {
+      p.q_work.insert(p.q_work.end(), {r, s0, s1, 0});
+      p.k_work.insert(p.k_work.end(), {r, s0, s1, 0});
+    }
+  }
+  const int q4 = c.d / 4;
+  p.freq.resize(q4);
+  for (int k = 0; k < q4; ++k) p.freq[k] = (float)std::pow((double)c.theta, -4.0 * k / (double)c.d);
+
+  // ---- workspace ----
+  const int64_t h = c.hidden, m = c.mlp, H = c.llm, E = c.esz, nh = c.heads;
+  Arena ws;
+  p.ws_pos = ws.take(sizeof(int32_t) * N);
+  p.ws_qwork = ws.take(sizeof(int32_t) * p.q_work.size());
+  p.ws_kwork = ws.take(sizeof(int32_t) * p.k_work.size());
+  p.ws_freq = ws.take(sizeof(float) * q4);
+  p.meta_bytes = ws.top;
+  if (c.kp != c.kpe) {
+    p.ws_xp = ws.take((size_t)N * c.kp * E);
+    p.ws_wpe = ws.take((size_t)h * c.kp * E);
+  }
+  auto act_set = [&](Arena& a, bool keep_u, bool share_h) {
+    ActSet s{};
+    s.hin = a.take((size_t)N * h * 4);
+    s.hmid = share_h ? s.hin : a.take((size_t)N * h * 4);
+    s.hout = share_h ? s.hin : 0;  // filled by the caller when not shared
+    s.a = a.take((size_t)N * h * E);
+    s.mean1 = a.take((size_t)N * 4);
+    s.rstd1 = a.take((size_t)N * 4);
+    s.qkv = a.take((size_t)N * 3 * h * E);
+    s.o = a.take((size_t)N * h * E);
+    s.lse = a.take((size_t)N * nh * 4);
+    s.b = a.take((size_t)N * h * E);
+    s.mean2 = a.take((size_t)N * 4);
+    s.rstd2 = a.take((size_t)N * 4);
+    s.u = keep_u ? a.take((size_t)N * m * E) : 0;
+    s.g = a.take((size_t)N * m * E);
+    return s;
+  };
+  auto merger_set = [&](Arena& a, size_t hfin, bool keep_u) {
+    MergerSet s{};
+    s.hfin = hfin;
+    s.z = a.take((size_t)N * h * E);
+    s.meanz = a.take((size_t)N * 4);
+    s.rstdz = a.take((size_t)N * 4);
+    s.um = keep_u ? a.take((size_t)Tm * 4 * h * E) : 0;
+    s.gm = a.take((size_t)Tm * 4 * h * E);
+    return s;
+  };
+  if (!trainable) {
+    p.ws_act = act_set(ws, false, true);
+    p.ws_mrg = merger_set(ws, p.ws_act.hin, false);
+  } else {
+    // backward scratch
+    p.ws_dh = ws.take((size_t)N * h * 4);
+    p.ws_dht = ws.take((size_t)N * h * E);
+    p.ws_dhm = ws.take((size_t)N * h * 4);
+    p.ws_dhmt = ws.take((size_t)N * h * E);
+    p.ws_dx32 = ws.take((size_t)N * h * 4);
+    p.ws_du = ws.take((size_t)N * std::max<int64_t>(m, h) * E);
+    p.ws_do = ws.take((size_t)N * h * E);
+    p.ws_delta = ws.take((size_t)N * nh * 4);
+    p.ws_dqkv = ws.take((size_t)N * 3 * h * E);
+    const int64_t widest = std::max({3 * h, m, 4 * h, H, (int64_t)c.kpe});
+    const int64_t part_rows = std::max<int64_t>((N + 63) / 64 * 4, 1);
+    p.ws_part = ws.take((size_t)part_rows * widest * 4 * 2);
+    // largest split-K partial over the weight-gradient GEMMs
+    size_t dw = 0;
+    auto need = [&](int64_t M_, int64_t N_, int64_t K_) {
+      GemmSplit g = choose_split(M_, N_, K_);
+      if (g.splits > 1) dw = std::max(dw, (size_t)g.splits * M_ * N_ * 4);
+    };
+    need(h, c.kpe, N);
+    need(3 * h, h, N);
+    need(h, h, N);
+    need(m, h, N);
+    need(h, m, N);
+    need(4 * h, 4 * h, Tm);
+    need(H, 4 * h, Tm);
+    p.ws_dwpart = dw ? ws.take(dw) : 0;
+  }
+  p.ws_bytes = ws.top;
+
+  // ---- tape ----
+  if (trainable) {
+    Arena tp;
+    p.tape_act.resize(c.layers);
+    size_t h_in = tp.take((size_t)N * h * 4);
+    for (int l = 0; l < c.layers; ++l) {
+      ActSet s{};
+      s.hin = h_in;
+      s.hmid = tp.take((size_t)N * h * 4);
+      s.hout = tp.take((size_t)N * h * 4);
+      s.a = tp.take((size_t)N * h * E);
+      s.mean1 = tp.take((size_t)N * 4);
+      s.rstd1 = tp.take((size_t)N * 4);
+      s.qkv = tp.take((size_t)N * 3 * h * E);
+      s.o = tp.take((size_t)N * h * E);
+      s.lse = tp.take((size_t)N * nh * 4);
+      s.b = tp.take((size_t)N * h * E);
+      s.mean2 = tp.take((size_t)N * 4);
+      s.rstd2 = tp.take((size_t)N * 4);
+      s.u = tp.take((size_t)N * m * E);
+      s.g = tp.take((size_t)N * m * E);
+      p.tape_act[l] = s;
+      h_in = s.hout;
+    }
+    p.tape_mrg = merger_set(tp, h_in, true);
+    p.tape_bytes = tp.top;
+  }
+  return 0;
+}
+
+}  // namespace mpipe

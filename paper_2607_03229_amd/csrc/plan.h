@@ -1,0 +1,98 @@
+// Host planner: validates one micro-batch's metadata and lays out the device
+// workspace and tape.  Pure C++ (no HIP), so every check runs before any launch.
+#pragma once
+#include <stddef.h>
+#include <stdint.h>
+
+#include <string>
+#include <vector>
+
+namespace mpipe {
+
+struct Cfg {
+  int in_chans = 3, patch = 14, tpatch = 1, hidden = 0, layers = 0, heads = 0, mlp = 0,
+      merge = 2, llm = 0, dtype = 1;
+  float eps = 1e-6f, theta = 10000.f;
+  // derived
+  int d = 0;        // head dim
+  int kpe = 0;      // patch vector length C*T*P*P
+  int kp = 0;       // kpe rounded up to the GEMM K step (64)
+  int esz = 2;      // bytes per activation element
+};
+
+// Returns "" when cfg is supported, else the reason.
+std::string check_cfg(const Cfg& c);
+void derive_cfg(Cfg& c);
+
+struct ParamEntry {
+  std::string name;
+  int64_t off, rows, cols;
+};
+std::vector<ParamEntry> param_table(const Cfg& c);
+
+// indices into param_table
+constexpr int P_PE_W = 0, P_PE_B = 1, P_BLK0 = 2, P_PER_BLK = 12;
+enum { B_LN1G, B_LN1B, B_QKVW, B_QKVB, B_PROJW, B_PROJB, B_LN2G, B_LN2B, B_FC1W, B_FC1B,
+       B_FC2W, B_FC2B };
+enum { M_LNG, M_LNB, M_FC1W, M_FC1B, M_FC2W, M_FC2B };
+inline int blk_param(const Cfg& c, int layer, int which) {
+  (void)c;
+  return P_BLK0 + P_PER_BLK * layer + which;
+}
+inline int merger_param(const Cfg& c, int which) { return P_BLK0 + P_PER_BLK * c.layers + which; }
+
+// Byte offsets of one layer's activations (in the tape when trainable, in the
+// workspace -- shared by all layers -- when frozen).
+struct ActSet {
+  size_t hin, hmid, hout;        // fp32 [N][h] residual stream: in, after attention, out
+  size_t a, b;                   // LN1 / LN2 outputs [N][h]
+  size_t mean1, rstd1, mean2, rstd2;  // fp32 [N]
+  size_t qkv;                    // [N][3h] (q, k after rotary)
+  size_t o;                      // attention output [N][h]
+  size_t lse;                    // fp32 [heads][N]
+  size_t u;                      // fc1 pre-activation [N][m] (trainable only)
+  size_t g;                      // GELU output [N][m]
+};
+struct MergerSet {
+  size_t hfin;                   // fp32 [N][h] (the last layer's hout)
+  size_t z, meanz, rstdz;        // LN output [N][h] (= [Tm][4h]), fp32 stats
+  size_t um, gm;                 // [Tm][4h] pre-activation / GELU output
+};
+
+struct GemmSplit {
+  int splits = 1;
+  int kps = 0;
+};
+GemmSplit choose_split(int64_t M, int64_t N, int64_t K);
+
+struct Plan {
+  int64_t N = 0, Tm = 0;
+  int n_items = 0, n_seg = 0;
+  bool trainable = false;
+  int64_t sum_len2 = 0;          // sum over segments of len^2 (attention FLOPs)
+  // host metadata, uploaded into the workspace head
+  std::vector<int32_t> pos;        // N: y << 16 | x
+  std::vector<int32_t> q_work;     // 4 ints per query tile (start, seg start, seg end, 0)
+  std::vector<int32_t> k_work;     // 4 ints per key tile
+  std::vector<float> freq;         // d/4 rotary frequencies
+  size_t meta_bytes = 0;
+  // workspace layout
+  size_t ws_pos = 0, ws_qwork = 0, ws_kwork = 0, ws_freq = 0;
+  size_t ws_xp = 0, ws_wpe = 0;
+  ActSet ws_act{};                 // frozen forward activations
+  MergerSet ws_mrg{};
+  size_t ws_dh = 0, ws_dht = 0, ws_dhm = 0, ws_dhmt = 0, ws_dx32 = 0, ws_du = 0, ws_do = 0,
+         ws_delta = 0, ws_dqkv = 0, ws_part = 0, ws_dwpart = 0;
+  size_t ws_bytes = 0;
+  // tape layout (trainable)
+  std::vector<ActSet> tape_act;
+  MergerSet tape_mrg{};
+  size_t tape_bytes = 0;
+};
+
+// Validate metadata and build the plan.  Returns 0 or a negative mpipe_status;
+// `err` receives the reason.
+int build_plan(const Cfg& c, const int32_t* cu, int n_seg, const int32_t* thw, int n_items,
+               bool trainable, Plan& p, std::string& err);
+
+}  // namespace mpipe

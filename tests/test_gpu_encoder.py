@@ -1,0 +1,226 @@
+"""End-to-end parity of the encoder step on the GPU against the oracle, plus the
+paper's invariants on the GPU path (Lemma 1, Corollary 1, Accumulate,
+determinism)."""
+import dataclasses
+
+import numpy as np
+import pytest
+
+import oracle
+import workload as W
+from tests.gpu_util import announce, host, max_rel, to_dev, torch_dev, zeros
+
+pytestmark = pytest.mark.gpu
+
+TOL = {"f32": 1e-4, "bf16": 2e-2}
+
+
+class GpuRun:
+    """Runs mpipe_encoder_fwd / _bwd through the C-ABI on device copies of the inputs."""
+
+    def __init__(self, cfg, weights, patches, cu, grid):
+        import paper_2607_03229_amd as mp
+        self.torch, self.dev = torch_dev()
+        self.cfg, self.cu, self.grid = cfg, np.asarray(cu), np.asarray(grid)
+        self.enc = mp.Encoder(cfg)
+        self.w = to_dev(weights, cfg.dtype)
+        self.X = to_dev(patches, cfg.dtype)
+
+    def run(self, trainable, d_merged=None, want_dx=False, dw_init=None):
+        torch = self.torch
+        s = self.enc.sizes(self.cu, self.grid, trainable)
+        ws = torch.empty(max(s["workspace"], 1), dtype=torch.uint8, device=self.dev)
+        tape = (torch.empty(max(s["tape"], 1), dtype=torch.uint8, device=self.dev)
+                if trainable else None)
+        merged = zeros((s["n_merged"], self.cfg.llm_hidden), self.cfg.dtype)
+        self.enc.fwd(self.w, self.X, self.cu, self.grid, trainable, merged, tape, ws)
+        out = {"merged": merged}
+        if d_merged is not None:
+            dw = (to_dev(dw_init, "f32") if dw_init is not None
+                  else zeros((self.w.numel(),), "f32"))
+            dx = zeros(tuple(self.X.shape), self.cfg.dtype) if want_dx else None
+            out["status"] = self.enc.bwd(self.w, self.X, self.cu, self.grid, trainable, tape,
+                                         to_dev(d_merged, self.cfg.dtype), dw, dx, ws)
+            out["dw"], out["dx"] = dw, dx
+        torch.cuda.synchronize()
+        return out
+
+
+def _per_tensor_errors(cfg, got, ref):
+    errs = {}
+    off = 0
+    for name, shape, _ in W.param_table(cfg):
+        n = int(np.prod(shape))
+        errs[name] = max_rel(got[off:off + n], ref[off:off + n])
+        off += n
+    return errs
+
+
+def _check_full(wl_cfg, w, X, cu, grid, d_merged, tol, label):
+    announce(f"encoder fwd+bwd {label} N={len(X)}")
+    g = GpuRun(wl_cfg, w, X, cu, grid)
+    out = g.run(True, d_merged=d_merged, want_dx=True)
+    rc, rM, rdw, rdx = oracle.encoder(wl_cfg, w, X, cu, grid, True, d_merged=d_merged,
+                                      want_d_patches=True)
+    assert out["status"] == 0 and rc == 0
+    em = max_rel(host(out["merged"]), rM)
+    assert em < tol, f"merged max-rel {em}"
+    errs = _per_tensor_errors(wl_cfg, host(out["dw"]), rdw)
+    worst = max(errs, key=errs.get)
+    assert errs[worst] < tol, f"d_weights worst {worst}: {errs[worst]}"
+    ex = max_rel(host(out["dx"]), rdx)
+    assert ex < tol, f"d_patches max-rel {ex}"
+    print(f"{label}: merged {em:.2e}  d_w worst {worst} {errs[worst]:.2e}  d_patches {ex:.2e}")
+
+
+@pytest.mark.parametrize("seed", [0, 1])
+def test_c1_tiny_fp32_full(seed):
+    wl = W.make_workload("c1_tiny_fp32", seed)
+    _check_full(wl.cfg, wl.weights(), wl.patches(), wl.cu_seqlens, wl.grid_thw, wl.d_merged(),
+                TOL["f32"], f"c1 seed {seed}")
+
+
+SMALL_BF16 = {
+    # d = 64: images and a video clip (temporal patch 2), segments spanning tiles
+    "d64": (W.EncoderConfig(hidden=128, layers=2, heads=2, mlp=256, llm_hidden=256,
+                            temporal_patch=2),
+            [[1, 8, 8], [1, 16, 12], [4, 8, 8], [1, 2, 2], [1, 10, 14]]),
+    # d = 80 (the Qwen2-VL head width) with 8 heads
+    "d80": (W.EncoderConfig(hidden=640, layers=2, heads=8, mlp=1280, llm_hidden=512,
+                            temporal_patch=2),
+            [[1, 12, 10], [2, 6, 8], [1, 20, 8]]),
+    # d = 32, one long segment (several attention tiles)
+    "d32": (W.EncoderConfig(hidden=128, layers=1, heads=4, mlp=512, llm_hidden=128),
+            [[1, 24, 22], [1, 2, 4]]),
+}
+
+
+def _small_problem(key, seed=0, sharp=False):
+    cfg, grid = SMALL_BF16[key]
+    W.custom_spec(f"small_{key}", cfg)
+    wl = W.make_workload(f"small_{key}", seed, sharp=sharp, grid_thw=np.array(grid))
+    rng = np.random.default_rng(seed + 100)
+    dM = W.round_bf16(rng.standard_normal((wl.n_merged, cfg.llm_hidden)).astype(np.float32))
+    return cfg, wl, dM
+
+
+@pytest.mark.parametrize("key", ["d64", "d80", "d32"])
+def test_small_bf16_full(key):
+    cfg, wl, dM = _small_problem(key)
+    _check_full(cfg, wl.weights(), wl.patches(), wl.cu_seqlens, wl.grid_thw, dM, TOL["bf16"],
+                f"small-{key}")
+
+
+def test_small_bf16_sharp_attention():
+    cfg, wl, dM = _small_problem("d64", seed=3, sharp=True)
+    _check_full(cfg, wl.weights(), wl.patches(), wl.cu_seqlens, wl.grid_thw, dM, TOL["bf16"],
+                "small-d64-sharp")
+
+
+def test_per_slice_segments_video():
+    """A clip attended per temporal slice (cu_seqlens at slice boundaries)."""
+    cfg, wl, dM = _small_problem("d64", seed=4)
+    g = wl.grid_thw
+    cu = [0]
+    for t, gh, gw in g:
+        for _ in range(int(t)):
+            cu.append(cu[-1] + int(gh) * int(gw))
+    _check_full(cfg, wl.weights(), wl.patches(), np.array(cu, np.int32), g, dM, TOL["bf16"],
+                "per-slice")
+
+
+def test_invariants_on_gpu():
+    cfg, wl, dM = _small_problem("d64", seed=5)
+    w, X = wl.weights(), wl.patches()
+    announce("invariants: frozen/trained forward, determinism, NOOP, accumulate")
+    g = GpuRun(cfg, w, X, wl.cu_seqlens, wl.grid_thw)
+    frozen = g.run(False)
+    t1 = g.run(True, d_merged=dM)
+    t2 = g.run(True, d_merged=dM)
+    # Corollary 1: the forward does not depend on the trainability footprint
+    assert g.torch.equal(frozen["merged"], t1["merged"])
+    # deterministic kernels: identical runs are bitwise equal
+    assert g.torch.equal(t1["merged"], t2["merged"]) and g.torch.equal(t1["dw"], t2["dw"])
+    # Lemma 1: a frozen encoder has no backward; nothing is written
+    sentinel = np.full(w.shape, 3.5, np.float32)
+    fz = g.run(False, d_merged=dM, dw_init=sentinel)
+    assert fz["status"] == 1
+    np.testing.assert_array_equal(host(fz["dw"]), sentinel)
+    # Accumulate edge: gradients add into what the buffer holds
+    base = np.random.default_rng(1).standard_normal(w.shape).astype(np.float32)
+    acc = g.run(True, d_merged=dM, dw_init=base)
+    np.testing.assert_array_equal(host(acc["dw"]).astype(np.float32),
+                                  (base + host(t1["dw"]).astype(np.float32)))
+
+
+def test_relocation_owner_groups_on_gpu():
+    """Encoding owner groups separately then scattering equals encoding at once."""
+    import paper_2607_03229_amd as mp
+    cfg, wl, dM = _small_problem("d64", seed=6)
+    w, X = wl.weights(), wl.patches()
+    cu, grid = wl.cu_seqlens, wl.grid_thw
+    torch, dev = torch_dev()
+    announce("relocation: owner groups vs all at once")
+    n_rows = 600
+    idx = np.random.default_rng(2).permutation(n_rows)[:wl.n_merged]
+    emb_all = zeros((n_rows, cfg.llm_hidden), "bf16")
+    full = GpuRun(cfg, w, X, cu, grid).run(True, d_merged=dM)
+    mp.merge_scatter(full["merged"], torch.from_numpy(idx).to(dev), emb_all)
+    per_m = (grid[:, 0] * (grid[:, 1] // 2) * (grid[:, 2] // 2))
+    mo = np.concatenate([[0], np.cumsum(per_m)])
+    emb = zeros((n_rows, cfg.llm_hidden), "bf16")
+    dw_sum = np.zeros(w.shape)
+    for grp in ([0, 2, 4], [1, 3]):
+        Xg = np.concatenate([X[cu[i]:cu[i + 1]] for i in grp])
+        gg = grid[grp]
+        cug = np.concatenate([[0], np.cumsum(gg[:, 0] * gg[:, 1] * gg[:, 2])]).astype(np.int32)
+        ig = np.concatenate([idx[mo[i]:mo[i + 1]] for i in grp])
+        dMg = np.concatenate([dM[mo[i]:mo[i + 1]] for i in grp])
+        r = GpuRun(cfg, w, Xg, cug, gg).run(True, d_merged=dMg)
+        mp.merge_scatter(r["merged"], torch.from_numpy(ig).to(dev), emb)
+        dw_sum += host(r["dw"])
+    torch.cuda.synchronize()
+    assert torch.equal(emb, emb_all)      # per-item work is independent: bitwise
+    errs = _per_tensor_errors(cfg, dw_sum, host(full["dw"]))
+    assert max(errs.values()) < 1e-4, max(errs.items(), key=lambda kv: kv[1])
+
+
+def _smallest_items(wl, k):
+    n = wl.grid_thw[:, 0] * wl.grid_thw[:, 1] * wl.grid_thw[:, 2]
+    return sorted(np.argsort(n, kind="stable")[:k].tolist())
+
+
+@pytest.mark.parametrize("name", ["c2_vitl_frozen", "c4_qwen2vl_trained"])
+def test_full_size_forward_sampled(name):
+    """Full micro-batch on the GPU; the oracle recomputes the smallest item alone
+    (valid by the block-diagonal independence of items)."""
+    wl = W.make_workload(name, 0)
+    cfg = wl.cfg
+    w, X = wl.weights(), wl.patches()
+    announce(f"full-size forward {name} N={wl.n_patches} items={wl.n_items}")
+    g = GpuRun(cfg, w, X, wl.cu_seqlens, wl.grid_thw)
+    out = g.run(wl.trainable, d_merged=wl.d_merged() if wl.trainable else None)
+    got = host(out["merged"])
+    per_m = wl.merged_per_item
+    mo = np.concatenate([[0], np.cumsum(per_m)])
+    for i in _smallest_items(wl, 1):
+        sl = slice(int(wl.cu_seqlens[i]), int(wl.cu_seqlens[i + 1]))
+        n = sl.stop - sl.start
+        _, Mi, _, _ = oracle.encoder(cfg, w, X[sl], [0, n], wl.grid_thw[i:i + 1], False)
+        err = max_rel(got[mo[i]:mo[i + 1]], Mi)
+        print(f"{name} item {i} ({n} patches): merged max-rel {err:.2e}")
+        assert err < TOL["bf16"]
+    assert np.isfinite(got).all()
+    if wl.trainable:
+        assert np.isfinite(host(out["dw"])).all()
+
+
+def test_full_depth_gradients_one_item():
+    """Qwen2-VL-ViT shape at full depth (32 layers): weight and patch gradients
+    of one 256-patch image against the oracle."""
+    cfg = W.CONFIGS["c4_qwen2vl_trained"].cfg
+    wl = W.make_workload("c4_qwen2vl_trained", 0, grid_thw=np.array([[1, 16, 16]]))
+    rng = np.random.default_rng(9)
+    dM = W.round_bf16(rng.standard_normal((wl.n_merged, cfg.llm_hidden)).astype(np.float32))
+    _check_full(cfg, wl.weights(), wl.patches(), wl.cu_seqlens, wl.grid_thw, dM, TOL["bf16"],
+                "c4-shape one item")

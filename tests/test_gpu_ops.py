@@ -1,0 +1,202 @@
+"""Per-kernel parity on the GPU: each HIP kernel (through the op C-ABI) against
+the oracle's building block on the same seeded inputs, at sizes spanning
+several tiles with ragged tails."""
+import numpy as np
+import pytest
+
+import oracle
+from tests.gpu_util import announce, host, max_rel, rnd, to_dev, torch_dev, zeros
+
+pytestmark = pytest.mark.gpu
+
+NT, NN, TN = 0, 1, 2
+E_STORE, E_GELU, E_RESID, E_GELUBWD, E_F32 = range(5)
+TOL = {"bf16": 1e-2, "f32": 2e-5}
+
+
+def _dt(s):
+    return 1 if s == "bf16" else 0
+
+
+def _ref_product(layout, A, B):
+    if layout == NT:
+        return oracle.linear(A, B)
+    if layout == NN:
+        return oracle.linear(A, B.T)
+    return oracle.linear(A.T, B.T)
+
+
+GEMM_SHAPES = {
+    NT: [(300, 200, 256), (1, 8, 8), (129, 257, 72), (512, 384, 1280)],
+    NN: [(300, 200, 256), (129, 264, 72), (77, 8, 520)],
+    TN: [(200, 264, 333), (8, 16, 1), (136, 128, 1000)],
+}
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("layout", [NT, NN, TN])
+def test_gemm_layouts(dtype, layout):
+    import paper_2607_03229_amd as mp
+    torch, dev = torch_dev()
+    rng = np.random.default_rng(10 * layout + len(dtype))
+    for (M, N, K) in GEMM_SHAPES[layout]:
+        if dtype == "f32" and layout != TN and K % 4:
+            continue
+        announce(f"gemm {dtype} layout={layout} M={M} N={N} K={K}")
+        A = rnd(rng, (K, M) if layout == TN else (M, K), dtype)
+        B = rnd(rng, (N, K) if layout == NT else (K, N), dtype)
+        ref = _ref_product(layout, A, B)
+        C = zeros((M, N), "f32")
+        mp.op_gemm(_dt(dtype), layout, E_F32, M, N, K, to_dev(A, dtype), A.shape[1],
+                   to_dev(B, dtype), B.shape[1], C, N)
+        torch.cuda.synchronize()
+        err = max_rel(host(C), ref)
+        assert err < (2e-5 if dtype == "f32" else 1e-5), (M, N, K, err)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_gemm_epilogues(dtype):
+    import paper_2607_03229_amd as mp
+    torch, dev = torch_dev()
+    rng = np.random.default_rng(7)
+    M, N, K = 333, 264, 192
+    A, B, bias = rnd(rng, (M, K), dtype), rnd(rng, (N, K), dtype, 0.1), rnd(rng, (N,), dtype)
+    dA, dB, db = to_dev(A, dtype), to_dev(B, dtype), to_dev(bias, dtype)
+    pre = oracle.linear(A, B, bias)
+    # store with bias
+    announce(f"gemm epilogue store {dtype}")
+    C = zeros((M, N), dtype)
+    mp.op_gemm(_dt(dtype), NT, E_STORE, M, N, K, dA, K, dB, K, C, N, bias=db)
+    assert max_rel(host(C), pre) < TOL[dtype]
+    # GELU with the pre-activation stored
+    announce(f"gemm epilogue gelu {dtype}")
+    C, C2 = zeros((M, N), dtype), zeros((M, N), dtype)
+    mp.op_gemm(_dt(dtype), NT, E_GELU, M, N, K, dA, K, dB, K, C, N, bias=db, C2=C2, ldc2=N)
+    assert max_rel(host(C2), pre) < TOL[dtype]
+    assert max_rel(host(C), oracle.gelu(pre)) < TOL[dtype]
+    # residual update in place (aux aliases C)
+    announce(f"gemm epilogue resid {dtype}")
+    R = rng.standard_normal((M, N)).astype(np.float32)
+    C = to_dev(R, "f32")
+    mp.op_gemm(_dt(dtype), NT, E_RESID, M, N, K, dA, K, dB, K, C, N, bias=db, aux=C, ld_aux=N)
+    assert max_rel(host(C), R + pre) < 2e-5
+    # GELU backward: acc * GELU'(aux)
+    announce(f"gemm epilogue gelu-bwd {dtype}")
+    U = rnd(rng, (M, N), dtype)
+    C = zeros((M, N), dtype)
+    mp.op_gemm(_dt(dtype), NT, E_GELUBWD, M, N, K, dA, K, dB, K, C, N, aux=to_dev(U, dtype),
+               ld_aux=N)
+    assert max_rel(host(C), oracle.linear(A, B) * oracle.gelu_grad(U)) < TOL[dtype]
+    # fp32 accumulate (beta = 1)
+    announce(f"gemm epilogue f32 accumulate {dtype}")
+    C = to_dev(R, "f32")
+    mp.op_gemm(_dt(dtype), NT, E_F32, M, N, K, dA, K, dB, K, C, N, beta=1)
+    assert max_rel(host(C), R + oracle.linear(A, B)) < 2e-5
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_gemm_split_k(dtype):
+    import paper_2607_03229_amd as mp
+    torch, dev = torch_dev()
+    rng = np.random.default_rng(3)
+    M, N, K, kps = 136, 264, 1000, 256
+    announce(f"gemm split-k {dtype}")
+    A, B = rnd(rng, (K, M), dtype), rnd(rng, (K, N), dtype)
+    splits = (K + kps - 1) // kps
+    part = zeros((splits, M, N), "f32")
+    mp.op_gemm(_dt(dtype), TN, E_F32, M, N, K, to_dev(A, dtype), M, to_dev(B, dtype), N, part, N,
+               k_per_split=kps, split_stride=M * N)
+    got = host(part)
+    for s in range(splits):
+        sl = slice(s * kps, min(K, (s + 1) * kps))
+        assert max_rel(got[s], A[sl].T.astype(np.float64) @ B[sl]) < 2e-5
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("n", [128, 1024, 1280])
+def test_layernorm_fwd_bwd(dtype, n):
+    import paper_2607_03229_amd as mp
+    torch, dev = torch_dev()
+    rng = np.random.default_rng(n)
+    rows = 333
+    announce(f"layernorm {dtype} n={n}")
+    X = (rng.standard_normal((rows, n)) * 3 + 1).astype(np.float32)
+    g, b = rnd(rng, (n,), dtype, 0.1, 1.0), rnd(rng, (n,), dtype, 0.1)
+    Y = zeros((rows, n), dtype)
+    mean, rstd = zeros((rows,), "f32"), zeros((rows,), "f32")
+    dX_ = to_dev(X, "f32")
+    mp.op_layernorm_fwd(_dt(dtype), dX_, rows, n, to_dev(g, dtype), to_dev(b, dtype), 1e-6, Y,
+                        mean, rstd)
+    ry, rmu, rrs = oracle.layernorm(X, g, b, 1e-6)
+    assert max_rel(host(Y), ry) < TOL[dtype]
+    assert max_rel(host(mean), rmu) < 1e-5 and max_rel(host(rstd), rrs) < 1e-5
+    dY = rng.standard_normal((rows, n)).astype(np.float32)
+    dres = rng.standard_normal((rows, n)).astype(np.float32)
+    dX, dXt = zeros((rows, n), "f32"), zeros((rows, n), dtype)
+    gg, gb = to_dev(np.ones(n), "f32"), to_dev(np.zeros(n), "f32")
+    scratch = torch.empty(mp.op_scratch_bytes(rows, 1, n, 0), dtype=torch.uint8, device=dev)
+    mp.op_layernorm_bwd(_dt(dtype), to_dev(dY, "f32"), dX_, mean, rstd, to_dev(g, dtype), rows, n,
+                        to_dev(dres, "f32"), dX, dXt, gg, gb, scratch)
+    rdx, rdg, rdb = oracle.layernorm_bwd(dY, X, g, rmu, rrs)
+    assert max_rel(host(dX), rdx + dres) < 1e-4
+    assert max_rel(host(dXt), rdx + dres) < TOL[dtype]
+    assert max_rel(host(gg), 1 + rdg) < 1e-4 and max_rel(host(gb), rdb) < 1e-4
+
+
+@pytest.mark.parametrize("dtype,heads,d", [("bf16", 16, 80), ("bf16", 4, 64), ("f32", 4, 32)])
+def test_rope(dtype, heads, d):
+    import paper_2607_03229_amd as mp
+    torch, dev = torch_dev()
+    grid = np.array([[1, 6, 8], [2, 4, 4], [1, 96, 2]], np.int32)
+    N = int((grid[:, 0] * grid[:, 1] * grid[:, 2]).sum())
+    announce(f"rope {dtype} heads={heads} d={d} N={N}")
+    rng = np.random.default_rng(d)
+    h = heads * d
+    qkv = rnd(rng, (N, 3 * h), dtype)
+    t = to_dev(qkv, dtype)
+    scratch = torch.empty(mp.op_scratch_bytes(N, heads, h, 3), dtype=torch.uint8, device=dev)
+    mp.op_rope(_dt(dtype), t, N, heads, d, grid, 10000.0, 0, scratch)
+    py, px = oracle.positions(grid)
+    got = host(t)
+    for part in (0, 1):
+        ref = oracle.rope2d(qkv[:, part * h:(part + 1) * h], heads, d, py, px)
+        assert max_rel(got[:, part * h:(part + 1) * h], ref) < TOL[dtype]
+    np.testing.assert_array_equal(got[:, 2 * h:], qkv[:, 2 * h:])    # v untouched
+    mp.op_rope(_dt(dtype), t, N, heads, d, grid, 10000.0, 1, scratch)
+    assert max_rel(host(t), qkv) < 2 * TOL[dtype]
+
+
+ATTN_LENS = [1, 5, 64, 127, 128, 129, 300, 16]
+
+
+@pytest.mark.parametrize("dtype,heads,d", [("bf16", 2, 80), ("bf16", 2, 64), ("bf16", 3, 32),
+                                           ("f32", 2, 32)])
+def test_attention_fwd_bwd(dtype, heads, d):
+    import paper_2607_03229_amd as mp
+    torch, dev = torch_dev()
+    rng = np.random.default_rng(d + heads)
+    cu = np.concatenate([[0], np.cumsum(ATTN_LENS)]).astype(np.int32)
+    N = int(cu[-1])
+    h = heads * d
+    announce(f"attention {dtype} heads={heads} d={d} N={N}")
+    qkv = rnd(rng, (N, 3 * h), dtype, 1.5)
+    q, k, v = qkv[:, :h], qkv[:, h:2 * h], qkv[:, 2 * h:]
+    ro, rlse = oracle.attention(q, k, v, cu, heads, d)
+    tq = to_dev(qkv, dtype)
+    o, lse = zeros((N, h), dtype), zeros((heads, N), "f32")
+    scratch = torch.empty(mp.op_scratch_bytes(N, heads, h, len(ATTN_LENS)), dtype=torch.uint8,
+                          device=dev)
+    mp.op_attention_fwd(_dt(dtype), tq, N, heads, d, cu, o, lse, scratch)
+    tol = 2e-2 if dtype == "bf16" else 1e-5
+    assert max_rel(host(o), ro) < tol
+    assert max_rel(host(lse), rlse.T) < (1e-3 if dtype == "bf16" else 1e-5)
+    announce(f"attention bwd {dtype} heads={heads} d={d} N={N}")
+    dO = rnd(rng, (N, h), dtype)
+    rdq, rdk, rdv = oracle.attention_bwd(q, k, v, ro, dO, rlse, cu, heads, d)
+    dqkv = zeros((N, 3 * h), dtype)
+    mp.op_attention_bwd(_dt(dtype), tq, o, to_dev(dO, dtype), lse, N, heads, d, cu, dqkv, scratch)
+    got = host(dqkv)
+    for name, sl, ref in (("dq", slice(0, h), rdq), ("dk", slice(h, 2 * h), rdk),
+                          ("dv", slice(2 * h, 3 * h), rdv)):
+        err = max_rel(got[:, sl], ref)
+        assert err < (3e-2 if dtype == "bf16" else 1e-5), (name, err)
