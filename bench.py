@@ -45,24 +45,37 @@ def model_flops(cfg, n_patches: int, sum_len2: int, trainable: bool) -> float:
     return float(3 * F - 2 * N * kpe * h) if trainable else float(F)
 
 
-def cpu_baseline(seconds_hint: float = 20.0):
+def cpu_baseline(sample_layers: int = 8):
     """Time the CPU oracle on a bounded sample of the same workload shape: one
-    224x224 image (256 patches) through the full-depth encoder, forward and
-    backward (trained) or forward only (frozen)."""
+    224x224 image (256 patches, the smallest the size draw produces) through the
+    Qwen2-VL-ViT-shaped encoder truncated to `sample_layers` of its blocks (patch
+    embedding and merger included), forward and backward.  The measured time is
+    scaled to the full-depth encoder by the ratio of model FLOPs (every block
+    costs the same), and the sample is stated alongside."""
+    import dataclasses
+
     import oracle
     import workload as W
-    cfg = W.CONFIGS["c4_qwen2vl_trained"].cfg
-    wl = W.make_workload("c4_qwen2vl_trained", 0, grid_thw=np.array([[1, 16, 16]]))
+    full = W.CONFIGS["c4_qwen2vl_trained"].cfg
+    cfg = dataclasses.replace(full, layers=sample_layers)
+    W.custom_spec("cpu_baseline_sample", cfg)
+    wl = W.make_workload("cpu_baseline_sample", 0, grid_thw=np.array([[1, 16, 16]]))
     w, X = wl.weights(), wl.patches()
     dM = np.random.default_rng(0).standard_normal((wl.n_merged, cfg.llm_hidden))
     t0 = time.perf_counter()
     oracle.encoder(cfg, w, X, wl.cu_seqlens, wl.grid_thw, True, d_merged=dM)
     dt = time.perf_counter() - t0
-    return {"value": wl.n_patches / dt, "unit": "patch-tokens/s", "cores": oracle.num_threads(),
-            "kind": "oracle",
-            "sample": ("one 224x224 image (256 patches), Qwen2-VL-ViT shape, all 32 layers, "
-                       "fp64 forward+backward incl. merger; " f"{dt:.1f} s"),
-            "cpu": platform.processor() or _cpu_model()}
+    n = wl.n_patches
+    f_sample = model_flops(cfg, n, n * n, True)
+    f_full = model_flops(full, n, n * n, True)
+    t_full = dt * f_full / f_sample
+    return {"value": round(n / t_full, 4), "unit": "patch-tokens/s",
+            "cores": oracle.num_threads(), "kind": "oracle",
+            "sample": (f"one 224x224 image (256 patches), Qwen2-VL-ViT shape truncated to "
+                       f"{sample_layers} of 32 blocks, fp64 forward+backward incl. patch "
+                       f"embedding and merger: {dt:.1f} s measured, scaled by model FLOPs "
+                       f"({f_full / f_sample:.2f}x) to the full 32-block encoder"),
+            "cpu": _cpu_model()}
 
 
 def _cpu_model() -> str:

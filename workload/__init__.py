@@ -42,9 +42,9 @@ __all__ = [
 
 def bf16_bits(x: np.ndarray) -> np.ndarray:
     """float32 array -> uint16 bf16 bit patterns, round to nearest even."""
-    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
-    bias = ((u >> np.uint32(16)) & np.uint32(1)) + np.uint32(0x7FFF)
-    return ((u + bias) >> np.uint32(16)).astype(np.uint16)
+    r = np.array(x, dtype=np.float32, copy=True, order="C")
+    round_bf16_inplace(r)
+    return (r.view(np.uint32) >> np.uint32(16)).astype(np.uint16)
 
 
 def bf16_bits_to_f32(b: np.ndarray) -> np.ndarray:
@@ -52,9 +52,20 @@ def bf16_bits_to_f32(b: np.ndarray) -> np.ndarray:
             << np.uint32(16)).view(np.float32)
 
 
+def round_bf16_inplace(x: np.ndarray, chunk: int = 1 << 24) -> None:
+    """Round a float32 array to the nearest bf16 values in place (RNE)."""
+    u = x.reshape(-1).view(np.uint32)
+    for i in range(0, u.size, chunk):
+        c = u[i:i + chunk]
+        c += ((c >> np.uint32(16)) & np.uint32(1)) + np.uint32(0x7FFF)
+        c &= np.uint32(0xFFFF0000)
+
+
 def round_bf16(x: np.ndarray) -> np.ndarray:
     """float32 values rounded to the nearest bf16 (returned as float32)."""
-    return bf16_bits_to_f32(bf16_bits(x))
+    r = np.array(x, dtype=np.float32, copy=True, order="C")
+    round_bf16_inplace(r)
+    return r
 
 
 # --------------------------------------------------------------------------
@@ -306,17 +317,19 @@ class Workload:
         so that attention rows are far from uniform."""
         rng = self._rng(2)
         cfg = self.cfg
-        chunks = []
+        w = np.empty(param_count(cfg), np.float32)
+        off = 0
         for name, shape, kind in param_table(cfg):
             n = int(np.prod(shape))
+            seg = w[off:off + n]
             std = 0.1 if (self.sharp and name.endswith("qkv.w")) else 0.02
-            v = rng.standard_normal(n, dtype=np.float32) * np.float32(std)
+            rng.standard_normal(out=seg, dtype=np.float32)
+            seg *= np.float32(std)
             if kind == "g":
-                v += np.float32(1.0)
-            chunks.append(v)
-        w = np.concatenate(chunks)
+                seg += np.float32(1.0)
+            off += n
         if cfg.dtype == "bf16":
-            w = round_bf16(w)
+            round_bf16_inplace(w)
         return w
 
     # -- placeholders ------------------------------------------------------
