@@ -370,6 +370,7 @@ __global__ __launch_bounds__(NTHR, 2) void attn_bwd_dq_kernel(AttnArgs p) {
   const bf16* dO = reinterpret_cast<const bf16*>(p.d_o) + head * D;
   const float sl2 = p.scale * kLog2e;
 
+  const bf16* O = reinterpret_cast<const bf16*>(p.o) + head * D;
   RowFrag<D> qf[2], dof[2];
   int qrow[2];
   float lse2[2], del[2];
@@ -380,7 +381,25 @@ __global__ __launch_bounds__(NTHR, 2) void attn_bwd_dq_kernel(AttnArgs p) {
     load_rowfrag<D>(qf[qs], Q, p.ld, qc, g);
     load_rowfrag<D>(dof[qs], dO, p.ldo, qc, g);
     lse2[qs] = p.lse[(int64_t)head * p.N + qc] * kLog2e;
-    del[qs] = p.delta[(int64_t)head * p.N + qc];
+    // delta = rowsum(dO o O): this lane holds d-chunks of its query; the four
+    // lane groups g together cover all d
+    RowFrag<D> of;
+    load_rowfrag<D>(of, O, p.ldo, qc, g);
+    float dl = 0.f;
+#pragma unroll
+    for (int f = 0; f < AD<D>::NF; ++f)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) dl += (float)of.f[f][e] * (float)dof[qs].f[f][e];
+    if constexpr (AD<D>::REM) {
+      const bf16* ro = reinterpret_cast<const bf16*>(&of.rem);
+      const bf16* rd = reinterpret_cast<const bf16*>(&dof[qs].rem);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) dl += (float)ro[e] * (float)rd[e];
+    }
+    dl += __shfl_xor(dl, 16);
+    dl += __shfl_xor(dl, 32);
+    del[qs] = dl;
+    if (g == 0 && qrow[qs] < s1) p.delta_out[(int64_t)head * p.N + qrow[qs]] = dl;
   }
   f32x4 dq[2][NDT];
 #pragma unroll
@@ -500,7 +519,7 @@ __global__ void attn_bwd_dq_f32_kernel(AttnArgs p) {
     dov[e] = dO[(int64_t)q * p.ldo + e];
     dq[e] = 0.f;
   }
-  const float L = p.lse[(int64_t)head * p.N + q], del = p.delta[(int64_t)head * p.N + q];
+  const float L = p.lse[(int64_t)head * p.N + q], del = p.delta_out[(int64_t)head * p.N + q];
   for (int k = s0; k < s1; ++k) {
     float s = 0.f, dp = 0.f;
     for (int e = 0; e < D; ++e) {
@@ -573,6 +592,9 @@ hipError_t fwd_f32(const AttnArgs& a, hipStream_t s) {
 }
 template <int D>
 hipError_t dq_f32(const AttnArgs& a, hipStream_t s) {
+  const int64_t n = a.N * a.heads;
+  hipLaunchKernelGGL(attn_delta_kernel<float>, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s,
+                     (const float*)a.o, (const float*)a.d_o, a.ldo, a.N, a.heads, D, a.delta_out);
   hipLaunchKernelGGL(attn_bwd_dq_f32_kernel<D>, dim3(a.n_work * a.heads), dim3(ATTN_TILE), 0, s, a);
   return hipGetLastError();
 }
@@ -631,19 +653,5 @@ hipError_t attention_bwd_dkdv(int dtype, int head_dim, const AttnArgs& a, hipStr
   MPIPE_ATTN_DISPATCH(dkdv_bf16, dkdv_f32)
 }
 #undef MPIPE_ATTN_DISPATCH
-
-hipError_t attention_delta(int dtype, const void* O, const void* dO, int64_t ldo, int64_t N,
-                           int heads, int d, float* delta, hipStream_t s) {
-  const int64_t n = N * heads;
-  if (n == 0) return hipSuccess;
-  const int blocks = (int)((n + 255) / 256);
-  if (dtype == DT_BF16)
-    hipLaunchKernelGGL(attn_delta_kernel<bf16>, dim3(blocks), dim3(256), 0, s,
-                       (const bf16*)O, (const bf16*)dO, ldo, N, heads, d, delta);
-  else
-    hipLaunchKernelGGL(attn_delta_kernel<float>, dim3(blocks), dim3(256), 0, s,
-                       (const float*)O, (const float*)dO, ldo, N, heads, d, delta);
-  return hipGetLastError();
-}
 
 }  // namespace mpipe

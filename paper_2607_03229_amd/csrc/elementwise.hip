@@ -86,16 +86,33 @@ __global__ __launch_bounds__(256) void ln_fwd_kernel(const float* X, int64_t ldx
 
 // ---- LayerNorm backward -------------------------------------------------------------
 // dx = rstd * (g*dy - mean(g*dy) - xhat * mean(g*dy*xhat)) + dres, written in fp32
-// (and optionally as T for the next GEMM); per-wave partial sums of dy*xhat and
-// dy go to part_g / part_b [gridDim.x * 4][n] for a deterministic reduction.
-constexpr int LN_ROWS_PER_WAVE = 16;
+// (and optionally as T for the next GEMM).  Each block owns a contiguous chunk of
+// rows (its four waves take every fourth row); the block's sums of dy*xhat and dy
+// are combined in LDS in a fixed order and written to part_g / part_b
+// [gridDim.x][n] for a deterministic reduction.
+constexpr int LN_BWD_MAX_BLOCKS = 512;
+
+__device__ __forceinline__ void combine_waves(const float4* red, int nc, float* out) {
+  for (int c = threadIdx.x; c < nc; c += 256) {
+    const int i = c / 64, ll = c % 64;
+    float4 t = red[i * 64 + ll];
+#pragma unroll
+    for (int w = 1; w < 4; ++w) {
+      const float4 u = red[(w * MAXC + i) * 64 + ll];
+      t.x += u.x; t.y += u.y; t.z += u.z; t.w += u.w;
+    }
+    *reinterpret_cast<float4*>(out + 4 * c) = t;
+  }
+}
 
 template <class T>
 __global__ __launch_bounds__(256) void ln_bwd_kernel(const float* dY, int64_t ldd, const float* X,
                                                      int64_t ldx, const float* mean,
                                                      const float* rstd, const T* gam, int64_t rows,
-                                                     int n, const float* dres, float* dX,
-                                                     T* dXt, float* part_g, float* part_b) {
+                                                     int n, int64_t rows_per_block,
+                                                     const float* dres, float* dX, T* dXt,
+                                                     float* part_g, float* part_b) {
+  __shared__ float4 red[4 * MAXC * 64];
   const int wave = threadIdx.x >> 6, l = threadIdx.x & 63;
   const int nc = n / 4;
   float4 ag[MAXC], ab[MAXC], gm[MAXC];
@@ -105,10 +122,9 @@ __global__ __launch_bounds__(256) void ln_bwd_kernel(const float* dY, int64_t ld
     const int c = l + 64 * i;
     if (c < nc) gm[i] = V4<T>::load(gam + 4 * c);
   }
-  const int64_t rbase = ((int64_t)blockIdx.x * 4 + wave) * LN_ROWS_PER_WAVE;
-  for (int rr = 0; rr < LN_ROWS_PER_WAVE; ++rr) {
-    const int64_t row = rbase + rr;
-    if (row >= rows) break;
+  const int64_t r0 = (int64_t)blockIdx.x * rows_per_block;
+  const int64_t r1 = min(rows, r0 + rows_per_block);
+  for (int64_t row = r0 + wave; row < r1; row += 4) {
     const float mu = mean[row], rs = rstd[row];
     float4 xh[MAXC], dy[MAXC];
     float s1 = 0.f, s2 = 0.f;
@@ -148,36 +164,52 @@ __global__ __launch_bounds__(256) void ln_bwd_kernel(const float* dY, int64_t ld
       }
     }
   }
-  const int64_t prow = (int64_t)blockIdx.x * 4 + wave;
+  // combine the four waves in a fixed order: gain sums, then shift sums
 #pragma unroll
-  for (int i = 0; i < MAXC; ++i) {
-    const int c = l + 64 * i;
-    if (c < nc) {
-      V4<float>::store(part_g + prow * n + 4 * c, ag[i]);
-      V4<float>::store(part_b + prow * n + 4 * c, ab[i]);
-    }
-  }
+  for (int i = 0; i < MAXC; ++i) red[(wave * MAXC + i) * 64 + l] = ag[i];
+  __syncthreads();
+  combine_waves(red, nc, part_g + (int64_t)blockIdx.x * n);
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < MAXC; ++i) red[(wave * MAXC + i) * 64 + l] = ab[i];
+  __syncthreads();
+  combine_waves(red, nc, part_b + (int64_t)blockIdx.x * n);
 }
 
-// ---- column partial sums over 64-row blocks: part[b][c] = sum_r X[64b + r][c] -------
+// ---- column sums: part[b][c] = sum of X[r][c] over row chunk b ----------------------
+constexpr int COLSUM_MAX_CHUNKS = 256;
+
 template <class T>
-__global__ void colsum_partial_kernel(const T* X, int64_t ld, int64_t rows, int n, float* part) {
+__global__ void colsum_partial_kernel(const T* X, int64_t ld, int64_t rows, int n,
+                                      int64_t rows_per_chunk, float* part) {
   const int c = blockIdx.x * blockDim.x + threadIdx.x;
   if (c >= n) return;
-  const int64_t r0 = (int64_t)blockIdx.y * 64;
-  const int64_t r1 = min(rows, r0 + 64);
-  float s = 0.f;
-  for (int64_t r = r0; r < r1; ++r) s += to_f(X[r * ld + c]);
-  part[(int64_t)blockIdx.y * n + c] = s;
+  const int64_t r0 = (int64_t)blockIdx.y * rows_per_chunk;
+  const int64_t r1 = min(rows, r0 + rows_per_chunk);
+  float s0 = 0.f, s1 = 0.f, s2 = 0.f, s3 = 0.f;
+  int64_t r = r0;
+  for (; r + 4 <= r1; r += 4) {
+    s0 += to_f(X[r * ld + c]);
+    s1 += to_f(X[(r + 1) * ld + c]);
+    s2 += to_f(X[(r + 2) * ld + c]);
+    s3 += to_f(X[(r + 3) * ld + c]);
+  }
+  for (; r < r1; ++r) s0 += to_f(X[r * ld + c]);
+  part[(int64_t)blockIdx.y * n + c] = (s0 + s1) + (s2 + s3);
 }
 
-// out[c] += sum_b part[b][c]   (fixed order)
+// out[c] += sum_b part[b][c], b < nb.  One block per 64 columns; its four waves
+// take every fourth partial row and are combined in a fixed order.
 __global__ void reduce_partials_kernel(const float* part, int64_t nb, int n, float* out) {
-  const int c = blockIdx.x * blockDim.x + threadIdx.x;
-  if (c >= n) return;
+  __shared__ float red[4][64];
+  const int w = threadIdx.x >> 6, l = threadIdx.x & 63;
+  const int c = blockIdx.x * 64 + l;
   float s = 0.f;
-  for (int64_t b = 0; b < nb; ++b) s += part[b * n + c];
-  out[c] += s;
+  if (c < n)
+    for (int64_t b = w; b < nb; b += 4) s += part[b * n + c];
+  red[w][l] = s;
+  __syncthreads();
+  if (w == 0 && c < n) out[c] += (red[0][l] + red[1][l]) + (red[2][l] + red[3][l]);
 }
 
 // out[m][n] += sum_s part[s][m][n]   (partials are dense [M][N])
@@ -202,30 +234,38 @@ __global__ void pad_cols_kernel(const T* src, int64_t rows, int K, T* dst, int K
 }
 
 // ---- 2D rotary position, in place on the q and k column blocks -------------------
-// pos[r] = y << 16 | x;  freq[k] = theta^(-4k/d), k < d/4.  Pair (j, j + d/2) of
-// each head rotates by a_j = y * freq[j] (j < d/4) or x * freq[j - d/4].
+// pos[r] = y << 16 | x.  tab[p * q4 + k] = (cos, sin) of p * theta^(-4k/d) (k < q4 = d/4,
+// computed on the host in double).  Pair (j, j + d/2) of each head rotates by the
+// angle of y (j < d/4) or of x (j >= d/4).  Each thread rotates 4 consecutive pairs.
 template <class T>
 __global__ void rope_kernel(T* qk, int64_t ld, int64_t rows, int heads, int d, int kcol,
-                            const int32_t* pos, const float* freq, int inverse) {
+                            const int32_t* pos, const float2* tab, int inverse) {
   const int half = d / 2, quarter = d / 4;
-  const int64_t per_row = (int64_t)heads * half * 2;  // (q or k) x head x pair
+  const int groups = half / 4;                       // 4-pair groups per head
+  const int64_t per_row = (int64_t)2 * heads * groups;
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= rows * per_row) return;
   const int64_t r = i / per_row;
   int rem = (int)(i % per_row);
-  const int which = rem / (heads * half);
-  rem %= heads * half;
-  const int hd = rem / half, j = rem % half;
+  const int which = rem / (heads * groups);
+  rem %= heads * groups;
+  const int hd = rem / groups, j0 = 4 * (rem % groups);
   const int32_t pp = pos[r];
-  const float coord = (j < quarter) ? (float)(pp >> 16) : (float)(pp & 0xFFFF);
-  const float a = coord * freq[j < quarter ? j : j - quarter];
-  float sn, cs;
-  sincosf(a, &sn, &cs);
-  if (inverse) sn = -sn;
   T* v = qk + r * ld + (which ? kcol : 0) + hd * d;
-  const float x1 = to_f(v[j]), x2 = to_f(v[j + half]);
-  v[j] = from_f<T>(x1 * cs - x2 * sn);
-  v[j + half] = from_f<T>(x2 * cs + x1 * sn);
+  const float4 a = V4<T>::load(v + j0), b = V4<T>::load(v + j0 + half);
+  const float x1[4] = {a.x, a.y, a.z, a.w}, x2[4] = {b.x, b.y, b.z, b.w};
+  float o1[4], o2[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const int j = j0 + e;
+    const int coord = (j < quarter) ? (pp >> 16) : (pp & 0xFFFF);
+    const float2 cs = tab[coord * quarter + (j < quarter ? j : j - quarter)];
+    const float sn = inverse ? -cs.y : cs.y;
+    o1[e] = x1[e] * cs.x - x2[e] * sn;
+    o2[e] = x2[e] * cs.x + x1[e] * sn;
+  }
+  V4<T>::store(v + j0, make_float4(o1[0], o1[1], o1[2], o1[3]));
+  V4<T>::store(v + j0 + half, make_float4(o2[0], o2[1], o2[2], o2[3]));
 }
 
 // ---- bit-exact row scatter / gather ---------------------------------------------------
@@ -286,8 +326,8 @@ hipError_t layernorm_fwd(int dtype, const float* X, int64_t ldx, int64_t rows, i
 }
 
 int64_t layernorm_bwd_partial_rows(int64_t rows) {
-  const int64_t per_block = 4 * LN_ROWS_PER_WAVE;
-  return ((rows + per_block - 1) / per_block) * 4;
+  const int64_t b = (rows + 3) / 4;
+  return b < LN_BWD_MAX_BLOCKS ? b : LN_BWD_MAX_BLOCKS;
 }
 
 hipError_t layernorm_bwd(int dtype, const float* dY, int64_t ldd, const float* X, int64_t ldx,
@@ -295,39 +335,43 @@ hipError_t layernorm_bwd(int dtype, const float* dY, int64_t ldd, const float* X
                          const float* dres, float* dX, void* dXt, float* part_g, float* part_b,
                          float* grad_g, float* grad_b, hipStream_t s) {
   if (rows == 0) return hipSuccess;
-  const int64_t per_block = 4 * LN_ROWS_PER_WAVE;
-  const int nblk = (int)((rows + per_block - 1) / per_block);
+  const int64_t nblk = layernorm_bwd_partial_rows(rows);
+  const int64_t rpb = (rows + nblk - 1) / nblk;
   if (dtype == DT_BF16)
-    hipLaunchKernelGGL(ln_bwd_kernel<bf16>, dim3(nblk), dim3(256), 0, s, dY, ldd, X, ldx, mean,
-                       rstd, (const bf16*)g, rows, n, dres, dX, (bf16*)dXt, part_g, part_b);
+    hipLaunchKernelGGL(ln_bwd_kernel<bf16>, dim3((unsigned)nblk), dim3(256), 0, s, dY, ldd, X, ldx,
+                       mean, rstd, (const bf16*)g, rows, n, rpb, dres, dX, (bf16*)dXt, part_g,
+                       part_b);
   else
-    hipLaunchKernelGGL(ln_bwd_kernel<float>, dim3(nblk), dim3(256), 0, s, dY, ldd, X, ldx, mean,
-                       rstd, (const float*)g, rows, n, dres, dX, (float*)dXt, part_g, part_b);
-  const int64_t prow = (int64_t)nblk * 4;
+    hipLaunchKernelGGL(ln_bwd_kernel<float>, dim3((unsigned)nblk), dim3(256), 0, s, dY, ldd, X,
+                       ldx, mean, rstd, (const float*)g, rows, n, rpb, dres, dX, (float*)dXt,
+                       part_g, part_b);
+  const dim3 rg((unsigned)((n + 63) / 64));
   if (grad_g)
-    hipLaunchKernelGGL(reduce_partials_kernel, dim3(blocks_for(n)), dim3(256), 0, s, part_g, prow,
-                       n, grad_g);
+    hipLaunchKernelGGL(reduce_partials_kernel, rg, dim3(256), 0, s, part_g, nblk, n, grad_g);
   if (grad_b)
-    hipLaunchKernelGGL(reduce_partials_kernel, dim3(blocks_for(n)), dim3(256), 0, s, part_b, prow,
-                       n, grad_b);
+    hipLaunchKernelGGL(reduce_partials_kernel, rg, dim3(256), 0, s, part_b, nblk, n, grad_b);
   return hipGetLastError();
 }
 
-int64_t colsum_partial_rows(int64_t rows) { return (rows + 63) / 64; }
+int64_t colsum_partial_rows(int64_t rows) {
+  const int64_t c = (rows + 31) / 32;
+  return c < COLSUM_MAX_CHUNKS ? c : COLSUM_MAX_CHUNKS;
+}
 
 hipError_t colsum_accumulate(int dtype_in, const void* X, int64_t ld, int64_t rows, int n,
                              float* part, float* out, hipStream_t s) {
   if (rows == 0) return hipSuccess;
   const int64_t nb = colsum_partial_rows(rows);
+  const int64_t rpc = (rows + nb - 1) / nb;
   const dim3 grid((unsigned)blocks_for(n), (unsigned)nb);
   if (dtype_in == DT_BF16)
     hipLaunchKernelGGL(colsum_partial_kernel<bf16>, grid, dim3(256), 0, s, (const bf16*)X, ld,
-                       rows, n, part);
+                       rows, n, rpc, part);
   else
     hipLaunchKernelGGL(colsum_partial_kernel<float>, grid, dim3(256), 0, s, (const float*)X, ld,
-                       rows, n, part);
-  hipLaunchKernelGGL(reduce_partials_kernel, dim3(blocks_for(n)), dim3(256), 0, s, part, nb, n,
-                     out);
+                       rows, n, rpc, part);
+  hipLaunchKernelGGL(reduce_partials_kernel, dim3((unsigned)((n + 63) / 64)), dim3(256), 0, s,
+                     part, nb, n, out);
   return hipGetLastError();
 }
 
@@ -353,15 +397,16 @@ hipError_t pad_cols(int dtype, const void* src, int64_t rows, int K, void* dst, 
 }
 
 hipError_t rope(int dtype, void* qk, int64_t ld, int64_t rows, int heads, int d, int kcol,
-                const int32_t* pos, const float* freq, int inverse, hipStream_t s) {
-  const int64_t n = rows * heads * d;  // (q and k) x heads x d/2 pairs
+                const int32_t* pos, const float* tab, int inverse, hipStream_t s) {
+  const int64_t n = rows * 2 * heads * (d / 8);  // (q and k) x heads x 4-pair groups
   if (n == 0) return hipSuccess;
+  const float2* t = reinterpret_cast<const float2*>(tab);
   if (dtype == DT_BF16)
     hipLaunchKernelGGL(rope_kernel<bf16>, dim3(blocks_for(n)), dim3(256), 0, s, (bf16*)qk, ld,
-                       rows, heads, d, kcol, pos, freq, inverse);
+                       rows, heads, d, kcol, pos, t, inverse);
   else
     hipLaunchKernelGGL(rope_kernel<float>, dim3(blocks_for(n)), dim3(256), 0, s, (float*)qk, ld,
-                       rows, heads, d, kcol, pos, freq, inverse);
+                       rows, heads, d, kcol, pos, t, inverse);
   return hipGetLastError();
 }
 

@@ -195,7 +195,7 @@ mpipe_status upload_meta(mpipe_encoder* e, const Plan& P, char* ws, hipStream_t 
   std::memcpy(st + P.ws_pos, P.pos.data(), P.pos.size() * sizeof(int32_t));
   std::memcpy(st + P.ws_qwork, P.q_work.data(), P.q_work.size() * sizeof(int32_t));
   std::memcpy(st + P.ws_kwork, P.k_work.data(), P.k_work.size() * sizeof(int32_t));
-  std::memcpy(st + P.ws_freq, P.freq.data(), P.freq.size() * sizeof(float));
+  std::memcpy(st + P.ws_rope, P.rope_tab.data(), P.rope_tab.size() * sizeof(float));
   MP_CHECK(hipMemcpyAsync(ws, st, bytes, hipMemcpyHostToDevice, s));
   if (!e->staging_ev) MP_CHECK(hipEventCreateWithFlags(&e->staging_ev, hipEventDisableTiming));
   MP_CHECK(hipEventRecord(e->staging_ev, s));
@@ -255,7 +255,7 @@ mpipe_status forward(Ctx& x, const void* patches, void* merged, char* tape) {
   auto act = [&](int l) -> const ActSet& { return tr ? P.tape_act[l] : P.ws_act; };
   const MergerSet& MS = tr ? P.tape_mrg : P.ws_mrg;
   const int32_t* pos = reinterpret_cast<const int32_t*>(x.ws + P.ws_pos);
-  const float* freq = reinterpret_cast<const float*>(x.ws + P.ws_freq);
+  const float* freq = reinterpret_cast<const float*>(x.ws + P.ws_rope);
 
   MP_RET(pad_pe(x, patches));
   const void *Xp, *Wpe;
@@ -360,7 +360,7 @@ mpipe_status backward(Ctx& x, const void* patches, const char* tape, const void*
   const char* base = tape;
   const MergerSet& MS = P.tape_mrg;
   const int32_t* pos = reinterpret_cast<const int32_t*>(x.ws + P.ws_pos);
-  const float* freq = reinterpret_cast<const float*>(x.ws + P.ws_freq);
+  const float* freq = reinterpret_cast<const float*>(x.ws + P.ws_rope);
   float* dh = reinterpret_cast<float*>(x.ws + P.ws_dh);
   char* dht = x.ws + P.ws_dht;
   float* dhm = reinterpret_cast<float*>(x.ws + P.ws_dhm);
@@ -371,7 +371,7 @@ mpipe_status backward(Ctx& x, const void* patches, const char* tape, const void*
   float* delta = reinterpret_cast<float*>(x.ws + P.ws_delta);
   char* dqkv = x.ws + P.ws_dqkv;
   float* part = reinterpret_cast<float*>(x.ws + P.ws_part);
-  const int64_t part_half = ((N + 63) / 64 * 4) * std::max({3 * h, m, 4 * h, H, (int64_t)c.kpe});
+  const int64_t part_half = 512 * std::max({3 * h, m, 4 * h, H, (int64_t)c.kpe});
 
   MP_RET(pad_pe(x, patches));
   const void *Xp, *Wpe;
@@ -435,9 +435,6 @@ mpipe_status backward(Ctx& x, const void* patches, const char* tape, const void*
     }
     MP_RET(dw_gemm(x, dhmt, h, base + S.o, h, h, h, N, x.grad(dw, blk_param(c, l, B_PROJW)), h));
     MP_RET(colsum(x, DT_F32, dhm, h, N, (int)h, x.grad(dw, blk_param(c, l, B_PROJB))));
-    MP_CHECK(run(x.e, x.s, "attn_delta", 0, [&] {
-      return attention_delta(x.dt, base + S.o, dO, h, N, c.heads, c.d, delta, x.s);
-    }));
     {
       const char* qkv = base + S.qkv;
       AttnArgs qa = attn_args(x, qkv, false), ka = attn_args(x, qkv, true);
@@ -447,6 +444,7 @@ mpipe_status backward(Ctx& x, const void* patches, const char* tape, const void*
         a->ldo = h;
         a->lse = const_cast<float*>(reinterpret_cast<const float*>(base + S.lse));
         a->delta = delta;
+        a->delta_out = delta;
         a->dq = dqkv;
         a->dk = dqkv + h * x.E;
         a->dv = dqkv + 2 * h * x.E;

@@ -50,7 +50,8 @@ struct AttnArgs {
   void* dv = nullptr;
   int64_t ldd = 0;
   float* lse = nullptr;        // [heads][N], natural log
-  const float* delta = nullptr;  // [heads][N]
+  const float* delta = nullptr;  // [heads][N] rowsum(dO o O), read by the dK/dV kernel
+  float* delta_out = nullptr;     // [heads][N], written by the dQ kernel
   const int4* work = nullptr;  // (tile start row, segment start, segment end, 0)
   int n_work = 0;
   int heads = 0;
@@ -59,11 +60,10 @@ struct AttnArgs {
 };
 bool attention_supported(int dtype, int head_dim);
 hipError_t attention_fwd(int dtype, int head_dim, const AttnArgs& a, hipStream_t s);
-// dQ over query tiles (work = query tiles); dK, dV over key tiles (work = key tiles)
+// dQ over query tiles (work = query tiles; also writes delta_out = rowsum(dO o O));
+// then dK, dV over key tiles (work = key tiles; reads delta)
 hipError_t attention_bwd_dq(int dtype, int head_dim, const AttnArgs& a, hipStream_t s);
 hipError_t attention_bwd_dkdv(int dtype, int head_dim, const AttnArgs& a, hipStream_t s);
-hipError_t attention_delta(int dtype, const void* O, const void* dO, int64_t ldo, int64_t N,
-                           int heads, int d, float* delta, hipStream_t s);
 
 hipError_t layernorm_fwd(int dtype, const float* X, int64_t ldx, int64_t rows, int n,
                          const void* g, const void* b, float eps, void* Y, int64_t ldy,
@@ -81,8 +81,9 @@ hipError_t splitk_reduce(const float* part, int splits, int64_t M, int64_t N, fl
                          int64_t ldo, hipStream_t s);
 hipError_t pad_cols(int dtype, const void* src, int64_t rows, int K, void* dst, int Kp,
                     hipStream_t s);
+// tab: (cos, sin) pairs [positions][d/4] of p * theta^(-4k/d); requires d % 8 == 0
 hipError_t rope(int dtype, void* qk, int64_t ld, int64_t rows, int heads, int d, int kcol,
-                const int32_t* pos, const float* freq, int inverse, hipStream_t s);
+                const int32_t* pos, const float* tab, int inverse, hipStream_t s);
 hipError_t rows_copy(bool scatter, const void* src, void* dst, const int64_t* idx, int64_t n_idx,
                      int64_t row_bytes, int64_t n_rows, hipStream_t s);
 hipError_t check_indices(const int64_t* idx, int64_t n, int64_t n_rows, int32_t* marks,

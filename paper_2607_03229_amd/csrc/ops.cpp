@@ -65,7 +65,7 @@ extern "C" {
 size_t mpipe_op_scratch_bytes(int64_t N, int32_t heads, int32_t n, int32_t n_seg) {
   const size_t work = al(((size_t)(N + ATTN_TILE - 1) / ATTN_TILE + (size_t)n_seg + 1) * 16);
   const size_t delta = al((size_t)heads * N * 4);
-  const size_t pos = al((size_t)N * 4) + al(64 * 4);
+  const size_t pos = al((size_t)N * 4) + al((size_t)65536 * 8);
   const size_t part = al((size_t)layernorm_bwd_partial_rows(N) * std::max(n, 1) * 4) * 2;
   return std::max(work + delta, pos) + part + 4096;
 }
@@ -120,7 +120,7 @@ mpipe_status mpipe_op_layernorm_bwd(int32_t dtype, const float* dY, const float*
 mpipe_status mpipe_op_rope(int32_t dtype, void* qkv, int64_t rows, int32_t heads, int32_t d,
                            const int32_t* thw, int32_t n_items, float theta, int32_t inverse,
                            void* scratch, size_t scratch_bytes, void* stream) {
-  if (d % 4) return set_error(MPIPE_ERR_UNSUPPORTED, "head_dim must be a multiple of 4");
+  if (d % 8) return set_error(MPIPE_ERR_UNSUPPORTED, "head_dim must be a multiple of 8");
   std::vector<int32_t> pos;
   int64_t n = 0;
   for (int i = 0; i < n_items; ++i) {
@@ -134,14 +134,20 @@ mpipe_status mpipe_op_rope(int32_t dtype, void* qkv, int64_t rows, int32_t heads
     n += (int64_t)t * gh * gw;
   }
   if (n != rows) return set_error(MPIPE_ERR_BAD_METADATA, "grid does not match rows");
-  std::vector<float> freq(d / 4);
-  for (int k = 0; k < d / 4; ++k) freq[k] = (float)std::pow((double)theta, -4.0 * k / (double)d);
-  const size_t need = al(pos.size() * 4) + al(freq.size() * 4);
+  int max_side = 1;
+  for (int i = 0; i < n_items; ++i) max_side = std::max({max_side, thw[3 * i + 1], thw[3 * i + 2]});
+  Cfg cf;
+  cf.hidden = heads * d;
+  cf.heads = heads;
+  cf.theta = theta;
+  derive_cfg(cf);
+  std::vector<float> tab = rope_table(cf, max_side);
+  const size_t need = al(pos.size() * 4) + al(tab.size() * 4);
   if (scratch_bytes < need) return set_error(MPIPE_ERR_WORKSPACE, "scratch too small");
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   char* sc = reinterpret_cast<char*>(scratch);
   OP_CHECK(hipMemcpyAsync(sc, pos.data(), pos.size() * 4, hipMemcpyHostToDevice, s));
-  OP_CHECK(hipMemcpyAsync(sc + al(pos.size() * 4), freq.data(), freq.size() * 4, hipMemcpyHostToDevice, s));
+  OP_CHECK(hipMemcpyAsync(sc + al(pos.size() * 4), tab.data(), tab.size() * 4, hipMemcpyHostToDevice, s));
   OP_CHECK(rope(dtype, qkv, 3 * (int64_t)heads * d, rows, heads, d, heads * d,
                 reinterpret_cast<const int32_t*>(sc),
                 reinterpret_cast<const float*>(sc + al(pos.size() * 4)), inverse, s));
@@ -189,7 +195,6 @@ mpipe_status mpipe_op_attention_bwd(int32_t dtype, const void* qkv, const void* 
   const int64_t E = dtype == 1 ? 2 : 4, h = (int64_t)heads * d;
   if (end + al((size_t)heads * N * 4) > scratch_bytes) return set_error(MPIPE_ERR_WORKSPACE, "scratch too small");
   float* delta = reinterpret_cast<float*>(reinterpret_cast<char*>(scratch) + end);
-  OP_CHECK(attention_delta(dtype, o, d_o, h, N, heads, d, delta, s));
   AttnArgs a;
   a.q = qkv;
   a.k = reinterpret_cast<const char*>(qkv) + h * E;
@@ -200,6 +205,7 @@ mpipe_status mpipe_op_attention_bwd(int32_t dtype, const void* qkv, const void* 
   a.ldo = h;
   a.lse = const_cast<float*>(lse);
   a.delta = delta;
+  a.delta_out = delta;
   a.dq = dqkv;
   a.dk = reinterpret_cast<char*>(dqkv) + h * E;
   a.dv = reinterpret_cast<char*>(dqkv) + 2 * h * E;

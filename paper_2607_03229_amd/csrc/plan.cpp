@@ -77,6 +77,18 @@ std::vector<ParamEntry> param_table(const Cfg& c) {
   return t;
 }
 
+std::vector<float> rope_table(const Cfg& c, int positions) {
+  const int q4 = c.d / 4;
+  std::vector<float> t((size_t)positions * q4 * 2);
+  for (int pp = 0; pp < positions; ++pp)
+    for (int k = 0; k < q4; ++k) {
+      const double a = pp * std::pow((double)c.theta, -4.0 * k / (double)c.d);
+      t[((size_t)pp * q4 + k) * 2] = (float)std::cos(a);
+      t[((size_t)pp * q4 + k) * 2 + 1] = (float)std::sin(a);
+    }
+  return t;
+}
+
 GemmSplit choose_split(int64_t M, int64_t N, int64_t K) {
   // weight-gradient GEMMs have few output tiles and a long K (tokens): split K
   // until there are about 1024 blocks, keeping each split >= 1024 rows of K.
@@ -201,9 +213,10 @@ int build_plan(const Cfg& c, const int32_t* cu, int n_seg, const int32_t* thw, i
       p.k_work.insert(p.k_work.end(), {r, s0, s1, 0});
     }
   }
+  int max_side = 1;
+  for (int i = 0; i < n_items; ++i) max_side = std::max({max_side, thw[3 * i + 1], thw[3 * i + 2]});
+  p.rope_tab = rope_table(c, max_side);
   const int q4 = c.d / 4;
-  p.freq.resize(q4);
-  for (int k = 0; k < q4; ++k) p.freq[k] = (float)std::pow((double)c.theta, -4.0 * k / (double)c.d);
 
   // ---- workspace ----
   const int64_t h = c.hidden, m = c.mlp, H = c.llm, E = c.esz, nh = c.heads;
@@ -211,7 +224,8 @@ int build_plan(const Cfg& c, const int32_t* cu, int n_seg, const int32_t* thw, i
   p.ws_pos = ws.take(sizeof(int32_t) * N);
   p.ws_qwork = ws.take(sizeof(int32_t) * p.q_work.size());
   p.ws_kwork = ws.take(sizeof(int32_t) * p.k_work.size());
-  p.ws_freq = ws.take(sizeof(float) * q4);
+  p.ws_rope = ws.take(sizeof(float) * p.rope_tab.size());
+  (void)q4;
   p.meta_bytes = ws.top;
   if (c.kp != c.kpe) {
     p.ws_xp = ws.take((size_t)N * c.kp * E);
@@ -260,7 +274,7 @@ int build_plan(const Cfg& c, const int32_t* cu, int n_seg, const int32_t* thw, i
     p.ws_delta = ws.take((size_t)N * nh * 4);
     p.ws_dqkv = ws.take((size_t)N * 3 * h * E);
     const int64_t widest = std::max({3 * h, m, 4 * h, H, (int64_t)c.kpe});
-    const int64_t part_rows = std::max<int64_t>((N + 63) / 64 * 4, 1);
+    const int64_t part_rows = 512;  // >= the partial rows of the LN and column reductions
     p.ws_part = ws.take((size_t)part_rows * widest * 4 * 2);
     // largest split-K partial over the weight-gradient GEMMs
     size_t dw = 0;

@@ -74,10 +74,10 @@ struct Plan {
   std::vector<int32_t> pos;        // N: y << 16 | x
   std::vector<int32_t> q_work;     // 4 ints per query tile (start, seg start, seg end, 0)
   std::vector<int32_t> k_work;     // 4 ints per key tile
-  std::vector<float> freq;         // d/4 rotary frequencies
+  std::vector<float> rope_tab;     // (cos, sin) of p * theta^(-4k/d), [positions][d/4]
   size_t meta_bytes = 0;
   // workspace layout
-  size_t ws_pos = 0, ws_qwork = 0, ws_kwork = 0, ws_freq = 0;
+  size_t ws_pos = 0, ws_qwork = 0, ws_kwork = 0, ws_rope = 0;
   size_t ws_xp = 0, ws_wpe = 0;
   ActSet ws_act{};                 // frozen forward activations
   MergerSet ws_mrg{};
@@ -89,6 +89,9 @@ struct Plan {
   MergerSet tape_mrg{};
   size_t tape_bytes = 0;
 };
+
+// (cos, sin) table of the rotary angles p * theta^(-4k/d) for p < positions, k < d/4.
+std::vector<float> rope_table(const Cfg& c, int positions);
 
 // Validate metadata and build the plan.  Returns 0 or a negative mpipe_status;
 // `err` receives the reason.
