@@ -33,6 +33,7 @@ struct GemmArgs {
   void* C2 = nullptr;
   int64_t ldc2 = 0;
   int beta = 0;
+  int vec = 0;   // set by gemm(): 16-byte epilogue accesses are aligned
 };
 hipError_t gemm(int dtype, int layout, int epi, const GemmArgs& a, hipStream_t s);
 

@@ -90,19 +90,33 @@ std::vector<float> rope_table(const Cfg& c, int positions) {
 }
 
 GemmSplit choose_split(int64_t M, int64_t N, int64_t K) {
-  // weight-gradient GEMMs have few output tiles and a long K (tokens): split K
-  // until there are about 1024 blocks, keeping each split >= 1024 rows of K.
-  const int64_t tiles = ((M + 127) / 128) * ((N + 127) / 128);
-  int64_t s = std::max<int64_t>(1, (1024 + tiles - 1) / tiles);
-  s = std::min<int64_t>(s, std::max<int64_t>(1, K / 1024));
-  s = std::min<int64_t>(s, 16);
+  // Weight-gradient GEMMs have few output tiles and a long K (tokens): split K so
+  // the grid fills whole rounds of 256 CUs (each split keeps >= 1024 rows of K).
+  // Tile size follows the kernel the GEMM dispatches to (256 when M >= 512, N >= 256).
+  const bool big = M >= 512 && N >= 256;
+  const int64_t t = big ? 256 : 128;
+  const int64_t tiles = ((M + t - 1) / t) * ((N + t - 1) / t);
+  const int64_t per_round = big ? 256 : 512;
+  int64_t best = 1;
+  double best_eff = 0.0;
+  for (int64_t s = 1; s <= 16; ++s) {
+    if (s > 1 && K / s < 1024) break;
+    const int64_t blocks = tiles * s;
+    const int64_t rounds = (blocks + per_round - 1) / per_round;
+    const double eff = (double)blocks / (double)(rounds * per_round);
+    if (eff > best_eff + 1e-9) {
+      best_eff = eff;
+      best = s;
+    }
+    if (eff >= 0.9) break;
+  }
   GemmSplit g;
-  if (s <= 1) {
+  if (best <= 1) {
     g.splits = 1;
     g.kps = 0;
     return g;
   }
-  int64_t kps = (K + s - 1) / s;
+  int64_t kps = (K + best - 1) / best;
   kps = (kps + 63) / 64 * 64;
   g.kps = (int)kps;
   g.splits = (int)((K + kps - 1) / kps);

@@ -27,9 +27,11 @@ def _ref_product(layout, A, B):
 
 
 GEMM_SHAPES = {
-    NT: [(300, 200, 256), (1, 8, 8), (129, 257, 72), (512, 384, 1280)],
-    NN: [(300, 200, 256), (129, 264, 72), (77, 8, 520)],
-    TN: [(200, 264, 333), (8, 16, 1), (136, 128, 1000)],
+    # small shapes use the 128x128 kernel; M >= 512 and N >= 256 use the 256x256 kernel
+    NT: [(300, 200, 256), (1, 8, 8), (129, 257, 72), (512, 384, 1280), (700, 520, 200),
+         (1030, 588, 64)],
+    NN: [(300, 200, 256), (129, 264, 72), (77, 8, 520), (600, 264, 136), (777, 1032, 1280)],
+    TN: [(200, 264, 333), (8, 16, 1), (136, 128, 1000), (520, 264, 1000), (1280, 600, 77)],
 }
 
 
@@ -54,12 +56,14 @@ def test_gemm_layouts(dtype, layout):
         assert err < (2e-5 if dtype == "f32" else 1e-5), (M, N, K, err)
 
 
-@pytest.mark.parametrize("dtype", ["bf16", "f32"])
-def test_gemm_epilogues(dtype):
+@pytest.mark.parametrize("dtype,M,N,K", [("bf16", 333, 264, 192), ("f32", 333, 264, 192),
+                                         ("bf16", 700, 392, 256), ("bf16", 530, 300, 64)])
+def test_gemm_epilogues(dtype, M, N, K):
+    """Fused epilogues; (700, 392) and (530, 300) run the 256x256 kernel, the
+    latter with rows whose stride breaks 16-byte alignment (scalar tail path)."""
     import paper_2607_03229_amd as mp
     torch, dev = torch_dev()
     rng = np.random.default_rng(7)
-    M, N, K = 333, 264, 192
     A, B, bias = rnd(rng, (M, K), dtype), rnd(rng, (N, K), dtype, 0.1), rnd(rng, (N,), dtype)
     dA, dB, db = to_dev(A, dtype), to_dev(B, dtype), to_dev(bias, dtype)
     pre = oracle.linear(A, B, bias)
