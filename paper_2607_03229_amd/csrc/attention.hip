@@ -35,56 +35,6 @@ template <int D> struct AD {
 
 // ---- LDS tile helpers ------------------------------------------------------------
 
-// Load rows [r0, r0+64) x D of a head from X (row stride ld) into a row tile with
-// pitch PC chunks, zero-filling rows >= rend.  Optionally also write the
-// transposed tile [D][64] (128-byte rows, swizzled chunks).
-template <int D, bool ROW, bool TR>
-__device__ __forceinline__ void load_tile(uint4* rowt, uint4* trt, const bf16* X, int64_t ld,
-                                          int r0, int rend) {
-  constexpr int NC = AD<D>::NC, PC = AD<D>::PC;
-  const int t = threadIdx.x;
-  if constexpr (TR) {
-    // 16 row-quads x NC d-chunks sub-blocks of 4 rows x 8 d
-    for (int sb = t; sb < 16 * NC; sb += NTHR) {
-      const int rq = sb % 16, dc = sb / 16;
-      uint4 v[4];
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int row = r0 + 4 * rq + j;
-        v[j] = row < rend ? *reinterpret_cast<const uint4*>(X + (int64_t)row * ld + 8 * dc)
-                          : make_uint4(0, 0, 0, 0);
-        if constexpr (ROW) rowt[(4 * rq + j) * PC + dc] = v[j];
-      }
-      const uint32_t* w0 = reinterpret_cast<const uint32_t*>(&v[0]);
-      const uint32_t* w1 = reinterpret_cast<const uint32_t*>(&v[1]);
-      const uint32_t* w2 = reinterpret_cast<const uint32_t*>(&v[2]);
-      const uint32_t* w3 = reinterpret_cast<const uint32_t*>(&v[3]);
-      uint2* t2 = reinterpret_cast<uint2*>(trt);
-#pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        const int pw = i >> 1;
-        uint2 o;
-        if (i & 1) {
-          o.x = pack_hi(w0[pw], w1[pw]);
-          o.y = pack_hi(w2[pw], w3[pw]);
-        } else {
-          o.x = pack_lo(w0[pw], w1[pw]);
-          o.y = pack_lo(w2[pw], w3[pw]);
-        }
-        const int drow = 8 * dc + i;
-        t2[swz(drow, rq >> 1) * 2 + (rq & 1)] = o;
-      }
-    }
-  } else {
-    for (int c = t; c < 64 * NC; c += NTHR) {
-      const int rr = c / NC, dc = c % NC;
-      const int row = r0 + rr;
-      rowt[rr * PC + dc] = row < rend ? *reinterpret_cast<const uint4*>(X + (int64_t)row * ld + 8 * dc)
-                                      : make_uint4(0, 0, 0, 0);
-    }
-  }
-}
-
 // A/B fragment of a 16x16x32 MFMA from a row tile: row `row`, d in [32f + 8g, +8)
 template <int D>
 __device__ __forceinline__ bf16x8 frag_row(const uint4* rowt, int row, int f, int g) {
@@ -98,16 +48,6 @@ __device__ __forceinline__ s16x4 frag_row_rem(const uint4* rowt, int row, int g)
   uint2 v = p[(row * AD<D>::PC + 4 * AD<D>::NF) * 2 + g];
   return *reinterpret_cast<s16x4*>(&v);
 }
-// fragment from a transposed tile: row `row` (a d index), columns {c0..c0+3, c0+16..c0+19}
-__device__ __forceinline__ bf16x8 frag_tr(const uint4* trt, int row, int c0) {
-  const uint2* p = reinterpret_cast<const uint2*>(trt);
-  uint2 a = p[swz(row, c0 >> 3) * 2 + ((c0 >> 2) & 1)];
-  const int c1 = c0 + 16;
-  uint2 b = p[swz(row, c1 >> 3) * 2 + ((c1 >> 2) & 1)];
-  uint4 v = make_uint4(a.x, a.y, b.x, b.y);
-  return *reinterpret_cast<bf16x8*>(&v);
-}
-
 // register fragments of one row (query/key) straight from global memory
 template <int D> struct RowFrag {
   bf16x8 f[AD<D>::NF > 0 ? AD<D>::NF : 1];
@@ -154,13 +94,90 @@ __device__ __forceinline__ bf16x8 pack8(const f32x4& a, const f32x4& b) {
   return r;
 }
 
-// ---- forward ----------------------------------------------------------------------
+// ---- asynchronous tile pipeline ------------------------------------------------------
+// A tile is 64 rows x D of one head, stored row-major in LDS with an odd pitch of PC
+// 16-byte chunks (conflict-free row-fragment reads).  It is filled by 16-byte
+// global->LDS DMA (global_load_lds): lane l of a wave instruction writes LDS slot
+// base + l, so each lane picks the source of its slot; pad slots duplicate chunk 0
+// and rows past the segment read a clamped (valid) row.  Transposed operands come
+// from the same raw tile through ds_read_b64_tr_b16.
+template <int D> struct TG {
+  static constexpr int PC = AD<D>::PC;
+  static constexpr int SLOTS = (64 * PC + 255) / 256 * 256;   // whole wave instructions
+  static constexpr int NI = SLOTS / 256;                       // instructions per wave
+};
+typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 
 template <int D>
+__device__ __forceinline__ void dma_tile(uint4* tile, const bf16* X, int64_t ld, int r0,
+                                         int rlast) {
+  constexpr int PC = AD<D>::PC, NC = AD<D>::NC;
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+#pragma unroll
+  for (int i = 0; i < TG<D>::NI; ++i) {
+    const int inst = i * 4 + w;
+    const int slot = inst * 64 + lane;
+    int row = slot / PC, ch = slot % PC;
+    ch = ch < NC ? ch : 0;
+    int grow = r0 + row;
+    grow = grow < rlast ? grow : rlast;
+    __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(X + (int64_t)grow * ld + 8 * ch),
+                                     (lds_void*)(tile + inst * 64), 16, 0, 0);
+  }
+}
+// 64 floats (one per query of a tile, rows clamped) by a 4-byte DMA from wave 0
+__device__ __forceinline__ void dma_vec64(float* dst, const float* src, int r0, int rlast) {
+  if ((threadIdx.x >> 6) == 0) {
+    int r = r0 + (threadIdx.x & 63);
+    r = r < rlast ? r : rlast;
+    __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(src + r),
+                                     (lds_void*)(dst), 4, 0, 0);
+  }
+}
+// Wait until at most `n` of this wave's vector-memory operations are outstanding
+// (gfx9 s_waitcnt encoding: vmcnt in bits 3:0 and 15:14; expcnt, lgkmcnt left at max).
+template <int n>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(n >= 0 && n < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((n & 15) | (7 << 4) | (15 << 8) | (((n >> 4) & 3) << 14));
+}
+// Workgroup barrier without the release fence of __syncthreads (which would wait for
+// every outstanding DMA); LDS reads are finished before it.
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_s_waitcnt(15 | (7 << 4) | (0 << 8) | (3 << 14));   // lgkmcnt(0)
+  asm volatile("s_barrier" ::: "memory");
+}
+// Transposed fragment of a raw [row][d] tile: for the 16-lane group of this lane,
+// rows {k0a..k0a+3} then {k0b..k0b+3} at column c0 + (lane & 15).
+template <int D>
+__device__ __forceinline__ bf16x8 frag_trt(const uint4* tile, int k0a, int k0b, int c0, int r) {
+  constexpr int PC = AD<D>::PC;
+  const char* base = reinterpret_cast<const char*>(tile);
+  const int off = (r >> 2) * PC * 16 + (c0 + 4 * (r & 3)) * 2;
+  const s16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (lds_s16x4*)(base + k0a * PC * 16 + off));
+  const s16x4 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (lds_s16x4*)(base + k0b * PC * 16 + off));
+  bf16x8 v;
+  const bf16* pa = reinterpret_cast<const bf16*>(&a);
+  const bf16* pb = reinterpret_cast<const bf16*>(&b);
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    v[e] = pa[e];
+    v[4 + e] = pb[e];
+  }
+  return v;
+}
+
+// ---- forward ----------------------------------------------------------------------
+
+// ---- forward ----------------------------------------------------------------------
+// 3-stage pipeline over 64-key tiles: tile t+2 is in flight while tile t is used.
+template <int D>
 __global__ __launch_bounds__(NTHR, 2) void attn_fwd_kernel(AttnArgs p) {
-  constexpr int PC = AD<D>::PC, NDT = AD<D>::NDT;
-  __shared__ uint4 kt_s[64 * PC];   // K tile [key][d]
-  __shared__ uint4 vt_s[D * 8];     // V^T tile [d][key]
+  constexpr int NDT = AD<D>::NDT, SL = TG<D>::SLOTS, NI = TG<D>::NI;
+  __shared__ uint4 k0s[SL], k1s[SL], k2s[SL], v0s[SL], v1s[SL], v2s[SL];
   const int work = blockIdx.x / p.heads, head = blockIdx.x % p.heads;
   const int4 wk = p.work[work];
   const int q0 = wk.x, s0 = wk.y, s1 = wk.z;
@@ -169,6 +186,7 @@ __global__ __launch_bounds__(NTHR, 2) void attn_fwd_kernel(AttnArgs p) {
   const bf16* K = reinterpret_cast<const bf16*>(p.k) + head * D;
   const bf16* V = reinterpret_cast<const bf16*>(p.v) + head * D;
   const float sl2 = p.scale * kLog2e;
+  const int nt = (s1 - s0 + 63) / 64;
 
   RowFrag<D> qf[2];
   int qrow[2];
@@ -184,11 +202,19 @@ __global__ __launch_bounds__(NTHR, 2) void attn_fwd_kernel(AttnArgs p) {
 #pragma unroll
     for (int dt = 0; dt < NDT; ++dt) o[qs][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  for (int k0 = s0; k0 < s1; k0 += 64) {
-    __syncthreads();
-    load_tile<D, true, false>(kt_s, nullptr, K, p.ld, k0, s1);
-    load_tile<D, false, true>(nullptr, vt_s, V, p.ld, k0, s1);
-    __syncthreads();
+  auto issue = [&](int t, uint4* kt, uint4* vt) __attribute__((always_inline)) {
+    if (t < nt) {
+      dma_tile<D>(kt, K, p.ld, s0 + 64 * t, s1 - 1);
+      dma_tile<D>(vt, V, p.ld, s0 + 64 * t, s1 - 1);
+    }
+  };
+  auto body = [&](int t, const uint4* kt_s, const uint4* vt_s, uint4* kn, uint4* vn)
+      __attribute__((always_inline)) {
+    if (t + 1 < nt) wait_vm<2 * NI>();
+    else wait_vm<0>();
+    lds_barrier();
+    issue(t + 2, kn, vn);
+    const int k0 = s0 + 64 * t;
     f32x4 s[4][2];
 #pragma unroll
     for (int kq = 0; kq < 4; ++kq)
@@ -232,11 +258,18 @@ __global__ __launch_bounds__(NTHR, 2) void attn_fwd_kernel(AttnArgs p) {
     for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
       for (int kk = 0; kk < 2; ++kk) {
-        const bf16x8 a = frag_tr(vt_s, 16 * dt + r, 32 * kk + 4 * g);
+        const bf16x8 a = frag_trt<D>(vt_s, 32 * kk + 4 * g, 32 * kk + 16 + 4 * g, 16 * dt, r);
 #pragma unroll
         for (int qs = 0; qs < 2; ++qs)
           o[qs][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb[qs][kk], o[qs][dt], 0, 0, 0);
       }
+  };
+  issue(0, k0s, v0s);
+  issue(1, k1s, v1s);
+  for (int t = 0; t < nt; t += 3) {
+    body(t, k0s, v0s, k2s, v2s);
+    if (t + 1 < nt) body(t + 1, k1s, v1s, k0s, v0s);
+    if (t + 2 < nt) body(t + 2, k2s, v2s, k1s, v1s);
   }
   bf16* O = reinterpret_cast<bf16*>(p.out) + head * D;
 #pragma unroll
@@ -261,13 +294,13 @@ __global__ __launch_bounds__(NTHR, 2) void attn_fwd_kernel(AttnArgs p) {
 }
 
 // ---- backward: dK, dV ------------------------------------------------------------
-
+// Per 128-key tile (32 keys per wave), 3-stage pipeline over 64-query tiles of Q, dO,
+// LSE and delta.
 template <int D>
 __global__ __launch_bounds__(NTHR, 1) void attn_bwd_dkdv_kernel(AttnArgs p) {
-  constexpr int PC = AD<D>::PC, NDT = AD<D>::NDT;
-  __shared__ uint4 q_s[64 * PC], do_s[64 * PC];   // [query][d]
-  __shared__ uint4 qT_s[D * 8], doT_s[D * 8];     // [d][query]
-  __shared__ float lse_s[64], del_s[64];
+  constexpr int NDT = AD<D>::NDT, SL = TG<D>::SLOTS, NI = TG<D>::NI;
+  __shared__ uint4 q0s[SL], q1s[SL], q2s[SL], d0s[SL], d1s[SL], d2s[SL];
+  __shared__ float l0s[64], l1s[64], l2s[64], e0s[64], e1s[64], e2s[64];
   const int work = blockIdx.x / p.heads, head = blockIdx.x % p.heads;
   const int4 wk = p.work[work];
   const int k0 = wk.x, s0 = wk.y, s1 = wk.z;
@@ -275,10 +308,12 @@ __global__ __launch_bounds__(NTHR, 1) void attn_bwd_dkdv_kernel(AttnArgs p) {
   const bf16* Q = reinterpret_cast<const bf16*>(p.q) + head * D;
   const bf16* K = reinterpret_cast<const bf16*>(p.k) + head * D;
   const bf16* V = reinterpret_cast<const bf16*>(p.v) + head * D;
-  const bf16* O = reinterpret_cast<const bf16*>(p.o) + head * D;
-  (void)O;
   const bf16* dO = reinterpret_cast<const bf16*>(p.d_o) + head * D;
+  const float* LSE = p.lse + (int64_t)head * p.N;
+  const float* DEL = p.delta + (int64_t)head * p.N;
   const float sl2 = p.scale * kLog2e;
+  const int nt = (s1 - s0 + 63) / 64;
+  constexpr int PER_TILE = 2 * NI + 2;   // wave 0 issues the two 4-byte vectors too
 
   RowFrag<D> kf[2], vf[2];
 #pragma unroll
@@ -293,31 +328,42 @@ __global__ __launch_bounds__(NTHR, 1) void attn_bwd_dkdv_kernel(AttnArgs p) {
 #pragma unroll
     for (int dt = 0; dt < NDT; ++dt) dk[ks][dt] = dv[ks][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  for (int q0 = s0; q0 < s1; q0 += 64) {
-    __syncthreads();
-    load_tile<D, true, true>(q_s, qT_s, Q, p.ld, q0, s1);
-    load_tile<D, true, true>(do_s, doT_s, dO, p.ldo, q0, s1);
-    if (threadIdx.x < 64) {
-      const int q = q0 + threadIdx.x;
-      lse_s[threadIdx.x] = q < s1 ? p.lse[(int64_t)head * p.N + q] * kLog2e : INFINITY;
-      del_s[threadIdx.x] = q < s1 ? p.delta[(int64_t)head * p.N + q] : 0.f;
+  auto issue = [&](int t, uint4* qt, uint4* dt_, float* lt, float* et)
+      __attribute__((always_inline)) {
+    if (t < nt) {
+      dma_tile<D>(qt, Q, p.ld, s0 + 64 * t, s1 - 1);
+      dma_tile<D>(dt_, dO, p.ldo, s0 + 64 * t, s1 - 1);
+      dma_vec64(lt, LSE, s0 + 64 * t, s1 - 1);
+      dma_vec64(et, DEL, s0 + 64 * t, s1 - 1);
     }
-    __syncthreads();
+  };
+  auto body = [&](int t, const uint4* q_s, const uint4* do_s, const float* lse_s,
+                  const float* del_s, uint4* qn, uint4* dn, float* ln, float* en)
+      __attribute__((always_inline)) {
+    if (w == 0) {
+      if (t + 1 < nt) wait_vm<PER_TILE>();
+      else wait_vm<0>();
+    } else {
+      if (t + 1 < nt) wait_vm<2 * NI>();
+      else wait_vm<0>();
+    }
+    lds_barrier();
+    issue(t + 2, qn, dn, ln, en);
+    const int qb = s0 + 64 * t;
 #pragma unroll
     for (int kk = 0; kk < 2; ++kk) {
-      // S and dP for queries [32kk, 32kk+32) of the tile, keys of this wave
-      f32x4 P[2][2], dS[2][2];   // [qs-in-half][ks]
+      f32x4 P[2][2], dS[2][2];   // [query half][ks]
 #pragma unroll
       for (int h2 = 0; h2 < 2; ++h2) {
-        const int qrow = 16 * (2 * kk + h2) + r;   // A-operand row (query) for this lane
+        const int qrow = 16 * (2 * kk + h2) + r;
 #pragma unroll
         for (int ks = 0; ks < 2; ++ks) {
           f32x4 s = dot_d<D>(q_s, qrow, kf[ks], g, f32x4{0.f, 0.f, 0.f, 0.f});
           f32x4 dp = dot_d<D>(do_s, qrow, vf[ks], g, f32x4{0.f, 0.f, 0.f, 0.f});
 #pragma unroll
           for (int v = 0; v < 4; ++v) {
-            const int qi = 16 * (2 * kk + h2) + 4 * g + v;   // query of output element v
-            const float pp = exp2f(s[v] * sl2 - lse_s[qi]);
+            const int qi = 16 * (2 * kk + h2) + 4 * g + v;
+            const float pp = (qb + qi < s1) ? exp2f(s[v] * sl2 - lse_s[qi] * kLog2e) : 0.f;
             P[h2][ks][v] = pp;
             dS[h2][ks][v] = pp * (dp[v] - del_s[qi]);
           }
@@ -329,13 +375,20 @@ __global__ __launch_bounds__(NTHR, 1) void attn_bwd_dkdv_kernel(AttnArgs p) {
         const bf16x8 ads = pack8(dS[0][ks], dS[1][ks]);
 #pragma unroll
         for (int dt = 0; dt < NDT; ++dt) {
-          const bf16x8 bdo = frag_tr(doT_s, 16 * dt + r, 32 * kk + 4 * g);
-          const bf16x8 bq = frag_tr(qT_s, 16 * dt + r, 32 * kk + 4 * g);
+          const bf16x8 bdo = frag_trt<D>(do_s, 32 * kk + 4 * g, 32 * kk + 16 + 4 * g, 16 * dt, r);
+          const bf16x8 bq = frag_trt<D>(q_s, 32 * kk + 4 * g, 32 * kk + 16 + 4 * g, 16 * dt, r);
           dv[ks][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ap, bdo, dv[ks][dt], 0, 0, 0);
           dk[ks][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ads, bq, dk[ks][dt], 0, 0, 0);
         }
       }
     }
+  };
+  issue(0, q0s, d0s, l0s, e0s);
+  issue(1, q1s, d1s, l1s, e1s);
+  for (int t = 0; t < nt; t += 3) {
+    body(t, q0s, d0s, l0s, e0s, q2s, d2s, l2s, e2s);
+    if (t + 1 < nt) body(t + 1, q1s, d1s, l1s, e1s, q0s, d0s, l0s, e0s);
+    if (t + 2 < nt) body(t + 2, q2s, d2s, l2s, e2s, q1s, d1s, l1s, e1s);
   }
   bf16* dK = reinterpret_cast<bf16*>(p.dk) + head * D;
   bf16* dV = reinterpret_cast<bf16*>(p.dv) + head * D;
@@ -353,13 +406,11 @@ __global__ __launch_bounds__(NTHR, 1) void attn_bwd_dkdv_kernel(AttnArgs p) {
     }
 }
 
-// ---- backward: dQ -----------------------------------------------------------------
-
+// ---- backward: dQ (and delta) --------------------------------------------------------
 template <int D>
 __global__ __launch_bounds__(NTHR, 2) void attn_bwd_dq_kernel(AttnArgs p) {
-  constexpr int PC = AD<D>::PC, NDT = AD<D>::NDT;
-  __shared__ uint4 k_s[64 * PC], v_s[64 * PC];   // [key][d]
-  __shared__ uint4 kT_s[D * 8];                  // [d][key]
+  constexpr int NDT = AD<D>::NDT, SL = TG<D>::SLOTS, NI = TG<D>::NI;
+  __shared__ uint4 k0s[SL], k1s[SL], k2s[SL], v0s[SL], v1s[SL], v2s[SL];
   const int work = blockIdx.x / p.heads, head = blockIdx.x % p.heads;
   const int4 wk = p.work[work];
   const int q0 = wk.x, s0 = wk.y, s1 = wk.z;
@@ -368,9 +419,10 @@ __global__ __launch_bounds__(NTHR, 2) void attn_bwd_dq_kernel(AttnArgs p) {
   const bf16* K = reinterpret_cast<const bf16*>(p.k) + head * D;
   const bf16* V = reinterpret_cast<const bf16*>(p.v) + head * D;
   const bf16* dO = reinterpret_cast<const bf16*>(p.d_o) + head * D;
-  const float sl2 = p.scale * kLog2e;
-
   const bf16* O = reinterpret_cast<const bf16*>(p.o) + head * D;
+  const float sl2 = p.scale * kLog2e;
+  const int nt = (s1 - s0 + 63) / 64;
+
   RowFrag<D> qf[2], dof[2];
   int qrow[2];
   float lse2[2], del[2];
@@ -381,8 +433,8 @@ __global__ __launch_bounds__(NTHR, 2) void attn_bwd_dq_kernel(AttnArgs p) {
     load_rowfrag<D>(qf[qs], Q, p.ld, qc, g);
     load_rowfrag<D>(dof[qs], dO, p.ldo, qc, g);
     lse2[qs] = p.lse[(int64_t)head * p.N + qc] * kLog2e;
-    // delta = rowsum(dO o O): this lane holds d-chunks of its query; the four
-    // lane groups g together cover all d
+    // delta = rowsum(dO o O): each lane holds d-chunks of its query; the four lane
+    // groups together cover all d
     RowFrag<D> of;
     load_rowfrag<D>(of, O, p.ldo, qc, g);
     float dl = 0.f;
@@ -407,22 +459,30 @@ __global__ __launch_bounds__(NTHR, 2) void attn_bwd_dq_kernel(AttnArgs p) {
 #pragma unroll
     for (int dt = 0; dt < NDT; ++dt) dq[qs][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  for (int k0 = s0; k0 < s1; k0 += 64) {
-    __syncthreads();
-    load_tile<D, true, true>(k_s, kT_s, K, p.ld, k0, s1);
-    load_tile<D, true, false>(v_s, nullptr, V, p.ld, k0, s1);
-    __syncthreads();
+  auto issue = [&](int t, uint4* kt, uint4* vt) __attribute__((always_inline)) {
+    if (t < nt) {
+      dma_tile<D>(kt, K, p.ld, s0 + 64 * t, s1 - 1);
+      dma_tile<D>(vt, V, p.ld, s0 + 64 * t, s1 - 1);
+    }
+  };
+  auto body = [&](int t, const uint4* k_s, const uint4* v_s, uint4* kn, uint4* vn)
+      __attribute__((always_inline)) {
+    if (t + 1 < nt) wait_vm<2 * NI>();
+    else wait_vm<0>();
+    lds_barrier();
+    issue(t + 2, kn, vn);
+    const int kb = s0 + 64 * t;
     f32x4 ds[4][2];
 #pragma unroll
     for (int kq = 0; kq < 4; ++kq)
 #pragma unroll
       for (int qs = 0; qs < 2; ++qs) {
-        f32x4 s = dot_d<D>(k_s, 16 * kq + r, qf[qs], g, f32x4{0.f, 0.f, 0.f, 0.f});
+        f32x4 sv = dot_d<D>(k_s, 16 * kq + r, qf[qs], g, f32x4{0.f, 0.f, 0.f, 0.f});
         f32x4 dp = dot_d<D>(v_s, 16 * kq + r, dof[qs], g, f32x4{0.f, 0.f, 0.f, 0.f});
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
-          const int key = k0 + 16 * kq + 4 * g + v;
-          const float pp = key < s1 ? exp2f(s[v] * sl2 - lse2[qs]) : 0.f;
+          const int key = kb + 16 * kq + 4 * g + v;
+          const float pp = key < s1 ? exp2f(sv[v] * sl2 - lse2[qs]) : 0.f;
           ds[kq][qs][v] = pp * (dp[v] - del[qs]);
         }
       }
@@ -433,12 +493,19 @@ __global__ __launch_bounds__(NTHR, 2) void attn_bwd_dq_kernel(AttnArgs p) {
       for (int qs = 0; qs < 2; ++qs) b[qs] = pack8(ds[2 * kk][qs], ds[2 * kk + 1][qs]);
 #pragma unroll
       for (int dt = 0; dt < NDT; ++dt) {
-        const bf16x8 a = frag_tr(kT_s, 16 * dt + r, 32 * kk + 4 * g);
+        const bf16x8 a = frag_trt<D>(k_s, 32 * kk + 4 * g, 32 * kk + 16 + 4 * g, 16 * dt, r);
 #pragma unroll
         for (int qs = 0; qs < 2; ++qs)
           dq[qs][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b[qs], dq[qs][dt], 0, 0, 0);
       }
     }
+  };
+  issue(0, k0s, v0s);
+  issue(1, k1s, v1s);
+  for (int t = 0; t < nt; t += 3) {
+    body(t, k0s, v0s, k2s, v2s);
+    if (t + 1 < nt) body(t + 1, k1s, v1s, k0s, v0s);
+    if (t + 2 < nt) body(t + 2, k2s, v2s, k1s, v1s);
   }
   bf16* dQ = reinterpret_cast<bf16*>(p.dq) + head * D;
 #pragma unroll
