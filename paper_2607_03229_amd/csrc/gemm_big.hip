@@ -1,0 +1,523 @@
+// Large-tile bf16 GEMM for gfx950: the encoder's Linear layers at full size.
+//
+// C[M,N] = sum_k A(m,k) B(n,k) with the same operand layouts and epilogues as the
+// general kernel (NT forward, NN input gradient, TN weight gradient).
+//
+// Block tile 256x256, 256 threads = 4 wave64 in a 2x2 grid; each wave owns a
+// 128x128 tile of 4x4 v_mfma_f32_32x32x16_bf16 accumulators (256 AGPRs).  A
+// 128x128 wave tile keeps the LDS traffic (fragment reads + tile fills) under what
+// the LDS delivers at the full MFMA rate; smaller wave tiles would not.
+//
+// Operand tiles (256 rows x 32 k, 16 KB each) are filled by 16-byte global->LDS DMA
+// (global_load_lds) in a 4-stage ring, so tiles t+1..t+3 are in flight while tile t
+// is multiplied and no tile data passes through VGPRs.  Each lane of a DMA
+// instruction owns one fixed LDS slot and picks the source element of that slot,
+// which is how the tiles get their bank-conflict-free XOR swizzles:
+//   K-contiguous operand ([rows][k]): 64-byte rows, chunk c of row r at c ^ fkc(r);
+//      fragment reads are 16-byte ds_read_b128.
+//   K-major operand ([k][cols]):      512-byte k-rows, chunk c of k-row k at c ^ gkm(k);
+//      fragments come straight from the raw tile through ds_read_b64_tr_b16, so no
+//      operand is ever transposed in registers.
+// Both swizzles keep every fragment read conflict-free whether the LDS serves 128
+// or 256 bytes per cycle.
+//
+// Pipeline per K tile t (stage t % 4): the fragments of its first 16-wide K half are
+// already in registers; the second half's fragments are read while the first half's
+// 16 MFMAs run; then one barrier (tile t+1 landed for every wave, stage t%4 no longer
+// read), the DMA of tile t+4 into stage t%4, and tile t+1's first fragments are read
+// while the second half's MFMAs run.  One barrier per 1024 MFMA cycles per wave.
+// Ragged M/N edges read clamped (valid) rows; a ragged K tail reads clamped rows and
+// zeroes the A fragments past the end.  The epilogue stages each wave's accumulators
+// through LDS, 16 rows at a time, so all epilogue global accesses are 16-byte vectors.
+#include <type_traits>
+
+#include "common.h"
+#include "internal.h"
+
+// (the DMA assembly declares the reserved register M0 clobbered, which clang reports)
+#pragma clang diagnostic ignored "-Winline-asm"
+
+namespace mpipe {
+namespace {
+
+constexpr int BM = 256, BN = 256, BK = 32, NTHR = 256, GROUP_M = 8;
+constexpr int TILE_U4 = BM * BK * 2 / 16;   // 16-byte slots per operand tile (1024)
+constexpr int SP = 136;                     // epilogue staging pitch in floats
+
+typedef __attribute__((ext_vector_type(16))) float f32x16;
+typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+
+// chunk swizzle of a K-contiguous tile (4 chunks per 64-byte row): bit1 = r2, bit0 = r1^r3
+__device__ __forceinline__ int fkc(int r) { return ((r >> 1) & 2) | (((r >> 1) ^ (r >> 3)) & 1); }
+// chunk swizzle of a K-major tile (32 chunks per 512-byte k-row), by k mod 4: 0, 10, 4, 14
+__device__ __forceinline__ int gkm(int k) { return ((k & 1) ? 10 : 0) ^ ((k & 2) ? 4 : 0); }
+
+// The DMAs, and the waits for them, are issued as inline assembly that the compiler
+// does not track: it then inserts no waits of its own for them (its conservative
+// vmcnt(0) before fragment reads would drain the ring once per pass of the loop).
+// This is safe because the main loop has no other vector-memory instructions and
+// every DMA is waited for (wait_vm<0>) before the epilogue's loads.
+template <int n>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(n >= 0 && n < 64, "vmcnt range");
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(n) : "memory");
+}
+// Barrier after this wave's LDS reads have completed; no fence for the DMAs in flight.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return (uint32_t)(size_t)(lds_void*)p;
+}
+
+// ---- DMA sources ---------------------------------------------------------------------
+// Wave w issues instructions q = 4w + i (i < 4) of each operand tile; instruction q
+// fills LDS slots 64q..64q+63, lane l slot 64q + l.
+
+// K-contiguous operand X[rows][ld], tile rows r0.., k from k0: slot (row 16q + l/4,
+// physical chunk l%4) holds logical chunk (l%4) ^ fkc(row).
+__device__ __forceinline__ const bf16* src_kc(const bf16* X, int64_t ld, int rows, int r0, int k0,
+                                              int kend, int i) {
+  const int w = threadIdx.x >> 6, l = threadIdx.x & 63;
+  const int q = 4 * w + i;
+  const int row = 16 * q + (l >> 2);
+  int k = k0 + 8 * ((l & 3) ^ fkc(row));
+  k = k < kend ? k : kend - 8;
+  int gr = r0 + row;
+  gr = gr < rows ? gr : rows - 1;
+  return X + (int64_t)gr * ld + k;
+}
+// K-major operand X[k][ld], tile cols c0.., k-rows from k0: slot (k-row 2q + l/32,
+// physical chunk l%32) holds logical chunk (l%32) ^ gkm(k-row).
+__device__ __forceinline__ const bf16* src_km(const bf16* X, int64_t ld, int cols, int c0, int k0,
+                                              int kend, int i) {
+  const int w = threadIdx.x >> 6, l = threadIdx.x & 63;
+  const int q = 4 * w + i;
+  const int kr = 2 * q + (l >> 5);
+  int col = c0 + 8 * ((l & 31) ^ gkm(kr));
+  col = col < cols ? col : cols - 8;
+  int k = k0 + kr;
+  k = k < kend ? k : kend - 1;
+  return X + (int64_t)k * ld + col;
+}
+// 16-byte global->LDS DMA of instruction q = 4w + i: lane l writes LDS byte
+// tile + 1024 q + 16 l (M0 holds the wave-uniform base).
+// M0 is declared clobbered; nothing else in these kernels keeps a value in it.
+__device__ __forceinline__ void dma16(const bf16* src, const uint4* tile, int i) {
+  const uint32_t base = lds_addr(tile) + 1024u * (4 * (threadIdx.x >> 6) + i);
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+               ::"v"(src), "s"(__builtin_amdgcn_readfirstlane(base)) : "memory", "m0");
+}
+
+// ---- epilogue ------------------------------------------------------------------------
+
+// 8 consecutive outputs (m, n..n+7) through the epilogue, vectorised
+template <int EPI>
+__device__ __forceinline__ void epi8(const GemmArgs& p, int split, int m, int n, float* v,
+                                     bool vec) {
+  const bf16* bias = reinterpret_cast<const bf16*>(p.bias);
+  if (vec) {
+    if (bias != nullptr && split == 0) {
+      const uint4 bb = *reinterpret_cast<const uint4*>(bias + n);
+      const bf16* b8 = reinterpret_cast<const bf16*>(&bb);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] += (float)b8[e];
+    }
+    if constexpr (EPI == EPI_STORE || EPI == EPI_GELU || EPI == EPI_GELU_BWD) {
+      bf16 o[8];
+      if constexpr (EPI == EPI_STORE) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) o[e] = (bf16)v[e];
+      } else if constexpr (EPI == EPI_GELU) {
+        bf16 pre[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          pre[e] = (bf16)v[e];
+          o[e] = (bf16)gelu_f((float)pre[e]);
+        }
+        if (p.C2)
+          *reinterpret_cast<uint4*>(reinterpret_cast<bf16*>(p.C2) + (int64_t)m * p.ldc2 + n) =
+              *reinterpret_cast<const uint4*>(pre);
+      } else {
+        const uint4 uu = *reinterpret_cast<const uint4*>(reinterpret_cast<const bf16*>(p.aux) +
+                                                         (int64_t)m * p.ld_aux + n);
+        const bf16* u8 = reinterpret_cast<const bf16*>(&uu);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) o[e] = (bf16)(v[e] * gelu_grad_f((float)u8[e]));
+      }
+      *reinterpret_cast<uint4*>(reinterpret_cast<bf16*>(p.C) + (int64_t)m * p.ldc + n) =
+          *reinterpret_cast<const uint4*>(o);
+    } else if constexpr (EPI == EPI_RESID) {
+      const float* R = reinterpret_cast<const float*>(p.aux);
+      float4 r0 = make_float4(0.f, 0.f, 0.f, 0.f), r1 = r0;
+      if (R) {
+        r0 = *reinterpret_cast<const float4*>(R + (int64_t)m * p.ld_aux + n);
+        r1 = *reinterpret_cast<const float4*>(R + (int64_t)m * p.ld_aux + n + 4);
+      }
+      float* C = reinterpret_cast<float*>(p.C) + (int64_t)m * p.ldc + n;
+      *reinterpret_cast<float4*>(C) =
+          make_float4(r0.x + v[0], r0.y + v[1], r0.z + v[2], r0.w + v[3]);
+      *reinterpret_cast<float4*>(C + 4) =
+          make_float4(r1.x + v[4], r1.y + v[5], r1.z + v[6], r1.w + v[7]);
+    } else {  // EPI_F32
+      float* C = reinterpret_cast<float*>(p.C) + (int64_t)split * p.split_stride +
+                 (int64_t)m * p.ldc + n;
+      float4 a = make_float4(v[0], v[1], v[2], v[3]), b = make_float4(v[4], v[5], v[6], v[7]);
+      if (p.beta) {
+        const float4 c0 = *reinterpret_cast<const float4*>(C);
+        const float4 c1 = *reinterpret_cast<const float4*>(C + 4);
+        a.x += c0.x; a.y += c0.y; a.z += c0.z; a.w += c0.w;
+        b.x += c1.x; b.y += c1.y; b.z += c1.z; b.w += c1.w;
+      }
+      *reinterpret_cast<float4*>(C) = a;
+      *reinterpret_cast<float4*>(C + 4) = b;
+    }
+    return;
+  }
+  // scalar tail (ragged N or unaligned strides)
+  for (int e = 0; e < 8; ++e) {
+    const int nn = n + e;
+    if (nn >= p.N) break;
+    float x = v[e] + ((bias != nullptr && split == 0) ? (float)bias[nn] : 0.f);
+    if constexpr (EPI == EPI_STORE) {
+      reinterpret_cast<bf16*>(p.C)[(int64_t)m * p.ldc + nn] = (bf16)x;
+    } else if constexpr (EPI == EPI_GELU) {
+      const bf16 pre = (bf16)x;
+      if (p.C2) reinterpret_cast<bf16*>(p.C2)[(int64_t)m * p.ldc2 + nn] = pre;
+      reinterpret_cast<bf16*>(p.C)[(int64_t)m * p.ldc + nn] = (bf16)gelu_f((float)pre);
+    } else if constexpr (EPI == EPI_RESID) {
+      const float* R = reinterpret_cast<const float*>(p.aux);
+      const float base = R ? R[(int64_t)m * p.ld_aux + nn] : 0.f;
+      reinterpret_cast<float*>(p.C)[(int64_t)m * p.ldc + nn] = base + x;
+    } else if constexpr (EPI == EPI_GELU_BWD) {
+      const float u = (float)reinterpret_cast<const bf16*>(p.aux)[(int64_t)m * p.ld_aux + nn];
+      reinterpret_cast<bf16*>(p.C)[(int64_t)m * p.ldc + nn] = (bf16)(x * gelu_grad_f(u));
+    } else {
+      float* C = reinterpret_cast<float*>(p.C) + (int64_t)split * p.split_stride;
+      const int64_t o = (int64_t)m * p.ldc + nn;
+      C[o] = p.beta ? C[o] + x : x;
+    }
+  }
+}
+
+// ---- the kernel ----------------------------------------------------------------------
+
+template <bool AK, bool BKM, int EPI>
+__global__ __launch_bounds__(NTHR, 1) void gemm_big_kernel(GemmArgs p) {
+  // one LDS object per stage and operand, so the compiler can tell a fragment read
+  // of one stage from the DMAs still writing another
+  __shared__ uint4 sa0[TILE_U4], sa1[TILE_U4], sa2[TILE_U4], sa3[TILE_U4];
+  __shared__ uint4 sb0[TILE_U4], sb1[TILE_U4], sb2[TILE_U4], sb3[TILE_U4];
+
+  // XCD-aware block order (consecutive block ids go round-robin to the 8 XCDs), then
+  // groups of GROUP_M tile-rows for L2 reuse
+  const int ntiles = p.tiles_m * p.tiles_n;
+  const int nb = gridDim.x;
+  const int b = blockIdx.x;
+  const int pid = (b % 8) * (nb / 8) + (b / 8);
+  if (pid >= ntiles) return;
+  const int group = pid / (GROUP_M * p.tiles_n);
+  const int first_m = group * GROUP_M;
+  const int gsize = min(p.tiles_m - first_m, GROUP_M);
+  const int tm = first_m + (pid % gsize);
+  const int tn = (pid % (GROUP_M * p.tiles_n)) / gsize;
+  const int split = blockIdx.y;
+  const int m0 = tm * BM, n0 = tn * BN;
+  const int kbeg = split * p.kps;
+  const int kend = min(p.K, kbeg + p.kps);
+  const int nk = kend > kbeg ? (kend - kbeg + BK - 1) / BK : 0;
+  const bf16* A = reinterpret_cast<const bf16*>(p.A);
+  const bf16* B = reinterpret_cast<const bf16*>(p.B);
+  const int w = threadIdx.x >> 6, l = threadIdx.x & 63;
+  const int wm = w >> 1, wn = w & 1;
+
+  f32x16 acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+
+  // per-lane DMA sources of the first K tile; a full tile t adds t*BK (K-contiguous)
+  // or t*BK*ld (K-major) elements
+  const bf16* sA[4];
+  const bf16* sB[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    sA[i] = AK ? src_km(A, p.lda, p.M, m0, kbeg, kend, i) : src_kc(A, p.lda, p.M, m0, kbeg, kend, i);
+    sB[i] = BKM ? src_km(B, p.ldb, p.N, n0, kbeg, kend, i) : src_kc(B, p.ldb, p.N, n0, kbeg, kend, i);
+  }
+  const int64_t stepA = AK ? (int64_t)BK * p.lda : BK;
+  const int64_t stepB = BKM ? (int64_t)BK * p.ldb : BK;
+
+  auto dma_tile = [&](uint4* ta, uint4* tb, int t) __attribute__((always_inline)) {
+    const int k0 = kbeg + t * BK;
+    if (k0 + BK <= kend) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        dma16(sA[i] + t * stepA, ta, i);
+        dma16(sB[i] + t * stepB, tb, i);
+      }
+    } else {   // ragged last tile: clamped sources
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        dma16(AK ? src_km(A, p.lda, p.M, m0, k0, kend, i) : src_kc(A, p.lda, p.M, m0, k0, kend, i),
+              ta, i);
+        dma16(BKM ? src_km(B, p.ldb, p.N, n0, k0, kend, i) : src_kc(B, p.ldb, p.N, n0, k0, kend, i),
+              tb, i);
+      }
+    }
+  };
+
+  // Per-lane fragment offsets (bytes).  K-contiguous block of 32 rows at row base rb:
+  // lane reads row rb + l%32, logical chunk 2h + l/32 -> rb*64 + (koff ^ 32h), since
+  // fkc depends only on the row bits below 32.
+  const int kc_off = 64 * (l & 31) + 16 * ((l >> 5) ^ fkc(l & 31));
+  // K-major block of 32 cols at col base cb = 128 wv + 32 i: 16-lane group G = l/16
+  // reads k-rows 8(G/2) + (l%16)/4 (+4 for the second read, +16 for the second K half)
+  // at col cb + 16(G%2) + 4(l%4); the swizzle makes the chunk depend on i.
+  int km_off[4];
+  {
+    const int G = l >> 4, j = l & 15;
+    const int kr = 8 * (G >> 1) + (j >> 2);
+    const int gg = gkm(j >> 2);
+    const int lo = 2 * (G & 1) + ((j & 3) >> 1);
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      km_off[i] = kr * 512 + 16 * ((4 * (i ^ (gg >> 2))) + (lo ^ (gg & 3))) + 8 * (j & 1);
+  }
+
+  // fragments of K half h (16 k) of a stage: operand rows/cols of wave (wm, wn)
+  auto frag_kc = [&](const uint4* t, int rb, int h) __attribute__((always_inline)) -> bf16x8 {
+    const char* base = reinterpret_cast<const char*>(t) + rb * 64;
+    const uint4 v = *reinterpret_cast<const uint4*>(base + (kc_off ^ (32 * h)));
+    return *reinterpret_cast<const bf16x8*>(&v);
+  };
+  auto frag_km = [&](const uint4* t, int wv, int i, int h) __attribute__((always_inline)) -> bf16x8 {
+    const char* base = reinterpret_cast<const char*>(t) + 16 * 16 * wv + h * 16 * 512 + km_off[i];
+    const s16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(base));
+    const s16x4 c = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(base + 4 * 512));
+    bf16x8 v;
+    const bf16* pa = reinterpret_cast<const bf16*>(&a);
+    const bf16* pc = reinterpret_cast<const bf16*>(&c);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      v[e] = pa[e];
+      v[4 + e] = pc[e];
+    }
+    return v;
+  };
+  bf16x8 fa[2][4], fb[2][4];
+  auto read_frags = [&](const uint4* ta, const uint4* tb, int h, int t, bf16x8 (&a)[4],
+                        bf16x8 (&bb)[4]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      a[i] = AK ? frag_km(ta, wm, i, h) : frag_kc(ta, wm * 128 + 32 * i, h);
+      bb[i] = BKM ? frag_km(tb, wn, i, h) : frag_kc(tb, wn * 128 + 32 * i, h);
+    }
+    // ragged K tail: zero the A elements past kend (B there holds clamped, finite data)
+    const int kr = kend - (kbeg + t * BK) - 16 * h - 8 * (l >> 5);
+    if (kend - (kbeg + t * BK) < BK) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          if (e >= kr) a[i][e] = (bf16)0.f;
+    }
+  };
+  auto mma = [&](const bf16x8 (&a)[4], const bf16x8 (&bb)[4]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], bb[j], acc[i][j], 0, 0, 0);
+  };
+  auto stage_a = [&](auto S) -> uint4* {
+    constexpr int s = decltype(S)::value;
+    if constexpr (s == 0) return sa0;
+    else if constexpr (s == 1) return sa1;
+    else if constexpr (s == 2) return sa2;
+    else return sa3;
+  };
+  auto stage_b = [&](auto S) -> uint4* {
+    constexpr int s = decltype(S)::value;
+    if constexpr (s == 0) return sb0;
+    else if constexpr (s == 1) return sb1;
+    else if constexpr (s == 2) return sb2;
+    else return sb3;
+  };
+
+  // one K tile t in stage S; fa[0]/fb[0] hold its first half on entry and the next
+  // tile's first half on exit
+  auto body = [&](auto S, int t) __attribute__((always_inline)) {
+    constexpr int s = decltype(S)::value;
+    using SN = std::integral_constant<int, (s + 1) & 3>;
+    read_frags(stage_a(S), stage_b(S), 1, t, fa[1], fb[1]);
+    mma(fa[0], fb[0]);
+    // tile t+1 has landed for this wave once at most the later tiles' DMAs are pending
+    const int later = nk - 2 - t;   // tiles issued after t+1 (at most 2)
+    if (later >= 2) wait_vm<16>();
+    else if (later == 1) wait_vm<8>();
+    else wait_vm<0>();
+    lds_barrier();
+    if (t + 4 < nk) dma_tile(stage_a(S), stage_b(S), t + 4);
+    if (t + 1 < nk) read_frags(stage_a(SN{}), stage_b(SN{}), 0, t + 1, fa[0], fb[0]);
+    mma(fa[1], fb[1]);
+  };
+
+  // Steady-state tile (t + 9 <= nk at the start of the pass): the same work as body(),
+  // with each fragment read and DMA placed between two MFMAs in a fixed order
+  // (sched_barrier fences), so the MFMA pipe never waits behind a burst of memory
+  // instructions.
+  auto rd1 = [&](const uint4* ta, const uint4* tb, int h, int k, bf16x8 (&a)[4],
+                 bf16x8 (&bb)[4]) __attribute__((always_inline)) {
+    // in the order the MFMAs (i-major) first use them: A0, B0, B1, B2, B3, A1, A2, A3
+    const bool isb = k >= 1 && k <= 4;
+    const int i = k == 0 ? 0 : isb ? k - 1 : k - 4;
+    if (isb) bb[i] = BKM ? frag_km(tb, wn, i, h) : frag_kc(tb, wn * 128 + 32 * i, h);
+    else a[i] = AK ? frag_km(ta, wm, i, h) : frag_kc(ta, wm * 128 + 32 * i, h);
+  };
+  auto mf1 = [&](int n, const bf16x8 (&a)[4], const bf16x8 (&bb)[4]) __attribute__((always_inline)) {
+    acc[n >> 2][n & 3] =
+        __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[n >> 2], bb[n & 3], acc[n >> 2][n & 3], 0, 0, 0);
+  };
+  auto dm1 = [&](uint4* ta, uint4* tb, int t, int q) __attribute__((always_inline)) {
+    if (q < 4) dma16(sA[q] + t * stepA, ta, q);
+    else dma16(sB[q - 4] + t * stepB, tb, q - 4);
+  };
+  auto body_full = [&](auto S, int t) __attribute__((always_inline)) {
+    constexpr int s = decltype(S)::value;
+    using SN = std::integral_constant<int, (s + 1) & 3>;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      rd1(stage_a(S), stage_b(S), 1, q, fa[1], fb[1]);
+      __builtin_amdgcn_sched_barrier(0);
+      mf1(2 * q, fa[0], fb[0]);
+      __builtin_amdgcn_sched_barrier(0);
+      mf1(2 * q + 1, fa[0], fb[0]);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    wait_vm<16>();
+    lds_barrier();
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      dm1(stage_a(S), stage_b(S), t + 4, q);
+      __builtin_amdgcn_sched_barrier(0);
+      mf1(2 * q, fa[1], fb[1]);
+      __builtin_amdgcn_sched_barrier(0);
+      rd1(stage_a(SN{}), stage_b(SN{}), 0, q, fa[0], fb[0]);
+      __builtin_amdgcn_sched_barrier(0);
+      mf1(2 * q + 1, fa[1], fb[1]);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+
+  using S0 = std::integral_constant<int, 0>;
+  using S1 = std::integral_constant<int, 1>;
+  using S2 = std::integral_constant<int, 2>;
+  using S3 = std::integral_constant<int, 3>;
+  if (nk > 0) {
+    dma_tile(sa0, sb0, 0);
+    if (nk > 1) dma_tile(sa1, sb1, 1);
+    if (nk > 2) dma_tile(sa2, sb2, 2);
+    if (nk > 3) dma_tile(sa3, sb3, 3);
+    if (nk > 3) wait_vm<24>();
+    else if (nk == 3) wait_vm<16>();
+    else if (nk == 2) wait_vm<8>();
+    else wait_vm<0>();
+    lds_barrier();
+    read_frags(sa0, sb0, 0, 0, fa[0], fb[0]);
+    int t = 0;
+    // steady state: the tiles read (<= t+4) and the tiles DMA'd (<= t+7) all precede the
+    // last, possibly ragged, tile, so every source is unclamped and in bounds
+    for (; t + 9 <= nk; t += 4) {
+      body_full(S0{}, t);
+      body_full(S1{}, t + 1);
+      body_full(S2{}, t + 2);
+      body_full(S3{}, t + 3);
+    }
+    for (; t < nk; t += 4) {
+      body(S0{}, t);
+      if (t + 1 < nk) body(S1{}, t + 1);
+      if (t + 2 < nk) body(S2{}, t + 2);
+      if (t + 3 < nk) body(S3{}, t + 3);
+    }
+  }
+
+  // epilogue: each wave stages 16x128 accumulator rows at a time in its own LDS tile
+  // (the last barrier of the loop ended every fragment read)
+  __syncthreads();
+  uint4* own = w == 0 ? sa0 : w == 1 ? sa1 : w == 2 ? sa2 : sa3;
+  float* stage = reinterpret_cast<float*>(own);
+  static_assert(16 * SP * 4 <= TILE_U4 * 16, "epilogue staging must fit in one tile");
+  const int cg = l & 15;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {     // (acc[i] must be indexed statically)
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh) {
+      __syncthreads();
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int e = 8 * hh; e < 8 * hh + 8; ++e) {
+          const int rr = 8 * ((e >> 2) & 1) + 4 * (l >> 5) + (e & 3);
+          stage[rr * SP + 32 * j + (l & 31)] = acc[i][j][e];
+        }
+      __syncthreads();
+#pragma unroll 1
+      for (int u = 0; u < 4; ++u) {
+        const int rr = (l >> 4) + 4 * u;
+        const int m = m0 + wm * 128 + 32 * i + 16 * hh + rr;
+        const int n = n0 + wn * 128 + 8 * cg;
+        if (m >= p.M || n >= p.N) continue;
+        float v[8];
+        const float4 x0 = *reinterpret_cast<const float4*>(stage + rr * SP + 8 * cg);
+        const float4 x1 = *reinterpret_cast<const float4*>(stage + rr * SP + 8 * cg + 4);
+        v[0] = x0.x; v[1] = x0.y; v[2] = x0.z; v[3] = x0.w;
+        v[4] = x1.x; v[5] = x1.y; v[6] = x1.z; v[7] = x1.w;
+        epi8<EPI>(p, split, m, n, v, p.vec && n + 8 <= p.N);
+      }
+    }
+  }
+}
+
+template <bool AK, bool BKM, int EPI>
+hipError_t launch_big(const GemmArgs& a0, hipStream_t s) {
+  GemmArgs a = a0;
+  a.tiles_m = (a.M + BM - 1) / BM;
+  a.tiles_n = (a.N + BN - 1) / BN;
+  const int nt = a.tiles_m * a.tiles_n;
+  const int nb = (nt + 7) / 8 * 8;
+  int splits = a.kps > 0 ? (a.K + a.kps - 1) / a.kps : 1;
+  if (a.kps <= 0) a.kps = a.K;
+  if (splits < 1) splits = 1;
+  hipLaunchKernelGGL((gemm_big_kernel<AK, BKM, EPI>), dim3(nb, splits), dim3(NTHR), 0, s, a);
+  return hipGetLastError();
+}
+
+template <bool AK, bool BKM>
+hipError_t dispatch_big(const GemmArgs& a, int epi, hipStream_t s) {
+  switch (epi) {
+    case EPI_STORE: return launch_big<AK, BKM, EPI_STORE>(a, s);
+    case EPI_GELU: return launch_big<AK, BKM, EPI_GELU>(a, s);
+    case EPI_RESID: return launch_big<AK, BKM, EPI_RESID>(a, s);
+    case EPI_GELU_BWD: return launch_big<AK, BKM, EPI_GELU_BWD>(a, s);
+    case EPI_F32: return launch_big<AK, BKM, EPI_F32>(a, s);
+  }
+  return hipErrorInvalidValue;
+}
+
+}  // namespace
+
+hipError_t gemm_big(int layout, int epi, const GemmArgs& a, hipStream_t s) {
+  switch (layout) {
+    case GEMM_NT: return dispatch_big<false, false>(a, epi, s);
+    case GEMM_NN: return dispatch_big<false, true>(a, epi, s);
+    case GEMM_TN: return dispatch_big<true, true>(a, epi, s);
+  }
+  return hipErrorInvalidValue;
+}
+
+}  // namespace mpipe

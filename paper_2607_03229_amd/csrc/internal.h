@@ -36,6 +36,8 @@ struct GemmArgs {
   int vec = 0;   // set by gemm(): 16-byte epilogue accesses are aligned
 };
 hipError_t gemm(int dtype, int layout, int epi, const GemmArgs& a, hipStream_t s);
+// 256x256-tile bf16 kernel (M >= 512, N >= 256), same contract as gemm()
+hipError_t gemm_big(int layout, int epi, const GemmArgs& a, hipStream_t s);
 
 struct AttnArgs {
   const void* q = nullptr;     // Q, K, V column blocks, row stride ld (head h at column h*d)

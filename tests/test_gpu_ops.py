@@ -28,10 +28,14 @@ def _ref_product(layout, A, B):
 
 GEMM_SHAPES = {
     # small shapes use the 128x128 kernel; M >= 512 and N >= 256 use the 256x256 kernel
+    # (the large kernel's K pipeline: 1 to 3 tiles, ragged last tiles, several passes)
     NT: [(300, 200, 256), (1, 8, 8), (129, 257, 72), (512, 384, 1280), (700, 520, 200),
-         (1030, 588, 64)],
-    NN: [(300, 200, 256), (129, 264, 72), (77, 8, 520), (600, 264, 136), (777, 1032, 1280)],
-    TN: [(200, 264, 333), (8, 16, 1), (136, 128, 1000), (520, 264, 1000), (1280, 600, 77)],
+         (1030, 588, 64), (600, 300, 24), (520, 264, 96), (515, 260, 168), (520, 264, 264),
+         (530, 256, 1000)],
+    NN: [(300, 200, 256), (129, 264, 72), (77, 8, 520), (600, 264, 136), (777, 1032, 1280),
+         (530, 280, 40)],
+    TN: [(200, 264, 333), (8, 16, 1), (136, 128, 1000), (520, 264, 1000), (1280, 600, 77),
+         (512, 256, 5), (600, 392, 63), (600, 392, 250), (520, 264, 291)],
 }
 
 
@@ -98,13 +102,14 @@ def test_gemm_epilogues(dtype, M, N, K):
     assert max_rel(host(C), R + oracle.linear(A, B)) < 2e-5
 
 
-@pytest.mark.parametrize("dtype", ["bf16", "f32"])
-def test_gemm_split_k(dtype):
+@pytest.mark.parametrize("dtype,M,N", [("bf16", 136, 264), ("f32", 136, 264),
+                                       ("bf16", 520, 264)])
+def test_gemm_split_k(dtype, M, N):
     import paper_2607_03229_amd as mp
     torch, dev = torch_dev()
     rng = np.random.default_rng(3)
-    M, N, K, kps = 136, 264, 1000, 256
-    announce(f"gemm split-k {dtype}")
+    K, kps = 1000, 256
+    announce(f"gemm split-k {dtype} M={M} N={N}")
     A, B = rnd(rng, (K, M), dtype), rnd(rng, (K, N), dtype)
     splits = (K + kps - 1) // kps
     part = zeros((splits, M, N), "f32")
