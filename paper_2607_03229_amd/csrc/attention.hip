@@ -24,6 +24,10 @@ namespace mpipe {
 namespace {
 
 constexpr int NTHR = 256;
+// 16-row sub-tiles per wave (NS) of the bf16 kernels; a 128-row work tile takes 8 / NS
+// waves.  NS = 4 reuses each LDS fragment over four MFMAs (half the LDS traffic of NS = 2)
+// at one wave per SIMD; NS = 2 runs two blocks of four waves per CU.
+constexpr int FWD_NS = 2, DQ_NS = 2, DKDV_NS = 2;
 
 template <int D> struct AD {
   static constexpr int NC = D / 8;                          // 16-byte chunks per row
@@ -101,22 +105,22 @@ __device__ __forceinline__ bf16x8 pack8(const f32x4& a, const f32x4& b) {
 // base + l, so each lane picks the source of its slot; pad slots duplicate chunk 0
 // and rows past the segment read a clamped (valid) row.  Transposed operands come
 // from the same raw tile through ds_read_b64_tr_b16.
-template <int D> struct TG {
+template <int D, int NW> struct TG {
   static constexpr int PC = AD<D>::PC;
-  static constexpr int SLOTS = (64 * PC + 255) / 256 * 256;   // whole wave instructions
-  static constexpr int NI = SLOTS / 256;                       // instructions per wave
+  static constexpr int SLOTS = (64 * PC + 64 * NW - 1) / (64 * NW) * (64 * NW);   // whole
+  static constexpr int NI = SLOTS / (64 * NW);   // wave instructions; instructions per wave
 };
 typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 
-template <int D>
+template <int D, int NW>
 __device__ __forceinline__ void dma_tile(uint4* tile, const bf16* X, int64_t ld, int r0,
                                          int rlast) {
   constexpr int PC = AD<D>::PC, NC = AD<D>::NC;
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
 #pragma unroll
-  for (int i = 0; i < TG<D>::NI; ++i) {
-    const int inst = i * 4 + w;
+  for (int i = 0; i < TG<D, NW>::NI; ++i) {
+    const int inst = i * NW + w;
     const int slot = inst * 64 + lane;
     int row = slot / PC, ch = slot % PC;
     ch = ch < NC ? ch : 0;
@@ -174,9 +178,10 @@ __device__ __forceinline__ bf16x8 frag_trt(const uint4* tile, int k0a, int k0b, 
 
 // ---- forward ----------------------------------------------------------------------
 // 3-stage pipeline over 64-key tiles: tile t+2 is in flight while tile t is used.
-template <int D>
-__global__ __launch_bounds__(NTHR, 2) void attn_fwd_kernel(AttnArgs p) {
-  constexpr int NDT = AD<D>::NDT, SL = TG<D>::SLOTS, NI = TG<D>::NI;
+template <int D, int NS>
+__global__ __launch_bounds__(64 * (8 / NS), NS == 2 ? 2 : 1) void attn_fwd_kernel(AttnArgs p) {
+  constexpr int NW = 8 / NS, RW = 16 * NS;   // waves per block, rows per wave
+  constexpr int NDT = AD<D>::NDT, SL = TG<D, NW>::SLOTS, NI = TG<D, NW>::NI;
   __shared__ uint4 k0s[SL], k1s[SL], k2s[SL], v0s[SL], v1s[SL], v2s[SL];
   const int work = blockIdx.x / p.heads, head = blockIdx.x % p.heads;
   const int4 wk = p.work[work];
@@ -188,24 +193,29 @@ __global__ __launch_bounds__(NTHR, 2) void attn_fwd_kernel(AttnArgs p) {
   const float sl2 = p.scale * kLog2e;
   const int nt = (s1 - s0 + 63) / 64;
 
-  RowFrag<D> qf[2];
-  int qrow[2];
+  RowFrag<D> qf[NS];
+  int qrow[NS];
 #pragma unroll
-  for (int qs = 0; qs < 2; ++qs) {
-    qrow[qs] = q0 + 32 * w + 16 * qs + r;
+  for (int qs = 0; qs < NS; ++qs) {
+    qrow[qs] = q0 + RW * w + 16 * qs + r;
     load_rowfrag<D>(qf[qs], Q, p.ld, min(qrow[qs], s1 - 1), g);
   }
-  float m[2] = {-INFINITY, -INFINITY}, lsum[2] = {0.f, 0.f};
-  f32x4 o[2][NDT];
+  float m[NS], lsum[NS];
+  f32x4 o[NS][NDT];
 #pragma unroll
-  for (int qs = 0; qs < 2; ++qs)
+  for (int qs = 0; qs < NS; ++qs)
 #pragma unroll
     for (int dt = 0; dt < NDT; ++dt) o[qs][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int qs = 0; qs < NS; ++qs) {
+    m[qs] = -INFINITY;
+    lsum[qs] = 0.f;
+  }
 
   auto issue = [&](int t, uint4* kt, uint4* vt) __attribute__((always_inline)) {
     if (t < nt) {
-      dma_tile<D>(kt, K, p.ld, s0 + 64 * t, s1 - 1);
-      dma_tile<D>(vt, V, p.ld, s0 + 64 * t, s1 - 1);
+      dma_tile<D, NW>(kt, K, p.ld, s0 + 64 * t, s1 - 1);
+      dma_tile<D, NW>(vt, V, p.ld, s0 + 64 * t, s1 - 1);
     }
   };
   auto body = [&](int t, const uint4* kt_s, const uint4* vt_s, uint4* kn, uint4* vn)
@@ -215,15 +225,15 @@ __global__ __launch_bounds__(NTHR, 2) void attn_fwd_kernel(AttnArgs p) {
     lds_barrier();
     issue(t + 2, kn, vn);
     const int k0 = s0 + 64 * t;
-    f32x4 s[4][2];
+    f32x4 s[4][NS];
 #pragma unroll
     for (int kq = 0; kq < 4; ++kq)
 #pragma unroll
-      for (int qs = 0; qs < 2; ++qs)
+      for (int qs = 0; qs < NS; ++qs)
         s[kq][qs] = dot_d<D>(kt_s, 16 * kq + r, qf[qs], g, f32x4{0.f, 0.f, 0.f, 0.f});
-    bf16x8 pb[2][2];
+    bf16x8 pb[NS][2];
 #pragma unroll
-    for (int qs = 0; qs < 2; ++qs) {
+    for (int qs = 0; qs < NS; ++qs) {
       float mx = -INFINITY;
 #pragma unroll
       for (int kq = 0; kq < 4; ++kq)
@@ -260,7 +270,7 @@ __global__ __launch_bounds__(NTHR, 2) void attn_fwd_kernel(AttnArgs p) {
       for (int kk = 0; kk < 2; ++kk) {
         const bf16x8 a = frag_trt<D>(vt_s, 32 * kk + 4 * g, 32 * kk + 16 + 4 * g, 16 * dt, r);
 #pragma unroll
-        for (int qs = 0; qs < 2; ++qs)
+        for (int qs = 0; qs < NS; ++qs)
           o[qs][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb[qs][kk], o[qs][dt], 0, 0, 0);
       }
   };
@@ -273,7 +283,7 @@ __global__ __launch_bounds__(NTHR, 2) void attn_fwd_kernel(AttnArgs p) {
   }
   bf16* O = reinterpret_cast<bf16*>(p.out) + head * D;
 #pragma unroll
-  for (int qs = 0; qs < 2; ++qs) {
+  for (int qs = 0; qs < NS; ++qs) {
     float tot = lsum[qs];
     tot += __shfl_xor(tot, 16);
     tot += __shfl_xor(tot, 32);
@@ -296,9 +306,10 @@ __global__ __launch_bounds__(NTHR, 2) void attn_fwd_kernel(AttnArgs p) {
 // ---- backward: dK, dV ------------------------------------------------------------
 // Per 128-key tile (32 keys per wave), 3-stage pipeline over 64-query tiles of Q, dO,
 // LSE and delta.
-template <int D>
-__global__ __launch_bounds__(NTHR, 1) void attn_bwd_dkdv_kernel(AttnArgs p) {
-  constexpr int NDT = AD<D>::NDT, SL = TG<D>::SLOTS, NI = TG<D>::NI;
+template <int D, int NS>
+__global__ __launch_bounds__(64 * (8 / NS), NS == 2 ? 2 : 1) void attn_bwd_dkdv_kernel(AttnArgs p) {
+  constexpr int NW = 8 / NS, RW = 16 * NS;   // waves per block, rows per wave
+  constexpr int NDT = AD<D>::NDT, SL = TG<D, NW>::SLOTS, NI = TG<D, NW>::NI;
   __shared__ uint4 q0s[SL], q1s[SL], q2s[SL], d0s[SL], d1s[SL], d2s[SL];
   __shared__ float l0s[64], l1s[64], l2s[64], e0s[64], e1s[64], e2s[64];
   const int work = blockIdx.x / p.heads, head = blockIdx.x % p.heads;
@@ -315,24 +326,24 @@ __global__ __launch_bounds__(NTHR, 1) void attn_bwd_dkdv_kernel(AttnArgs p) {
   const int nt = (s1 - s0 + 63) / 64;
   constexpr int PER_TILE = 2 * NI + 2;   // wave 0 issues the two 4-byte vectors too
 
-  RowFrag<D> kf[2], vf[2];
+  RowFrag<D> kf[NS], vf[NS];
 #pragma unroll
-  for (int ks = 0; ks < 2; ++ks) {
-    const int key = min(k0 + 32 * w + 16 * ks + r, s1 - 1);
+  for (int ks = 0; ks < NS; ++ks) {
+    const int key = min(k0 + RW * w + 16 * ks + r, s1 - 1);
     load_rowfrag<D>(kf[ks], K, p.ld, key, g);
     load_rowfrag<D>(vf[ks], V, p.ld, key, g);
   }
-  f32x4 dk[2][NDT], dv[2][NDT];
+  f32x4 dk[NS][NDT], dv[NS][NDT];
 #pragma unroll
-  for (int ks = 0; ks < 2; ++ks)
+  for (int ks = 0; ks < NS; ++ks)
 #pragma unroll
     for (int dt = 0; dt < NDT; ++dt) dk[ks][dt] = dv[ks][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   auto issue = [&](int t, uint4* qt, uint4* dt_, float* lt, float* et)
       __attribute__((always_inline)) {
     if (t < nt) {
-      dma_tile<D>(qt, Q, p.ld, s0 + 64 * t, s1 - 1);
-      dma_tile<D>(dt_, dO, p.ldo, s0 + 64 * t, s1 - 1);
+      dma_tile<D, NW>(qt, Q, p.ld, s0 + 64 * t, s1 - 1);
+      dma_tile<D, NW>(dt_, dO, p.ldo, s0 + 64 * t, s1 - 1);
       dma_vec64(lt, LSE, s0 + 64 * t, s1 - 1);
       dma_vec64(et, DEL, s0 + 64 * t, s1 - 1);
     }
@@ -352,12 +363,12 @@ __global__ __launch_bounds__(NTHR, 1) void attn_bwd_dkdv_kernel(AttnArgs p) {
     const int qb = s0 + 64 * t;
 #pragma unroll
     for (int kk = 0; kk < 2; ++kk) {
-      f32x4 P[2][2], dS[2][2];   // [query half][ks]
+      f32x4 P[2][NS], dS[2][NS];   // [query half][ks]
 #pragma unroll
       for (int h2 = 0; h2 < 2; ++h2) {
         const int qrow = 16 * (2 * kk + h2) + r;
 #pragma unroll
-        for (int ks = 0; ks < 2; ++ks) {
+        for (int ks = 0; ks < NS; ++ks) {
           f32x4 s = dot_d<D>(q_s, qrow, kf[ks], g, f32x4{0.f, 0.f, 0.f, 0.f});
           f32x4 dp = dot_d<D>(do_s, qrow, vf[ks], g, f32x4{0.f, 0.f, 0.f, 0.f});
 #pragma unroll
@@ -370,7 +381,7 @@ __global__ __launch_bounds__(NTHR, 1) void attn_bwd_dkdv_kernel(AttnArgs p) {
         }
       }
 #pragma unroll
-      for (int ks = 0; ks < 2; ++ks) {
+      for (int ks = 0; ks < NS; ++ks) {
         const bf16x8 ap = pack8(P[0][ks], P[1][ks]);
         const bf16x8 ads = pack8(dS[0][ks], dS[1][ks]);
 #pragma unroll
@@ -393,10 +404,10 @@ __global__ __launch_bounds__(NTHR, 1) void attn_bwd_dkdv_kernel(AttnArgs p) {
   bf16* dK = reinterpret_cast<bf16*>(p.dk) + head * D;
   bf16* dV = reinterpret_cast<bf16*>(p.dv) + head * D;
 #pragma unroll
-  for (int ks = 0; ks < 2; ++ks)
+  for (int ks = 0; ks < NS; ++ks)
 #pragma unroll
     for (int v = 0; v < 4; ++v) {
-      const int key = k0 + 32 * w + 16 * ks + 4 * g + v;
+      const int key = k0 + RW * w + 16 * ks + 4 * g + v;
       if (key >= s1) continue;
 #pragma unroll
       for (int dt = 0; dt < NDT; ++dt) {
@@ -407,9 +418,10 @@ __global__ __launch_bounds__(NTHR, 1) void attn_bwd_dkdv_kernel(AttnArgs p) {
 }
 
 // ---- backward: dQ (and delta) --------------------------------------------------------
-template <int D>
-__global__ __launch_bounds__(NTHR, 2) void attn_bwd_dq_kernel(AttnArgs p) {
-  constexpr int NDT = AD<D>::NDT, SL = TG<D>::SLOTS, NI = TG<D>::NI;
+template <int D, int NS>
+__global__ __launch_bounds__(64 * (8 / NS), NS == 2 ? 2 : 1) void attn_bwd_dq_kernel(AttnArgs p) {
+  constexpr int NW = 8 / NS, RW = 16 * NS;   // waves per block, rows per wave
+  constexpr int NDT = AD<D>::NDT, SL = TG<D, NW>::SLOTS, NI = TG<D, NW>::NI;
   __shared__ uint4 k0s[SL], k1s[SL], k2s[SL], v0s[SL], v1s[SL], v2s[SL];
   const int work = blockIdx.x / p.heads, head = blockIdx.x % p.heads;
   const int4 wk = p.work[work];
@@ -423,12 +435,12 @@ __global__ __launch_bounds__(NTHR, 2) void attn_bwd_dq_kernel(AttnArgs p) {
   const float sl2 = p.scale * kLog2e;
   const int nt = (s1 - s0 + 63) / 64;
 
-  RowFrag<D> qf[2], dof[2];
-  int qrow[2];
-  float lse2[2], del[2];
+  RowFrag<D> qf[NS], dof[NS];
+  int qrow[NS];
+  float lse2[NS], del[NS];
 #pragma unroll
-  for (int qs = 0; qs < 2; ++qs) {
-    qrow[qs] = q0 + 32 * w + 16 * qs + r;
+  for (int qs = 0; qs < NS; ++qs) {
+    qrow[qs] = q0 + RW * w + 16 * qs + r;
     const int qc = min(qrow[qs], s1 - 1);
     load_rowfrag<D>(qf[qs], Q, p.ld, qc, g);
     load_rowfrag<D>(dof[qs], dO, p.ldo, qc, g);
@@ -453,16 +465,16 @@ __global__ __launch_bounds__(NTHR, 2) void attn_bwd_dq_kernel(AttnArgs p) {
     del[qs] = dl;
     if (g == 0 && qrow[qs] < s1) p.delta_out[(int64_t)head * p.N + qrow[qs]] = dl;
   }
-  f32x4 dq[2][NDT];
+  f32x4 dq[NS][NDT];
 #pragma unroll
-  for (int qs = 0; qs < 2; ++qs)
+  for (int qs = 0; qs < NS; ++qs)
 #pragma unroll
     for (int dt = 0; dt < NDT; ++dt) dq[qs][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   auto issue = [&](int t, uint4* kt, uint4* vt) __attribute__((always_inline)) {
     if (t < nt) {
-      dma_tile<D>(kt, K, p.ld, s0 + 64 * t, s1 - 1);
-      dma_tile<D>(vt, V, p.ld, s0 + 64 * t, s1 - 1);
+      dma_tile<D, NW>(kt, K, p.ld, s0 + 64 * t, s1 - 1);
+      dma_tile<D, NW>(vt, V, p.ld, s0 + 64 * t, s1 - 1);
     }
   };
   auto body = [&](int t, const uint4* k_s, const uint4* v_s, uint4* kn, uint4* vn)
@@ -472,11 +484,11 @@ __global__ __launch_bounds__(NTHR, 2) void attn_bwd_dq_kernel(AttnArgs p) {
     lds_barrier();
     issue(t + 2, kn, vn);
     const int kb = s0 + 64 * t;
-    f32x4 ds[4][2];
+    f32x4 ds[4][NS];
 #pragma unroll
     for (int kq = 0; kq < 4; ++kq)
 #pragma unroll
-      for (int qs = 0; qs < 2; ++qs) {
+      for (int qs = 0; qs < NS; ++qs) {
         f32x4 sv = dot_d<D>(k_s, 16 * kq + r, qf[qs], g, f32x4{0.f, 0.f, 0.f, 0.f});
         f32x4 dp = dot_d<D>(v_s, 16 * kq + r, dof[qs], g, f32x4{0.f, 0.f, 0.f, 0.f});
 #pragma unroll
@@ -488,14 +500,14 @@ __global__ __launch_bounds__(NTHR, 2) void attn_bwd_dq_kernel(AttnArgs p) {
       }
 #pragma unroll
     for (int kk = 0; kk < 2; ++kk) {
-      bf16x8 b[2];
+      bf16x8 b[NS];
 #pragma unroll
-      for (int qs = 0; qs < 2; ++qs) b[qs] = pack8(ds[2 * kk][qs], ds[2 * kk + 1][qs]);
+      for (int qs = 0; qs < NS; ++qs) b[qs] = pack8(ds[2 * kk][qs], ds[2 * kk + 1][qs]);
 #pragma unroll
       for (int dt = 0; dt < NDT; ++dt) {
         const bf16x8 a = frag_trt<D>(k_s, 32 * kk + 4 * g, 32 * kk + 16 + 4 * g, 16 * dt, r);
 #pragma unroll
-        for (int qs = 0; qs < 2; ++qs)
+        for (int qs = 0; qs < NS; ++qs)
           dq[qs][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b[qs], dq[qs][dt], 0, 0, 0);
       }
     }
@@ -509,7 +521,7 @@ __global__ __launch_bounds__(NTHR, 2) void attn_bwd_dq_kernel(AttnArgs p) {
   }
   bf16* dQ = reinterpret_cast<bf16*>(p.dq) + head * D;
 #pragma unroll
-  for (int qs = 0; qs < 2; ++qs) {
+  for (int qs = 0; qs < NS; ++qs) {
     const int q = qrow[qs];
     if (q >= s1) continue;
 #pragma unroll
@@ -639,17 +651,17 @@ __global__ void attn_bwd_dkdv_f32_kernel(AttnArgs p) {
 
 template <int D>
 hipError_t fwd_bf16(const AttnArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL(attn_fwd_kernel<D>, dim3(a.n_work * a.heads), dim3(NTHR), 0, s, a);
+  hipLaunchKernelGGL((attn_fwd_kernel<D, FWD_NS>), dim3(a.n_work * a.heads), dim3(64 * (8 / FWD_NS)), 0, s, a);
   return hipGetLastError();
 }
 template <int D>
 hipError_t dq_bf16(const AttnArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL(attn_bwd_dq_kernel<D>, dim3(a.n_work * a.heads), dim3(NTHR), 0, s, a);
+  hipLaunchKernelGGL((attn_bwd_dq_kernel<D, DQ_NS>), dim3(a.n_work * a.heads), dim3(64 * (8 / DQ_NS)), 0, s, a);
   return hipGetLastError();
 }
 template <int D>
 hipError_t dkdv_bf16(const AttnArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL(attn_bwd_dkdv_kernel<D>, dim3(a.n_work * a.heads), dim3(NTHR), 0, s, a);
+  hipLaunchKernelGGL((attn_bwd_dkdv_kernel<D, DKDV_NS>), dim3(a.n_work * a.heads), dim3(64 * (8 / DKDV_NS)), 0, s, a);
   return hipGetLastError();
 }
 template <int D>
