@@ -91,6 +91,10 @@ __device__ __forceinline__ f32x4 dot_d(const uint4* rowt, int arow, const RowFra
   return acc;
 }
 
+// 2^x on the transcendental unit (v_exp_f32).  Inputs here are <= 0 (or -inf); results
+// below the normal range flush to zero, which cannot change a softmax weight in bf16.
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
 __device__ __forceinline__ bf16x8 pack8(const f32x4& a, const f32x4& b) {
   bf16x8 r;
   r[0] = (bf16)a[0]; r[1] = (bf16)a[1]; r[2] = (bf16)a[2]; r[3] = (bf16)a[3];
@@ -231,30 +235,36 @@ __global__ __launch_bounds__(64 * (8 / NS), NS == 2 ? 2 : 1) void attn_fwd_kerne
 #pragma unroll
       for (int qs = 0; qs < NS; ++qs)
         s[kq][qs] = dot_d<D>(kt_s, 16 * kq + r, qf[qs], g, f32x4{0.f, 0.f, 0.f, 0.f});
-    bf16x8 pb[NS][2];
-#pragma unroll
-    for (int qs = 0; qs < NS; ++qs) {
-      float mx = -INFINITY;
+    if (k0 + 64 > s1) {   // ragged last tile: keys past the segment never win or weigh
 #pragma unroll
       for (int kq = 0; kq < 4; ++kq)
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
-          const int key = k0 + 16 * kq + 4 * g + v;
-          const float x = key < s1 ? s[kq][qs][v] * sl2 : -INFINITY;
-          s[kq][qs][v] = x;
-          mx = fmaxf(mx, x);
+          const bool out = k0 + 16 * kq + 4 * g + v >= s1;
+#pragma unroll
+          for (int qs = 0; qs < NS; ++qs) s[kq][qs][v] = out ? -INFINITY : s[kq][qs][v];
         }
+    }
+    bf16x8 pb[NS][2];
+#pragma unroll
+    for (int qs = 0; qs < NS; ++qs) {
+      // running max in the scaled log2 domain; scaling by sl2 > 0 commutes with max
+      float mx = -INFINITY;
+#pragma unroll
+      for (int kq = 0; kq < 4; ++kq)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) mx = fmaxf(mx, s[kq][qs][v]);
       mx = fmaxf(mx, __shfl_xor(mx, 16));
       mx = fmaxf(mx, __shfl_xor(mx, 32));
-      const float mn = fmaxf(m[qs], mx);
-      const float alpha = exp2f(m[qs] - mn);
+      const float mn = fmaxf(m[qs], mx * sl2);
+      const float alpha = fast_exp2(m[qs] - mn);
       m[qs] = mn;
       float ps = 0.f;
 #pragma unroll
       for (int kq = 0; kq < 4; ++kq)
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
-          const float e = exp2f(s[kq][qs][v] - mn);
+          const float e = fast_exp2(fmaf(s[kq][qs][v], sl2, -mn));
           s[kq][qs][v] = e;
           ps += e;
         }
@@ -311,7 +321,7 @@ __global__ __launch_bounds__(64 * (8 / NS), NS == 2 ? 2 : 1) void attn_bwd_dkdv_
   constexpr int NW = 8 / NS, RW = 16 * NS;   // waves per block, rows per wave
   constexpr int NDT = AD<D>::NDT, SL = TG<D, NW>::SLOTS, NI = TG<D, NW>::NI;
   __shared__ uint4 q0s[SL], q1s[SL], q2s[SL], d0s[SL], d1s[SL], d2s[SL];
-  __shared__ float l0s[64], l1s[64], l2s[64], e0s[64], e1s[64], e2s[64];
+  __shared__ __attribute__((aligned(16))) float l0s[64], l1s[64], l2s[64], e0s[64], e1s[64], e2s[64];
   const int work = blockIdx.x / p.heads, head = blockIdx.x % p.heads;
   const int4 wk = p.work[work];
   const int k0 = wk.x, s0 = wk.y, s1 = wk.z;
@@ -367,16 +377,31 @@ __global__ __launch_bounds__(64 * (8 / NS), NS == 2 ? 2 : 1) void attn_bwd_dkdv_
 #pragma unroll
       for (int h2 = 0; h2 < 2; ++h2) {
         const int qrow = 16 * (2 * kk + h2) + r;
+        const int q4 = 16 * (2 * kk + h2) + 4 * g;   // this lane's four queries
+        const float4 lq = *reinterpret_cast<const float4*>(lse_s + q4);
+        const float4 eq = *reinterpret_cast<const float4*>(del_s + q4);
+        const float nl[4] = {-lq.x * kLog2e, -lq.y * kLog2e, -lq.z * kLog2e, -lq.w * kLog2e};
+        const float de[4] = {eq.x, eq.y, eq.z, eq.w};
 #pragma unroll
         for (int ks = 0; ks < NS; ++ks) {
           f32x4 s = dot_d<D>(q_s, qrow, kf[ks], g, f32x4{0.f, 0.f, 0.f, 0.f});
           f32x4 dp = dot_d<D>(do_s, qrow, vf[ks], g, f32x4{0.f, 0.f, 0.f, 0.f});
 #pragma unroll
           for (int v = 0; v < 4; ++v) {
-            const int qi = 16 * (2 * kk + h2) + 4 * g + v;
-            const float pp = (qb + qi < s1) ? exp2f(s[v] * sl2 - lse_s[qi] * kLog2e) : 0.f;
+            const float pp = fast_exp2(fmaf(s[v], sl2, nl[v]));
             P[h2][ks][v] = pp;
-            dS[h2][ks][v] = pp * (dp[v] - del_s[qi]);
+            dS[h2][ks][v] = pp * (dp[v] - de[v]);
+          }
+        }
+        if (qb + 64 > s1) {   // ragged last tile: queries past the segment contribute nothing
+#pragma unroll
+          for (int v = 0; v < 4; ++v) {
+            const bool out = qb + q4 + v >= s1;
+#pragma unroll
+            for (int ks = 0; ks < NS; ++ks) {
+              P[h2][ks][v] = out ? 0.f : P[h2][ks][v];
+              dS[h2][ks][v] = out ? 0.f : dS[h2][ks][v];
+            }
           }
         }
       }
@@ -493,11 +518,20 @@ __global__ __launch_bounds__(64 * (8 / NS), NS == 2 ? 2 : 1) void attn_bwd_dq_ke
         f32x4 dp = dot_d<D>(v_s, 16 * kq + r, dof[qs], g, f32x4{0.f, 0.f, 0.f, 0.f});
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
-          const int key = kb + 16 * kq + 4 * g + v;
-          const float pp = key < s1 ? exp2f(sv[v] * sl2 - lse2[qs]) : 0.f;
+          const float pp = fast_exp2(fmaf(sv[v], sl2, -lse2[qs]));
           ds[kq][qs][v] = pp * (dp[v] - del[qs]);
         }
       }
+    if (kb + 64 > s1) {   // ragged last tile: keys past the segment contribute nothing
+#pragma unroll
+      for (int kq = 0; kq < 4; ++kq)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const bool out = kb + 16 * kq + 4 * g + v >= s1;
+#pragma unroll
+          for (int qs = 0; qs < NS; ++qs) ds[kq][qs][v] = out ? 0.f : ds[kq][qs][v];
+        }
+    }
 #pragma unroll
     for (int kk = 0; kk < 2; ++kk) {
       bf16x8 b[NS];
