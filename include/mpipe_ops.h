@@ -21,9 +21,11 @@ extern "C" {
  *          2 TN  C[m][n] = sum_k A[k][m] B[k][n]     (weight gradient, dW = dY^T X)
  * Epilogues (acc = the sum, bias per column, cfg dtype unless noted):
  *          0 C = acc + bias
- *          1 C2 = acc + bias (optional), C = GELU(acc + bias)   (erf form)
+ *          1 u = acc + bias rounded to dtype: C = GELU(u), C2 = GELU'(u) (C2 optional).
+ *            GELU is the erf form: fp32 evaluates erf exactly; bf16 uses the
+ *            Abramowitz & Stegun 7.1.26 erf (|error| <= 1.5e-7), in every kernel.
  *          2 C(fp32) = aux(fp32, nullable, may alias C) + acc + bias
- *          3 C = acc * GELU'(aux)
+ *          3 C = acc * aux   (aux = the GELU'(u) that epilogue 1 stored: the MLP backward)
  *          4 C(fp32) = acc, or C + acc when beta != 0; with k_per_split > 0 the
  *            K range is split and split s writes C + s * split_stride.
  * Requirements: K-contiguous operands need K and their row stride to be

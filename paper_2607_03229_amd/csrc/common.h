@@ -33,6 +33,32 @@ __device__ __forceinline__ float gelu_grad_f(float u) {
   return Phi + u * phi;
 }
 
+// bf16 GELU: standard normal CDF Phi(u) and density phi(u) sharing one
+// exp(-u^2/2): erfc(x) = y(t) exp(-x^2), t = 1 / (1 + p x), x = |u| / sqrt(2), with the
+// five-term polynomial y of Abramowitz & Stegun 7.1.26 (|error in erf| <= 1.5e-7, far
+// below the bf16 rounding of the outputs).  Every bf16 GEMM epilogue uses these, so a
+// token's result never depends on which kernel (tile size) computed it; fp32 uses erff.
+__device__ __forceinline__ void phi_pair(float u, float& Phi, float& dens) {
+  const float x = fabsf(u) * 0.70710678118654752f;
+  const float t = __builtin_amdgcn_rcpf(fmaf(0.3275911f, x, 1.0f));
+  const float y = t * fmaf(t, fmaf(t, fmaf(t, fmaf(t, 1.061405429f, -1.453152027f), 1.421413741f),
+                               -0.284496736f), 0.254829592f);
+  const float e = __builtin_amdgcn_exp2f(-x * x * 1.4426950408889634f);   // exp(-u^2/2)
+  const float tail = 0.5f * y * e;                                           // Phi(-|u|)
+  Phi = u >= 0.f ? 1.0f - tail : tail;
+  dens = e * 0.3989422804014327f;
+}
+__device__ __forceinline__ float gelu_fast(float u) {
+  float P, d;
+  phi_pair(u, P, d);
+  return u * P;
+}
+__device__ __forceinline__ float gelu_grad_fast(float u) {
+  float P, d;
+  phi_pair(u, P, d);
+  return fmaf(u, d, P);
+}
+
 // bf16 pair packing helpers on 32-bit words (low half = first element)
 __device__ __forceinline__ uint32_t pack_lo(uint32_t a, uint32_t b) {  // a.lo | b.lo << 16
   return __builtin_amdgcn_perm(b, a, 0x05040100u);

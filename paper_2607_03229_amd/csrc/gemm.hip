@@ -14,6 +14,8 @@
 // (64 KB); the next tile's global loads are in flight during the MFMAs.
 // Blocks are remapped so that consecutive tiles land on the same XCD and walk
 // the output in groups of 8 tile-rows (L2 reuse of A rows and B columns).
+#include <type_traits>
+
 #include "common.h"
 #include "internal.h"
 
@@ -208,18 +210,22 @@ __device__ __forceinline__ void epilogue(const GemmArgs& p, int split, int m0, i
         if constexpr (EPI == EPI_STORE) {
           reinterpret_cast<T*>(p.C)[(int64_t)m * p.ldc + n] = from_f<T>(x);
         } else if constexpr (EPI == EPI_GELU) {
-          if (p.C2) reinterpret_cast<T*>(p.C2)[(int64_t)m * p.ldc2 + n] = from_f<T>(x);
-          // GELU of the stored (rounded) pre-activation, so the backward sees the
-          // same value the forward used
+          // GELU and GELU' at the rounded pre-activation u; the backward multiplies by
+          // the stored GELU'(u)
           const float u = to_f(from_f<T>(x));
-          reinterpret_cast<T*>(p.C)[(int64_t)m * p.ldc + n] = from_f<T>(gelu_f(u));
+          const bool fast = std::is_same<T, bf16>::value;
+          const float gv = fast ? gelu_fast(u) : gelu_f(u);
+          if (p.C2)
+            reinterpret_cast<T*>(p.C2)[(int64_t)m * p.ldc2 + n] =
+                from_f<T>(fast ? gelu_grad_fast(u) : gelu_grad_f(u));
+          reinterpret_cast<T*>(p.C)[(int64_t)m * p.ldc + n] = from_f<T>(gv);
         } else if constexpr (EPI == EPI_RESID) {
           const float* R = reinterpret_cast<const float*>(p.aux);
           const float base = R ? R[(int64_t)m * p.ld_aux + n] : 0.0f;
           reinterpret_cast<float*>(p.C)[(int64_t)m * p.ldc + n] = base + x;
         } else if constexpr (EPI == EPI_GELU_BWD) {
-          const float u = to_f(reinterpret_cast<const T*>(p.aux)[(int64_t)m * p.ld_aux + n]);
-          reinterpret_cast<T*>(p.C)[(int64_t)m * p.ldc + n] = from_f<T>(x * gelu_grad_f(u));
+          const float gg = to_f(reinterpret_cast<const T*>(p.aux)[(int64_t)m * p.ld_aux + n]);
+          reinterpret_cast<T*>(p.C)[(int64_t)m * p.ldc + n] = from_f<T>(x * gg);
         } else {  // EPI_F32: fp32 output (split-K partial slice, or accumulate)
           float* C = reinterpret_cast<float*>(p.C) + (int64_t)split * p.split_stride;
           const int64_t o = (int64_t)m * p.ldc + n;
@@ -331,16 +337,17 @@ hipError_t dispatch_epi(const GemmArgs& a, int epi, hipStream_t s) {
 // their column count and ld to be multiples of VEC; all pointers 16-byte aligned.
 hipError_t gemm(int dtype, int layout, int epi, const GemmArgs& a, hipStream_t s) {
   if (a.M <= 0 || a.N <= 0) return hipSuccess;
-  if (dtype == DT_BF16 && a.M >= 512 && a.N >= 256) {
-    GemmArgs b = a;
-    // 16-byte vector epilogue when every output/aux row stride keeps 16-byte alignment
+  if (dtype == DT_BF16 && a.M >= 512 && a.N >= 256 && a.N % 8 == 0) {
+    // the 256x256 kernel's epilogue is 16-byte vectors only: every output/aux row stride
+    // must keep 16-byte alignment, else the general kernel takes the problem
     auto al16 = [](const void* q) { return (reinterpret_cast<uintptr_t>(q) & 15) == 0; };
     const bool f32out = epi == EPI_RESID || epi == EPI_F32;
     const int64_t vq = f32out ? 4 : 8;
-    b.vec = al16(a.C) && a.ldc % vq == 0 && (a.bias == nullptr || al16(a.bias)) &&
-            (a.aux == nullptr || (al16(a.aux) && a.ld_aux % (epi == EPI_RESID ? 4 : 8) == 0)) &&
-            (a.C2 == nullptr || (al16(a.C2) && a.ldc2 % 8 == 0));
-    return gemm_big(layout, epi, b, s);
+    const bool vec = al16(a.C) && a.ldc % vq == 0 && (a.bias == nullptr || al16(a.bias)) &&
+                     (a.aux == nullptr || (al16(a.aux) && a.ld_aux % (epi == EPI_RESID ? 4 : 8) == 0)) &&
+                     (a.C2 == nullptr || (al16(a.C2) && a.ldc2 % 8 == 0)) &&
+                     (epi != EPI_F32 || a.split_stride % 4 == 0);
+    if (vec) return gemm_big(layout, epi, a, s);
   }
   if (dtype == DT_BF16) {
     switch (layout) {

@@ -28,7 +28,10 @@
 // while the second half's MFMAs run.  One barrier per 1024 MFMA cycles per wave.
 // Ragged M/N edges read clamped (valid) rows; a ragged K tail reads clamped rows and
 // zeroes the A fragments past the end.  The epilogue stages each wave's accumulators
-// through LDS, 16 rows at a time, so all epilogue global accesses are 16-byte vectors.
+// through LDS, 16 rows at a time, so all epilogue global accesses are 16-byte vectors
+// (the dispatcher sends ragged-N or misaligned problems to the general kernel); the
+// operands it reads (GELU' factor, residual, accumulate target) are fetched one staging
+// pass ahead.
 #include <type_traits>
 
 #include "common.h"
@@ -112,92 +115,76 @@ __device__ __forceinline__ void dma16(const bf16* src, const uint4* tile, int i)
 
 // ---- epilogue ------------------------------------------------------------------------
 
-// 8 consecutive outputs (m, n..n+7) through the epilogue, vectorised
+// The vector epilogue works on 8 consecutive outputs (m, n..n+7) of a lane.  Its global
+// operands (GELU' factor, residual, accumulate target) are fetched one staging pass
+// ahead, so their latency overlaps the previous pass instead of stalling each store.
+struct AuxV { uint4 v[2]; };
+
 template <int EPI>
-__device__ __forceinline__ void epi8(const GemmArgs& p, int split, int m, int n, float* v,
-                                     bool vec) {
-  const bf16* bias = reinterpret_cast<const bf16*>(p.bias);
-  if (vec) {
-    if (bias != nullptr && split == 0) {
-      const uint4 bb = *reinterpret_cast<const uint4*>(bias + n);
-      const bf16* b8 = reinterpret_cast<const bf16*>(&bb);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) v[e] += (float)b8[e];
+__device__ __forceinline__ void aux_fetch(const GemmArgs& p, int split, int m, int n, AuxV& a) {
+  if constexpr (EPI == EPI_GELU_BWD) {
+    a.v[0] = *reinterpret_cast<const uint4*>(reinterpret_cast<const bf16*>(p.aux) +
+                                             (int64_t)m * p.ld_aux + n);
+  } else if constexpr (EPI == EPI_RESID) {
+    if (p.aux) {
+      const float* R = reinterpret_cast<const float*>(p.aux) + (int64_t)m * p.ld_aux + n;
+      a.v[0] = *reinterpret_cast<const uint4*>(R);
+      a.v[1] = *reinterpret_cast<const uint4*>(R + 4);
     }
-    if constexpr (EPI == EPI_STORE || EPI == EPI_GELU || EPI == EPI_GELU_BWD) {
-      bf16 o[8];
-      if constexpr (EPI == EPI_STORE) {
-#pragma unroll
-        for (int e = 0; e < 8; ++e) o[e] = (bf16)v[e];
-      } else if constexpr (EPI == EPI_GELU) {
-        bf16 pre[8];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          pre[e] = (bf16)v[e];
-          o[e] = (bf16)gelu_f((float)pre[e]);
-        }
-        if (p.C2)
-          *reinterpret_cast<uint4*>(reinterpret_cast<bf16*>(p.C2) + (int64_t)m * p.ldc2 + n) =
-              *reinterpret_cast<const uint4*>(pre);
-      } else {
-        const uint4 uu = *reinterpret_cast<const uint4*>(reinterpret_cast<const bf16*>(p.aux) +
-                                                         (int64_t)m * p.ld_aux + n);
-        const bf16* u8 = reinterpret_cast<const bf16*>(&uu);
-#pragma unroll
-        for (int e = 0; e < 8; ++e) o[e] = (bf16)(v[e] * gelu_grad_f((float)u8[e]));
-      }
-      *reinterpret_cast<uint4*>(reinterpret_cast<bf16*>(p.C) + (int64_t)m * p.ldc + n) =
-          *reinterpret_cast<const uint4*>(o);
-    } else if constexpr (EPI == EPI_RESID) {
-      const float* R = reinterpret_cast<const float*>(p.aux);
-      float4 r0 = make_float4(0.f, 0.f, 0.f, 0.f), r1 = r0;
-      if (R) {
-        r0 = *reinterpret_cast<const float4*>(R + (int64_t)m * p.ld_aux + n);
-        r1 = *reinterpret_cast<const float4*>(R + (int64_t)m * p.ld_aux + n + 4);
-      }
-      float* C = reinterpret_cast<float*>(p.C) + (int64_t)m * p.ldc + n;
-      *reinterpret_cast<float4*>(C) =
-          make_float4(r0.x + v[0], r0.y + v[1], r0.z + v[2], r0.w + v[3]);
-      *reinterpret_cast<float4*>(C + 4) =
-          make_float4(r1.x + v[4], r1.y + v[5], r1.z + v[6], r1.w + v[7]);
-    } else {  // EPI_F32
-      float* C = reinterpret_cast<float*>(p.C) + (int64_t)split * p.split_stride +
-                 (int64_t)m * p.ldc + n;
-      float4 a = make_float4(v[0], v[1], v[2], v[3]), b = make_float4(v[4], v[5], v[6], v[7]);
-      if (p.beta) {
-        const float4 c0 = *reinterpret_cast<const float4*>(C);
-        const float4 c1 = *reinterpret_cast<const float4*>(C + 4);
-        a.x += c0.x; a.y += c0.y; a.z += c0.z; a.w += c0.w;
-        b.x += c1.x; b.y += c1.y; b.z += c1.z; b.w += c1.w;
-      }
-      *reinterpret_cast<float4*>(C) = a;
-      *reinterpret_cast<float4*>(C + 4) = b;
+  } else if constexpr (EPI == EPI_F32) {
+    if (p.beta) {
+      const float* C = reinterpret_cast<const float*>(p.C) + (int64_t)split * p.split_stride +
+                       (int64_t)m * p.ldc + n;
+      a.v[0] = *reinterpret_cast<const uint4*>(C);
+      a.v[1] = *reinterpret_cast<const uint4*>(C + 4);
     }
-    return;
   }
-  // scalar tail (ragged N or unaligned strides)
-  for (int e = 0; e < 8; ++e) {
-    const int nn = n + e;
-    if (nn >= p.N) break;
-    float x = v[e] + ((bias != nullptr && split == 0) ? (float)bias[nn] : 0.f);
+}
+
+template <int EPI>
+__device__ __forceinline__ void epi8_vec(const GemmArgs& p, int split, int m, int n, float* v,
+                                         const float* bias8, const AuxV& ax) {
+#pragma unroll
+  for (int e = 0; e < 8; ++e) v[e] += bias8[e];
+  if constexpr (EPI == EPI_STORE || EPI == EPI_GELU || EPI == EPI_GELU_BWD) {
+    bf16 o[8];
     if constexpr (EPI == EPI_STORE) {
-      reinterpret_cast<bf16*>(p.C)[(int64_t)m * p.ldc + nn] = (bf16)x;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) o[e] = (bf16)v[e];
     } else if constexpr (EPI == EPI_GELU) {
-      const bf16 pre = (bf16)x;
-      if (p.C2) reinterpret_cast<bf16*>(p.C2)[(int64_t)m * p.ldc2 + nn] = pre;
-      reinterpret_cast<bf16*>(p.C)[(int64_t)m * p.ldc + nn] = (bf16)gelu_f((float)pre);
-    } else if constexpr (EPI == EPI_RESID) {
-      const float* R = reinterpret_cast<const float*>(p.aux);
-      const float base = R ? R[(int64_t)m * p.ld_aux + nn] : 0.f;
-      reinterpret_cast<float*>(p.C)[(int64_t)m * p.ldc + nn] = base + x;
-    } else if constexpr (EPI == EPI_GELU_BWD) {
-      const float u = (float)reinterpret_cast<const bf16*>(p.aux)[(int64_t)m * p.ld_aux + nn];
-      reinterpret_cast<bf16*>(p.C)[(int64_t)m * p.ldc + nn] = (bf16)(x * gelu_grad_f(u));
-    } else {
-      float* C = reinterpret_cast<float*>(p.C) + (int64_t)split * p.split_stride;
-      const int64_t o = (int64_t)m * p.ldc + nn;
-      C[o] = p.beta ? C[o] + x : x;
+      // GELU and its derivative at the bf16-rounded pre-activation u, from one Phi/phi
+      // evaluation; the derivative is what the backward needs of u
+      bf16 gd[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float u = (float)(bf16)v[e];
+        float P, dens;
+        phi_pair(u, P, dens);
+        o[e] = (bf16)(u * P);
+        gd[e] = (bf16)fmaf(u, dens, P);
+      }
+      if (p.C2)
+        *reinterpret_cast<uint4*>(reinterpret_cast<bf16*>(p.C2) + (int64_t)m * p.ldc2 + n) =
+            *reinterpret_cast<const uint4*>(gd);
+    } else {   // EPI_GELU_BWD: aux holds GELU'(u) from the forward
+      const bf16* g8 = reinterpret_cast<const bf16*>(&ax.v[0]);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) o[e] = (bf16)(v[e] * (float)g8[e]);
     }
+    *reinterpret_cast<uint4*>(reinterpret_cast<bf16*>(p.C) + (int64_t)m * p.ldc + n) =
+        *reinterpret_cast<const uint4*>(o);
+  } else {   // EPI_RESID, EPI_F32: fp32 out, plus the fetched residual / previous value
+    float* C = reinterpret_cast<float*>(p.C) +
+               (EPI == EPI_F32 ? (int64_t)split * p.split_stride : 0) + (int64_t)m * p.ldc + n;
+    const bool add = EPI == EPI_RESID ? p.aux != nullptr : p.beta != 0;
+    const float* r8 = reinterpret_cast<const float*>(&ax.v[0]);
+    float4 a = make_float4(v[0], v[1], v[2], v[3]), b = make_float4(v[4], v[5], v[6], v[7]);
+    if (add) {
+      a.x += r8[0]; a.y += r8[1]; a.z += r8[2]; a.w += r8[3];
+      b.x += r8[4]; b.y += r8[5]; b.z += r8[6]; b.w += r8[7];
+    }
+    *reinterpret_cast<float4*>(C) = a;
+    *reinterpret_cast<float4*>(C + 4) = b;
   }
 }
 
@@ -447,16 +434,44 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_big_kernel(GemmArgs p) {
   }
 
   // epilogue: each wave stages 16x128 accumulator rows at a time in its own LDS tile
-  // (the last barrier of the loop ended every fragment read)
+  // (the last barrier of the loop ended every fragment read).  Pass pi = 2i + hh covers
+  // rows 32i + 16hh .. +15 of the wave tile; lane (u, cg) takes row (l/16) + 4u, columns
+  // 8cg..8cg+7.
   __syncthreads();
   uint4* own = w == 0 ? sa0 : w == 1 ? sa1 : w == 2 ? sa2 : sa3;
   float* stage = reinterpret_cast<float*>(own);
   static_assert(16 * SP * 4 <= TILE_U4 * 16, "epilogue staging must fit in one tile");
   const int cg = l & 15;
+  const int n = n0 + wn * 128 + 8 * cg;   // N % 8 == 0: all eight columns or none in range
+  const bool vec = n < p.N;
+  float bias8[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) bias8[e] = 0.f;
+  if (vec && p.bias != nullptr && split == 0) {
+    const uint4 bb = *reinterpret_cast<const uint4*>(reinterpret_cast<const bf16*>(p.bias) + n);
+    const bf16* b8 = reinterpret_cast<const bf16*>(&bb);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) bias8[e] = (float)b8[e];
+  }
+  auto row_of = [&](int pi, int u) { return m0 + wm * 128 + 16 * pi + (l >> 4) + 4 * u; };
+  constexpr bool kAux = EPI == EPI_GELU_BWD || EPI == EPI_RESID || EPI == EPI_F32;
+  AuxV ax[2][4];
+  auto fetch = [&](int pi, AuxV (&dst)[4]) __attribute__((always_inline)) {
+    if constexpr (kAux) {
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int m = row_of(pi, u);
+        if (vec && m < p.M) aux_fetch<EPI>(p, split, m, n, dst[u]);
+      }
+    }
+  };
+  fetch(0, ax[0]);
 #pragma unroll
   for (int i = 0; i < 4; ++i) {     // (acc[i] must be indexed statically)
 #pragma unroll
     for (int hh = 0; hh < 2; ++hh) {
+      const int pi = 2 * i + hh;
+      if (pi + 1 < 8) fetch(pi + 1, ax[(pi + 1) & 1]);
       __syncthreads();
 #pragma unroll
       for (int j = 0; j < 4; ++j)
@@ -466,18 +481,23 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_big_kernel(GemmArgs p) {
           stage[rr * SP + 32 * j + (l & 31)] = acc[i][j][e];
         }
       __syncthreads();
-#pragma unroll 1
-      for (int u = 0; u < 4; ++u) {
+      auto out_row = [&](int u, const AuxV& a) __attribute__((always_inline)) {
         const int rr = (l >> 4) + 4 * u;
-        const int m = m0 + wm * 128 + 32 * i + 16 * hh + rr;
-        const int n = n0 + wn * 128 + 8 * cg;
-        if (m >= p.M || n >= p.N) continue;
+        const int m = row_of(pi, u);
+        if (m >= p.M || n >= p.N) return;
         float v[8];
         const float4 x0 = *reinterpret_cast<const float4*>(stage + rr * SP + 8 * cg);
         const float4 x1 = *reinterpret_cast<const float4*>(stage + rr * SP + 8 * cg + 4);
         v[0] = x0.x; v[1] = x0.y; v[2] = x0.z; v[3] = x0.w;
         v[4] = x1.x; v[5] = x1.y; v[6] = x1.z; v[7] = x1.w;
-        epi8<EPI>(p, split, m, n, v, p.vec && n + 8 <= p.N);
+        epi8_vec<EPI>(p, split, m, n, v, bias8, a);
+      };
+      if constexpr (kAux) {   // static u: the prefetched operands live in registers
+#pragma unroll
+        for (int u = 0; u < 4; ++u) out_row(u, ax[pi & 1][u]);
+      } else {                // no operands to prefetch: a rolled loop keeps the code small
+#pragma unroll 1
+        for (int u = 0; u < 4; ++u) out_row(u, ax[0][0]);
       }
     }
   }

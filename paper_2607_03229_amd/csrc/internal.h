@@ -15,9 +15,9 @@ constexpr int ATTN_TILE = 128;   // queries (forward, dQ) or keys (dK/dV) per at
 //   kps: K range per split (multiple of the K step; <= 0 means no split); split s
 //        covers [s*kps, (s+1)*kps) and writes C + s*split_stride (EPI_F32 only).
 //   EPI_STORE     C(T)   = acc + bias
-//   EPI_GELU      C2(T)  = acc + bias (pre-activation, optional), C(T) = GELU(that)
+//   EPI_GELU      u = T(acc + bias): C(T) = GELU(u), C2(T) = GELU'(u) (optional)
 //   EPI_RESID     C(f32) = aux(f32, may alias C, may be null) + acc + bias
-//   EPI_GELU_BWD  C(T)   = acc * GELU'(aux(T))
+//   EPI_GELU_BWD  C(T)   = acc * aux(T)   (aux = the GELU'(u) the forward stored)
 //   EPI_F32       C(f32) = acc (+ C if beta)
 struct GemmArgs {
   const void* A = nullptr;
@@ -33,7 +33,6 @@ struct GemmArgs {
   void* C2 = nullptr;
   int64_t ldc2 = 0;
   int beta = 0;
-  int vec = 0;   // set by gemm(): 16-byte epilogue accesses are aligned
 };
 hipError_t gemm(int dtype, int layout, int epi, const GemmArgs& a, hipStream_t s);
 // 256x256-tile bf16 kernel (M >= 512, N >= 256), same contract as gemm()
