@@ -45,6 +45,121 @@ def model_flops(cfg, n_patches: int, sum_len2: int, trainable: bool) -> float:
     return float(3 * F - 2 * N * kpe * h) if trainable else float(F)
 
 
+# ---- HBM traffic of the dominant kernel (rocprofv3 PMC counters) ---------------------
+# FETCH_SIZE / WRITE_SIZE are read in two separate `rocprofv3 --pmc` runs of this script
+# (one counter per run), each scaled by what the same counter reads for a plain copy of
+# known size: the library's row gather with identity indices (--copy-calibration).
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.json")
+CAL_ROWS, CAL_COLS = 32768, 3584          # bf16 rows copied by the calibration gather
+CAL_READ = CAL_ROWS * CAL_COLS * 2 + 8 * CAL_ROWS
+CAL_WRITE = CAL_ROWS * CAL_COLS * 2
+EPI_NAMES = ["store", "gelu", "resid", "gelubwd", "f32"]
+
+
+def source_digest() -> str:
+    """Digest of the kernel sources: stored traffic is reported only while it matches."""
+    import hashlib
+    h = hashlib.sha256()
+    src = os.path.join(ROOT, "paper_2607_03229_amd", "csrc")
+    for f in sorted(os.listdir(src)):
+        if f.endswith((".hip", ".cpp", ".h")):
+            h.update(f.encode())
+            with open(os.path.join(src, f), "rb") as fh:
+                h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def kernel_class(name: str):
+    """Library profiling class of a dispatched kernel symbol (mangled or demangled)."""
+    import re
+    lay = {(0, 0): "NT", (0, 1): "NN", (1, 1): "TN"}
+    m = re.search(r"gemm_big_kernel<(true|false), (true|false), (\d)>", name)
+    if m:
+        return f"gemm_{lay[(int(m.group(1) == 'true'), int(m.group(2) == 'true'))]}_{EPI_NAMES[int(m.group(3))]}"
+    m = re.search(r"gemm_(?:big_)?kernelI(?:DF16b|f)?Lb([01])ELb([01])ELi(\d)E", name)
+    if m:
+        return f"gemm_{lay[(int(m.group(1)), int(m.group(2)))]}_{EPI_NAMES[int(m.group(3))]}"
+    for key, cls in (("attn_fwd_kernel", "attn_fwd"), ("attn_bwd_dq_kernel", "attn_bwd_dq"),
+                     ("attn_bwd_dkdv_kernel", "attn_bwd_dkdv"), ("rows_copy_kernel", "rows_copy")):
+        if key in name:
+            return cls
+    return None
+
+
+def _pmc_by_dispatch(db: str, counter: str):
+    import sqlite3
+    c = sqlite3.connect(db)
+    out = {}
+    for name, disp, cn, cv in c.execute(
+            "select name, dispatch_id, counter_name, counter_value from pmc_events"):
+        if cn != counter:
+            continue
+        key = (disp, name)
+        out[key] = out.get(key, 0.0) + float(cv)
+    return out
+
+
+def summarize_pmc(fetch_cal: str, write_cal: str, fetch_db: str, write_db: str, cmds: str):
+    """Scale the counters by the calibration copy and store bytes per dispatch per class."""
+    def cal(db, counter, known):
+        vals = [v for (d, n), v in _pmc_by_dispatch(db, counter).items() if kernel_class(n) == "rows_copy"]
+        if not vals:
+            raise SystemExit(f"no calibration copy dispatch in {db}")
+        kib = sorted(vals)[len(vals) // 2]
+        return known / (kib * 1024.0), kib
+    ff, fk = cal(fetch_cal, "FETCH_SIZE", CAL_READ)
+    fw, wk = cal(write_cal, "WRITE_SIZE", CAL_WRITE)
+    per = {}
+    for counter, db, fac in (("FETCH_SIZE", fetch_db, ff), ("WRITE_SIZE", write_db, fw)):
+        for (d, n), kib in _pmc_by_dispatch(db, counter).items():
+            cls = kernel_class(n)
+            if cls is None or cls == "rows_copy":
+                continue
+            e = per.setdefault(cls, {"FETCH_SIZE": [0.0, 0], "WRITE_SIZE": [0.0, 0]})
+            e[counter][0] += kib * 1024.0 * fac
+            e[counter][1] += 1
+    table = {}
+    for cls, e in per.items():
+        f, nf = e["FETCH_SIZE"]
+        w, nw = e["WRITE_SIZE"]
+        if nf and nw:
+            table[cls] = {"fetch_bytes": round(f / nf), "write_bytes": round(w / nw),
+                          "bytes": round(f / nf + w / nw), "dispatches": nf}
+    rec = {"digest": source_digest(), "calibration": {
+               "copy_read_bytes": CAL_READ, "copy_write_bytes": CAL_WRITE,
+               "fetch_kib": fk, "write_kib": wk, "fetch_scale": ff, "write_scale": fw},
+           "per_launch": table, "commands": cmds}
+    with open(TRAFFIC_FILE, "w") as fh:
+        json.dump(rec, fh, indent=1)
+    print(json.dumps(rec, indent=1))
+
+
+def stored_traffic(cls: str):
+    try:
+        with open(TRAFFIC_FILE) as fh:
+            rec = json.load(fh)
+    except (OSError, ValueError):
+        return None
+    if rec.get("digest") != source_digest():
+        return None
+    e = rec.get("per_launch", {}).get(cls)
+    return e["bytes"] if e else None
+
+
+def copy_calibration():
+    """A plain copy of known size through the library's row gather (identity indices)."""
+    import torch
+    import paper_2607_03229_amd as mp
+    dev = torch.device("cuda:0")
+    src = torch.ones((CAL_ROWS, CAL_COLS), dtype=torch.bfloat16, device=dev)
+    dst = torch.empty_like(src)
+    idx = torch.arange(CAL_ROWS, dtype=torch.int64, device=dev)
+    for _ in range(3):
+        mp.merge_gather(src, idx, dst)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_read_bytes": CAL_READ, "copy_write_bytes": CAL_WRITE}), flush=True)
+
+
 def cpu_baseline(sample_layers: int = 8):
     """Time the CPU oracle on a bounded sample of the same workload shape: one
     224x224 image (256 patches, the smallest the size draw produces) through the
@@ -98,12 +213,23 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true",
                     help="skip the per-kernel event timing (roofline figures)")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run the known-size copy that scales the PMC byte counters")
+    ap.add_argument("--summarize-pmc", nargs=4, metavar=("FETCH_CAL", "WRITE_CAL", "FETCH", "WRITE"),
+                    help="rocprofv3 PMC databases -> profiles/hbm_traffic.json")
+    ap.add_argument("--pmc-commands", default="", help="commands recorded with --summarize-pmc")
     args = ap.parse_args()
+    if args.summarize_pmc:
+        summarize_pmc(*args.summarize_pmc, args.pmc_commands)
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one MI355X only: the encoder step runs on one GPU "
               "(see DESIGN.md for how the transpose schedule shards it).", file=sys.stderr)
         sys.exit(2)
 
+    if args.copy_calibration:
+        copy_calibration()
+        return
     import torch
     import paper_2607_03229_amd as mp
     import workload as W
@@ -187,7 +313,8 @@ def main():
         n, ms, fl = kern[dom]
         ach = fl / n / (ms / n * 1e-3) / 1e12
         roofline = {"kernel": dom, "bound": "mfma", "achieved": round(ach, 1), "peak": peak,
-                    "unit": "TFLOP/s", "frac": round(ach / peak, 4), "traffic": None,
+                    "unit": "TFLOP/s", "frac": round(ach / peak, 4),
+                    "traffic": stored_traffic(dom),
                     "launches": n, "avg_ms": round(ms / n, 4),
                     "flop_per_launch": fl / n}
 
