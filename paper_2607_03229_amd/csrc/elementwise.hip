@@ -3,13 +3,17 @@
 // rotary position, operand padding, deterministic column reductions for the
 // bias / LayerNorm-affine gradients, the split-K reduction of weight
 // gradients, and the bit-exact placeholder row scatter / gather.
+#include <algorithm>
+#include <type_traits>
+
 #include "common.h"
 #include "internal.h"
+#include "plan.h"
 
 namespace mpipe {
 namespace {
 
-constexpr int MAXC = 8;  // float4 chunks per lane: rows up to 64 * 4 * 8 = 2048 wide
+constexpr int MAXC = 8;  // float4 chunks per lane: LayerNorm rows up to 64 * 4 * 8 = 2048 wide
 
 template <class T> struct V4;
 template <> struct V4<float> {
@@ -32,8 +36,35 @@ template <> struct V4<bf16> {
   }
 };
 
+// 8 consecutive elements as two float4 (one 16-byte access for bf16, two for fp32)
+template <class T> struct V8;
+template <> struct V8<float> {
+  static __device__ __forceinline__ void load(const float* p, float4& a, float4& b) {
+    a = *reinterpret_cast<const float4*>(p);
+    b = *reinterpret_cast<const float4*>(p + 4);
+  }
+  static __device__ __forceinline__ void store(float* p, float4 a, float4 b) {
+    *reinterpret_cast<float4*>(p) = a;
+    *reinterpret_cast<float4*>(p + 4) = b;
+  }
+};
+template <> struct V8<bf16> {
+  static __device__ __forceinline__ void load(const bf16* p, float4& a, float4& b) {
+    const uint4 u = *reinterpret_cast<const uint4*>(p);
+    const bf16* e = reinterpret_cast<const bf16*>(&u);
+    a = make_float4((float)e[0], (float)e[1], (float)e[2], (float)e[3]);
+    b = make_float4((float)e[4], (float)e[5], (float)e[6], (float)e[7]);
+  }
+  static __device__ __forceinline__ void store(bf16* p, float4 a, float4 b) {
+    bf16 e[8] = {(bf16)a.x, (bf16)a.y, (bf16)a.z, (bf16)a.w,
+                 (bf16)b.x, (bf16)b.y, (bf16)b.z, (bf16)b.w};
+    *reinterpret_cast<uint4*>(p) = *reinterpret_cast<const uint4*>(e);
+  }
+};
+
 // ---- LayerNorm forward: y = (x - mean) * rstd * g + b, biased variance -------------
-template <class T>
+// MC = float4 chunks per lane (rows up to 256 MC wide): register arrays sized to the row
+template <class T, int MC>
 __global__ __launch_bounds__(256) void ln_fwd_kernel(const float* X, int64_t ldx, int64_t rows,
                                                      int n, const T* gam, const T* bet, float eps,
                                                      T* Y, int64_t ldy, float* mean, float* rstd) {
@@ -42,10 +73,10 @@ __global__ __launch_bounds__(256) void ln_fwd_kernel(const float* X, int64_t ldx
   if (row >= rows) return;
   const int nc = n / 4;
   const float* x = X + row * ldx;
-  float4 v[MAXC];
+  float4 v[MC];
   float s = 0.f;
 #pragma unroll
-  for (int i = 0; i < MAXC; ++i) {
+  for (int i = 0; i < MC; ++i) {
     const int c = l + 64 * i;
     if (c < nc) {
       v[i] = V4<float>::load(x + 4 * c);
@@ -55,7 +86,7 @@ __global__ __launch_bounds__(256) void ln_fwd_kernel(const float* X, int64_t ldx
   const float mu = warp_sum(s) / (float)n;
   float q = 0.f;
 #pragma unroll
-  for (int i = 0; i < MAXC; ++i) {
+  for (int i = 0; i < MC; ++i) {
     const int c = l + 64 * i;
     if (c < nc) {
       const float a = v[i].x - mu, b = v[i].y - mu, cc = v[i].z - mu, d = v[i].w - mu;
@@ -66,7 +97,7 @@ __global__ __launch_bounds__(256) void ln_fwd_kernel(const float* X, int64_t ldx
   const float rs = rsqrtf(var + eps);
   T* y = Y + row * ldy;
 #pragma unroll
-  for (int i = 0; i < MAXC; ++i) {
+  for (int i = 0; i < MC; ++i) {
     const int c = l + 64 * i;
     if (c < nc) {
       const float4 gg = V4<T>::load(gam + 4 * c), bb = V4<T>::load(bet + 4 * c);
@@ -90,34 +121,36 @@ __global__ __launch_bounds__(256) void ln_fwd_kernel(const float* X, int64_t ldx
 // rows (its four waves take every fourth row); the block's sums of dy*xhat and dy
 // are combined in LDS in a fixed order and written to part_g / part_b
 // [gridDim.x][n] for a deterministic reduction.
-constexpr int LN_BWD_MAX_BLOCKS = 512;
+constexpr int LN_BWD_MAX_BLOCKS = 1024;
+static_assert(LN_BWD_MAX_BLOCKS <= kPartialRowsMax, "partials must fit the workspace");
 
+template <int MC>
 __device__ __forceinline__ void combine_waves(const float4* red, int nc, float* out) {
   for (int c = threadIdx.x; c < nc; c += 256) {
     const int i = c / 64, ll = c % 64;
     float4 t = red[i * 64 + ll];
 #pragma unroll
     for (int w = 1; w < 4; ++w) {
-      const float4 u = red[(w * MAXC + i) * 64 + ll];
+      const float4 u = red[(w * MC + i) * 64 + ll];
       t.x += u.x; t.y += u.y; t.z += u.z; t.w += u.w;
     }
     *reinterpret_cast<float4*>(out + 4 * c) = t;
   }
 }
 
-template <class T>
+template <class T, int MC>
 __global__ __launch_bounds__(256) void ln_bwd_kernel(const float* dY, int64_t ldd, const float* X,
                                                      int64_t ldx, const float* mean,
                                                      const float* rstd, const T* gam, int64_t rows,
                                                      int n, int64_t rows_per_block,
                                                      const float* dres, float* dX, T* dXt,
                                                      float* part_g, float* part_b) {
-  __shared__ float4 red[4 * MAXC * 64];
+  __shared__ float4 red[4 * MC * 64];
   const int wave = threadIdx.x >> 6, l = threadIdx.x & 63;
   const int nc = n / 4;
-  float4 ag[MAXC], ab[MAXC], gm[MAXC];
+  float4 ag[MC], ab[MC], gm[MC];
 #pragma unroll
-  for (int i = 0; i < MAXC; ++i) {
+  for (int i = 0; i < MC; ++i) {
     ag[i] = ab[i] = make_float4(0.f, 0.f, 0.f, 0.f);
     const int c = l + 64 * i;
     if (c < nc) gm[i] = V4<T>::load(gam + 4 * c);
@@ -126,39 +159,44 @@ __global__ __launch_bounds__(256) void ln_bwd_kernel(const float* dY, int64_t ld
   const int64_t r1 = min(rows, r0 + rows_per_block);
   for (int64_t row = r0 + wave; row < r1; row += 4) {
     const float mu = mean[row], rs = rstd[row];
-    float4 xh[MAXC], dy[MAXC];
-    float s1 = 0.f, s2 = 0.f;
+    // every operand of the row is requested before any is used
+    float4 x[MC], dy[MC], dr[MC];
 #pragma unroll
-    for (int i = 0; i < MAXC; ++i) {
+    for (int i = 0; i < MC; ++i) {
       const int c = l + 64 * i;
       if (c < nc) {
-        const float4 x = V4<float>::load(X + row * ldx + 4 * c);
+        x[i] = V4<float>::load(X + row * ldx + 4 * c);
         dy[i] = V4<float>::load(dY + row * ldd + 4 * c);
-        xh[i] = make_float4((x.x - mu) * rs, (x.y - mu) * rs, (x.z - mu) * rs, (x.w - mu) * rs);
+        dr[i] = dres ? V4<float>::load(dres + row * ldx + 4 * c) : make_float4(0.f, 0.f, 0.f, 0.f);
+      }
+    }
+    float s1 = 0.f, s2 = 0.f;
+#pragma unroll
+    for (int i = 0; i < MC; ++i) {
+      const int c = l + 64 * i;
+      if (c < nc) {
+        x[i] = make_float4((x[i].x - mu) * rs, (x[i].y - mu) * rs, (x[i].z - mu) * rs,
+                           (x[i].w - mu) * rs);   // now xhat
         const float4 gd = make_float4(dy[i].x * gm[i].x, dy[i].y * gm[i].y, dy[i].z * gm[i].z,
                                       dy[i].w * gm[i].w);
         s1 += gd.x + gd.y + gd.z + gd.w;
-        s2 += gd.x * xh[i].x + gd.y * xh[i].y + gd.z * xh[i].z + gd.w * xh[i].w;
-        ag[i].x += dy[i].x * xh[i].x; ag[i].y += dy[i].y * xh[i].y;
-        ag[i].z += dy[i].z * xh[i].z; ag[i].w += dy[i].w * xh[i].w;
+        s2 += gd.x * x[i].x + gd.y * x[i].y + gd.z * x[i].z + gd.w * x[i].w;
+        ag[i].x += dy[i].x * x[i].x; ag[i].y += dy[i].y * x[i].y;
+        ag[i].z += dy[i].z * x[i].z; ag[i].w += dy[i].w * x[i].w;
         ab[i].x += dy[i].x; ab[i].y += dy[i].y; ab[i].z += dy[i].z; ab[i].w += dy[i].w;
       }
     }
     s1 = warp_sum(s1) / (float)n;
     s2 = warp_sum(s2) / (float)n;
 #pragma unroll
-    for (int i = 0; i < MAXC; ++i) {
+    for (int i = 0; i < MC; ++i) {
       const int c = l + 64 * i;
       if (c < nc) {
         float4 o;
-        o.x = rs * (dy[i].x * gm[i].x - s1 - xh[i].x * s2);
-        o.y = rs * (dy[i].y * gm[i].y - s1 - xh[i].y * s2);
-        o.z = rs * (dy[i].z * gm[i].z - s1 - xh[i].z * s2);
-        o.w = rs * (dy[i].w * gm[i].w - s1 - xh[i].w * s2);
-        if (dres) {
-          const float4 d = V4<float>::load(dres + row * ldx + 4 * c);
-          o.x += d.x; o.y += d.y; o.z += d.z; o.w += d.w;
-        }
+        o.x = rs * (dy[i].x * gm[i].x - s1 - x[i].x * s2) + dr[i].x;
+        o.y = rs * (dy[i].y * gm[i].y - s1 - x[i].y * s2) + dr[i].y;
+        o.z = rs * (dy[i].z * gm[i].z - s1 - x[i].z * s2) + dr[i].z;
+        o.w = rs * (dy[i].w * gm[i].w - s1 - x[i].w * s2) + dr[i].w;
         V4<float>::store(dX + row * ldx + 4 * c, o);
         if (dXt) V4<T>::store(dXt + row * ldx + 4 * c, o);
       }
@@ -166,18 +204,19 @@ __global__ __launch_bounds__(256) void ln_bwd_kernel(const float* dY, int64_t ld
   }
   // combine the four waves in a fixed order: gain sums, then shift sums
 #pragma unroll
-  for (int i = 0; i < MAXC; ++i) red[(wave * MAXC + i) * 64 + l] = ag[i];
+  for (int i = 0; i < MC; ++i) red[(wave * MC + i) * 64 + l] = ag[i];
   __syncthreads();
-  combine_waves(red, nc, part_g + (int64_t)blockIdx.x * n);
+  combine_waves<MC>(red, nc, part_g + (int64_t)blockIdx.x * n);
   __syncthreads();
 #pragma unroll
-  for (int i = 0; i < MAXC; ++i) red[(wave * MAXC + i) * 64 + l] = ab[i];
+  for (int i = 0; i < MC; ++i) red[(wave * MC + i) * 64 + l] = ab[i];
   __syncthreads();
-  combine_waves(red, nc, part_b + (int64_t)blockIdx.x * n);
+  combine_waves<MC>(red, nc, part_b + (int64_t)blockIdx.x * n);
 }
 
 // ---- column sums: part[b][c] = sum of X[r][c] over row chunk b ----------------------
 constexpr int COLSUM_MAX_CHUNKS = 256;
+static_assert(COLSUM_MAX_CHUNKS <= kPartialRowsMax, "partials must fit the workspace");
 
 template <class T>
 __global__ void colsum_partial_kernel(const T* X, int64_t ld, int64_t rows, int n,
@@ -198,18 +237,100 @@ __global__ void colsum_partial_kernel(const T* X, int64_t ld, int64_t rows, int 
   part[(int64_t)blockIdx.y * n + c] = (s0 + s1) + (s2 + s3);
 }
 
-// out[c] += sum_b part[b][c], b < nb.  One block per 64 columns; its four waves
-// take every fourth partial row and are combined in a fixed order.
-__global__ void reduce_partials_kernel(const float* part, int64_t nb, int n, float* out) {
-  __shared__ float red[4][64];
+// Vector form (n % 8 == 0, 16-byte aligned rows): lane l of a wave sums columns
+// [8l, 8l + 8) of a 512-column strip over every fourth row of the block's row chunk
+// (four of its rows in flight per iteration); the four waves are combined in LDS in a
+// fixed order.
+template <class T>
+__global__ __launch_bounds__(256) void colsum_vec_kernel(const T* X, int64_t ld, int64_t rows,
+                                                         int n, int64_t rows_per_chunk,
+                                                         float* part) {
+  __shared__ float red[4][512];
+  const int wave = threadIdx.x >> 6, l = threadIdx.x & 63;
+  const int c = blockIdx.x * 512 + 8 * l;
+  const int64_t r0 = (int64_t)blockIdx.y * rows_per_chunk;
+  const int64_t r1 = min(rows, r0 + rows_per_chunk);
+  float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  if (c < n) {
+    int64_t r = r0 + wave;
+    for (; r + 12 < r1; r += 16) {
+      const T* p0 = X + r * ld + c;
+      float4 a0, b0, a1, b1, a2, b2, a3, b3;
+      V8<T>::load(p0, a0, b0);
+      V8<T>::load(p0 + 4 * ld, a1, b1);
+      V8<T>::load(p0 + 8 * ld, a2, b2);
+      V8<T>::load(p0 + 12 * ld, a3, b3);
+      acc[0] += (a0.x + a1.x) + (a2.x + a3.x); acc[1] += (a0.y + a1.y) + (a2.y + a3.y);
+      acc[2] += (a0.z + a1.z) + (a2.z + a3.z); acc[3] += (a0.w + a1.w) + (a2.w + a3.w);
+      acc[4] += (b0.x + b1.x) + (b2.x + b3.x); acc[5] += (b0.y + b1.y) + (b2.y + b3.y);
+      acc[6] += (b0.z + b1.z) + (b2.z + b3.z); acc[7] += (b0.w + b1.w) + (b2.w + b3.w);
+    }
+    for (; r < r1; r += 4) {
+      float4 a, b;
+      V8<T>::load(X + r * ld + c, a, b);
+      acc[0] += a.x; acc[1] += a.y; acc[2] += a.z; acc[3] += a.w;
+      acc[4] += b.x; acc[5] += b.y; acc[6] += b.z; acc[7] += b.w;
+    }
+  }
+#pragma unroll
+  for (int e = 0; e < 8; ++e) red[wave][8 * l + e] = acc[e];
+  __syncthreads();
+  for (int j = threadIdx.x; j < 512; j += 256) {
+    const int cc = blockIdx.x * 512 + j;
+    if (cc < n)
+      part[(int64_t)blockIdx.y * n + cc] = (red[0][j] + red[1][j]) + (red[2][j] + red[3][j]);
+  }
+}
+
+// out[c] += sum_b part[b][c], b < nb.  One block of 16 waves per 64 columns: wave w
+// sums partial rows w, w + 16, ... with four loads in flight, and the 16 wave sums are
+// combined in a fixed order (the result depends only on nb, never on timing).
+constexpr int RED_WAVES = 16;
+__global__ __launch_bounds__(64 * RED_WAVES) void reduce_partials_kernel(const float* part,
+                                                                       int64_t nb, int n,
+                                                                       float* out) {
+  __shared__ float red[RED_WAVES][64];
   const int w = threadIdx.x >> 6, l = threadIdx.x & 63;
   const int c = blockIdx.x * 64 + l;
-  float s = 0.f;
-  if (c < n)
-    for (int64_t b = w; b < nb; b += 4) s += part[b * n + c];
-  red[w][l] = s;
+  float s0 = 0.f, s1 = 0.f, s2 = 0.f, s3 = 0.f;
+  if (c < n) {
+    int64_t b = w;
+    for (; b + 3 * RED_WAVES < nb; b += 4 * RED_WAVES) {
+      s0 += part[b * n + c];
+      s1 += part[(b + RED_WAVES) * n + c];
+      s2 += part[(b + 2 * RED_WAVES) * n + c];
+      s3 += part[(b + 3 * RED_WAVES) * n + c];
+    }
+    for (; b < nb; b += RED_WAVES) s0 += part[b * n + c];
+  }
+  red[w][l] = (s0 + s1) + (s2 + s3);
   __syncthreads();
-  if (w == 0 && c < n) out[c] += (red[0][l] + red[1][l]) + (red[2][l] + red[3][l]);
+  if (w == 0 && c < n) {
+    float t = 0.f;
+#pragma unroll
+    for (int k = 0; k < RED_WAVES; ++k) t += red[k][l];
+    out[c] += t;
+  }
+}
+
+// out[m][n] += sum_s part[s][m][n], four columns per thread (N % 4 == 0, ldo % 4 == 0,
+// M * N / 4 < 2^31)
+__global__ void splitk_reduce4_kernel(const float* part, int splits, int M, int N4, float* out,
+                                      int64_t ldo) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= M * N4) return;
+  const int m = i / N4, c = i - m * N4;
+  const int64_t stride = (int64_t)M * N4;
+  const float4* p = reinterpret_cast<const float4*>(part) + i;
+  float4 acc = p[0];
+  for (int k = 1; k < splits; ++k) {
+    const float4 v = p[k * stride];
+    acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
+  }
+  float4* o = reinterpret_cast<float4*>(out + (int64_t)m * ldo) + c;
+  float4 r = *o;
+  r.x += acc.x; r.y += acc.y; r.z += acc.z; r.w += acc.w;
+  *o = r;
 }
 
 // out[m][n] += sum_s part[s][m][n]   (partials are dense [M][N])
@@ -268,6 +389,43 @@ __global__ void rope_kernel(T* qk, int64_t ld, int64_t rows, int heads, int d, i
   V4<T>::store(v + j0 + half, make_float4(o2[0], o2[1], o2[2], o2[3]));
 }
 
+// Eight consecutive pairs per thread (16-byte accesses; needs d % 16 == 0).
+template <class T>
+__global__ void rope8_kernel(T* qk, int64_t ld, int64_t rows, int heads, int d, int kcol,
+                             const int32_t* pos, const float2* tab, int inverse) {
+  const int half = d / 2, quarter = d / 4;
+  const int groups = half / 8;                       // 8-pair groups per head
+  const int per_row = 2 * heads * groups;
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= rows * per_row) return;
+  const int64_t r = i / per_row;
+  int rem = (int)(i - r * per_row);
+  const int which = rem / (heads * groups);
+  rem -= which * heads * groups;
+  const int hd = rem / groups, j0 = 8 * (rem - hd * groups);
+  const int32_t pp = pos[r];
+  T* v = qk + r * ld + (which ? kcol : 0) + hd * d;
+  float4 a0, a1, b0, b1;
+  V8<T>::load(v + j0, a0, a1);
+  V8<T>::load(v + j0 + half, b0, b1);
+  const float x1[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
+  const float x2[8] = {b0.x, b0.y, b0.z, b0.w, b1.x, b1.y, b1.z, b1.w};
+  float o1[8], o2[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const int j = j0 + e;
+    const int coord = (j < quarter) ? (pp >> 16) : (pp & 0xFFFF);
+    const float2 cs = tab[coord * quarter + (j < quarter ? j : j - quarter)];
+    const float sn = inverse ? -cs.y : cs.y;
+    o1[e] = x1[e] * cs.x - x2[e] * sn;
+    o2[e] = x2[e] * cs.x + x1[e] * sn;
+  }
+  V8<T>::store(v + j0, make_float4(o1[0], o1[1], o1[2], o1[3]),
+               make_float4(o1[4], o1[5], o1[6], o1[7]));
+  V8<T>::store(v + j0 + half, make_float4(o2[0], o2[1], o2[2], o2[3]),
+               make_float4(o2[4], o2[5], o2[6], o2[7]));
+}
+
 // ---- bit-exact row scatter / gather ---------------------------------------------------
 // dst row idx[j] <- src row j (scatter) or dst row j <- src row idx[j] (gather).
 // Rows with an index outside [0, n_rows) are skipped.
@@ -309,6 +467,38 @@ __global__ void fill_i32_kernel(int32_t* p, int64_t n, int32_t v) {
 
 inline int blocks_for(int64_t n, int t = 256) { return (int)((n + t - 1) / t); }
 
+// Blocks of `kernel` resident on the whole device at once (one full round), from the
+// occupancy calculator; computed once per (signature, TAG) -- TAG tells apart
+// instantiations that share a signature.
+template <int TAG, class K>
+int64_t resident_blocks(K kernel, int threads) {
+  static const int64_t n = [&] {
+    int dev = 0, cus = 0, per = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, kernel, threads, 0) != hipSuccess)
+      return (int64_t)1 << 30;   // unknown: no cap
+    return (int64_t)(per > 0 ? per : 1) * (cus > 0 ? cus : 1);
+  }();
+  return n;
+}
+
+// calls f(integral_constant<int, MC>) for the float4-per-lane count of a LayerNorm row
+template <class F>
+bool dispatch_mc(int mc, F&& f) {
+  switch (mc) {
+    case 1: f(std::integral_constant<int, 1>{}); return true;
+    case 2: f(std::integral_constant<int, 2>{}); return true;
+    case 3: f(std::integral_constant<int, 3>{}); return true;
+    case 4: f(std::integral_constant<int, 4>{}); return true;
+    case 5: f(std::integral_constant<int, 5>{}); return true;
+    case 6: f(std::integral_constant<int, 6>{}); return true;
+    case 7: f(std::integral_constant<int, 7>{}); return true;
+    case 8: f(std::integral_constant<int, 8>{}); return true;
+  }
+  return false;
+}
+
 }  // namespace
 
 hipError_t layernorm_fwd(int dtype, const float* X, int64_t ldx, int64_t rows, int n,
@@ -316,12 +506,17 @@ hipError_t layernorm_fwd(int dtype, const float* X, int64_t ldx, int64_t rows, i
                          float* mean, float* rstd, hipStream_t s) {
   if (rows == 0) return hipSuccess;
   const dim3 grid((unsigned)((rows + 3) / 4));
-  if (dtype == DT_BF16)
-    hipLaunchKernelGGL(ln_fwd_kernel<bf16>, grid, dim3(256), 0, s, X, ldx, rows, n,
-                       (const bf16*)g, (const bf16*)b, eps, (bf16*)Y, ldy, mean, rstd);
-  else
-    hipLaunchKernelGGL(ln_fwd_kernel<float>, grid, dim3(256), 0, s, X, ldx, rows, n,
-                       (const float*)g, (const float*)b, eps, (float*)Y, ldy, mean, rstd);
+  const int mc = (n / 4 + 63) / 64;
+  auto go = [&](auto MCc) {
+    constexpr int MC = decltype(MCc)::value;
+    if (dtype == DT_BF16)
+      hipLaunchKernelGGL((ln_fwd_kernel<bf16, MC>), grid, dim3(256), 0, s, X, ldx, rows, n,
+                         (const bf16*)g, (const bf16*)b, eps, (bf16*)Y, ldy, mean, rstd);
+    else
+      hipLaunchKernelGGL((ln_fwd_kernel<float, MC>), grid, dim3(256), 0, s, X, ldx, rows, n,
+                         (const float*)g, (const float*)b, eps, (float*)Y, ldy, mean, rstd);
+  };
+  if (!dispatch_mc(mc, go)) return hipErrorInvalidValue;
   return hipGetLastError();
 }
 
@@ -335,21 +530,30 @@ hipError_t layernorm_bwd(int dtype, const float* dY, int64_t ldd, const float* X
                          const float* dres, float* dX, void* dXt, float* part_g, float* part_b,
                          float* grad_g, float* grad_b, hipStream_t s) {
   if (rows == 0) return hipSuccess;
-  const int64_t nblk = layernorm_bwd_partial_rows(rows);
-  const int64_t rpb = (rows + nblk - 1) / nblk;
-  if (dtype == DT_BF16)
-    hipLaunchKernelGGL(ln_bwd_kernel<bf16>, dim3((unsigned)nblk), dim3(256), 0, s, dY, ldd, X, ldx,
-                       mean, rstd, (const bf16*)g, rows, n, rpb, dres, dX, (bf16*)dXt, part_g,
-                       part_b);
-  else
-    hipLaunchKernelGGL(ln_bwd_kernel<float>, dim3((unsigned)nblk), dim3(256), 0, s, dY, ldd, X,
-                       ldx, mean, rstd, (const float*)g, rows, n, rpb, dres, dX, (float*)dXt,
-                       part_g, part_b);
+  // one round of resident blocks (never more than the partial rows the caller sized)
+  const int mc = (n / 4 + 63) / 64;
+  int64_t nblk = 0;
+  auto go = [&](auto MCc) {
+    constexpr int MC = decltype(MCc)::value;
+    auto launch = [&](auto kern, auto gptr, auto dxt) {
+      nblk = std::min(layernorm_bwd_partial_rows(rows), resident_blocks<MC>(kern, 256));
+      const int64_t rpb = (rows + nblk - 1) / nblk;
+      hipLaunchKernelGGL(kern, dim3((unsigned)nblk), dim3(256), 0, s, dY, ldd, X, ldx, mean, rstd,
+                         gptr, rows, n, rpb, dres, dX, dxt, part_g, part_b);
+    };
+    if (dtype == DT_BF16)
+      launch(ln_bwd_kernel<bf16, MC>, (const bf16*)g, (bf16*)dXt);
+    else
+      launch(ln_bwd_kernel<float, MC>, (const float*)g, (float*)dXt);
+  };
+  if (!dispatch_mc(mc, go)) return hipErrorInvalidValue;
   const dim3 rg((unsigned)((n + 63) / 64));
   if (grad_g)
-    hipLaunchKernelGGL(reduce_partials_kernel, rg, dim3(256), 0, s, part_g, nblk, n, grad_g);
+    hipLaunchKernelGGL(reduce_partials_kernel, rg, dim3(64 * RED_WAVES), 0, s, part_g, nblk, n,
+                       grad_g);
   if (grad_b)
-    hipLaunchKernelGGL(reduce_partials_kernel, rg, dim3(256), 0, s, part_b, nblk, n, grad_b);
+    hipLaunchKernelGGL(reduce_partials_kernel, rg, dim3(64 * RED_WAVES), 0, s, part_b, nblk, n,
+                       grad_b);
   return hipGetLastError();
 }
 
@@ -363,21 +567,38 @@ hipError_t colsum_accumulate(int dtype_in, const void* X, int64_t ld, int64_t ro
   if (rows == 0) return hipSuccess;
   const int64_t nb = colsum_partial_rows(rows);
   const int64_t rpc = (rows + nb - 1) / nb;
-  const dim3 grid((unsigned)blocks_for(n), (unsigned)nb);
-  if (dtype_in == DT_BF16)
-    hipLaunchKernelGGL(colsum_partial_kernel<bf16>, grid, dim3(256), 0, s, (const bf16*)X, ld,
-                       rows, n, rpc, part);
-  else
-    hipLaunchKernelGGL(colsum_partial_kernel<float>, grid, dim3(256), 0, s, (const float*)X, ld,
-                       rows, n, rpc, part);
-  hipLaunchKernelGGL(reduce_partials_kernel, dim3((unsigned)((n + 63) / 64)), dim3(256), 0, s,
-                     part, nb, n, out);
+  const bool vec = n % 8 == 0 && ld % 8 == 0 && (reinterpret_cast<uintptr_t>(X) & 15) == 0;
+  if (vec) {
+    const dim3 grid((unsigned)((n + 511) / 512), (unsigned)nb);
+    if (dtype_in == DT_BF16)
+      hipLaunchKernelGGL(colsum_vec_kernel<bf16>, grid, dim3(256), 0, s, (const bf16*)X, ld, rows,
+                         n, rpc, part);
+    else
+      hipLaunchKernelGGL(colsum_vec_kernel<float>, grid, dim3(256), 0, s, (const float*)X, ld,
+                         rows, n, rpc, part);
+  } else {
+    const dim3 grid((unsigned)blocks_for(n), (unsigned)nb);
+    if (dtype_in == DT_BF16)
+      hipLaunchKernelGGL(colsum_partial_kernel<bf16>, grid, dim3(256), 0, s, (const bf16*)X, ld,
+                         rows, n, rpc, part);
+    else
+      hipLaunchKernelGGL(colsum_partial_kernel<float>, grid, dim3(256), 0, s, (const float*)X, ld,
+                         rows, n, rpc, part);
+  }
+  hipLaunchKernelGGL(reduce_partials_kernel, dim3((unsigned)((n + 63) / 64)), dim3(64 * RED_WAVES),
+                     0, s, part, nb, n, out);
   return hipGetLastError();
 }
 
 hipError_t splitk_reduce(const float* part, int splits, int64_t M, int64_t N, float* out,
                          int64_t ldo, hipStream_t s) {
   if (M * N == 0) return hipSuccess;
+  if (N % 4 == 0 && ldo % 4 == 0 && M * N / 4 < (int64_t)1 << 31 &&
+      (reinterpret_cast<uintptr_t>(part) & 15) == 0 && (reinterpret_cast<uintptr_t>(out) & 15) == 0) {
+    hipLaunchKernelGGL(splitk_reduce4_kernel, dim3(blocks_for(M * N / 4)), dim3(256), 0, s, part,
+                       splits, (int)M, (int)(N / 4), out, ldo);
+    return hipGetLastError();
+  }
   hipLaunchKernelGGL(splitk_reduce_kernel, dim3(blocks_for(M * N)), dim3(256), 0, s, part, splits,
                      M, N, out, ldo);
   return hipGetLastError();
@@ -401,6 +622,18 @@ hipError_t rope(int dtype, void* qk, int64_t ld, int64_t rows, int heads, int d,
   const int64_t n = rows * 2 * heads * (d / 8);  // (q and k) x heads x 4-pair groups
   if (n == 0) return hipSuccess;
   const float2* t = reinterpret_cast<const float2*>(tab);
+  const int esz = dtype == DT_BF16 ? 2 : 4;
+  if (d % 16 == 0 && (ld * esz) % 16 == 0 && (kcol * esz) % 16 == 0 &&
+      (reinterpret_cast<uintptr_t>(qk) & 15) == 0) {   // eight pairs per thread
+    const int64_t n8 = rows * 2 * heads * (d / 16);
+    if (dtype == DT_BF16)
+      hipLaunchKernelGGL(rope8_kernel<bf16>, dim3(blocks_for(n8)), dim3(256), 0, s, (bf16*)qk, ld,
+                         rows, heads, d, kcol, pos, t, inverse);
+    else
+      hipLaunchKernelGGL(rope8_kernel<float>, dim3(blocks_for(n8)), dim3(256), 0, s, (float*)qk,
+                         ld, rows, heads, d, kcol, pos, t, inverse);
+    return hipGetLastError();
+  }
   if (dtype == DT_BF16)
     hipLaunchKernelGGL(rope_kernel<bf16>, dim3(blocks_for(n)), dim3(256), 0, s, (bf16*)qk, ld,
                        rows, heads, d, kcol, pos, t, inverse);

@@ -371,7 +371,7 @@ mpipe_status backward(Ctx& x, const void* patches, const char* tape, const void*
   float* delta = reinterpret_cast<float*>(x.ws + P.ws_delta);
   char* dqkv = x.ws + P.ws_dqkv;
   float* part = reinterpret_cast<float*>(x.ws + P.ws_part);
-  const int64_t part_half = 512 * std::max({3 * h, m, 4 * h, H, (int64_t)c.kpe});
+  const int64_t part_half = kPartialRowsMax * std::max({3 * h, m, 4 * h, H, (int64_t)c.kpe});
 
   MP_RET(pad_pe(x, patches));
   const void *Xp, *Wpe;

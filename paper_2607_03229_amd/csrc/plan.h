@@ -59,6 +59,10 @@ struct MergerSet {
   size_t um, gm;                 // [Tm][4h] pre-activation / GELU output
 };
 
+// Upper bound of the partial-sum rows of the deterministic column reductions (LayerNorm
+// backward blocks, column-sum chunks); the workspace holds this many rows per reduction.
+constexpr int64_t kPartialRowsMax = 1024;
+
 struct GemmSplit {
   int splits = 1;
   int kps = 0;
