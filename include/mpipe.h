@@ -50,11 +50,15 @@
  *
  * Ownership and streams: the caller allocates every device buffer (weights,
  * gradients, patches, merged, embeddings, tape, workspace).  A handle holds
- * only the configuration and a small pinned host staging area for the
- * per-call metadata; it is not thread-safe.  All device work is enqueued on
- * the caller's stream (a hipStream_t passed as void*); no call synchronizes it
- * except to reuse the staging area of a still-running earlier call.  Host
- * metadata pointers are read during the call only.
+ * only the configuration, a small pinned host staging area for the per-call
+ * metadata and (after the first backward) one internal stream; it is not
+ * thread-safe.  All device work is ordered on the caller's stream (a
+ * hipStream_t passed as void*): it starts after the work already enqueued there
+ * and the stream does not pass the call's last kernel until all of it is done
+ * (the backward forks its weight-gradient work onto the internal stream and
+ * joins it back, see mpipe_encoder_set_side_stream).  No call synchronizes the
+ * stream except to reuse the staging area of a still-running earlier call.
+ * Host metadata pointers are read during the call only.
  *
  * Errors: every call returns an mpipe_status; all metadata checks run on the
  * host before any launch, so a non-OK status means nothing was enqueued.
@@ -140,6 +144,17 @@ mpipe_status mpipe_encoder_bwd(mpipe_encoder* enc, const void* weights, const vo
                                size_t tape_bytes, const void* d_merged, float* d_weights,
                                void* d_patches, void* workspace, size_t workspace_bytes,
                                void* hip_stream);
+
+/* Backward stream use.  enable != 0 (the default): the weight- and bias-gradient
+ * GEMMs and column sums, which nothing else in the backward reads, run on an
+ * internal stream of the handle (created on the current device at the first
+ * backward, default priority), forked from the caller's stream after each
+ * gradient buffer is produced and joined back before mpipe_encoder_bwd returns;
+ * the caller's stream waits for them only before it overwrites a buffer they
+ * read.  enable == 0: everything runs on the caller's stream.  The results are
+ * bitwise the same either way (same kernels, same operands, same order per
+ * output).  Overlapping backward calls on one handle are not supported. */
+mpipe_status mpipe_encoder_set_side_stream(mpipe_encoder* enc, int32_t enable);
 
 /* Seam Gather, local half (Table 2, Replicated -> Sharded, forward):
  * embeds[idx[j]][:] = merged[j][:] for j < n_merged, a bit-exact row copy.

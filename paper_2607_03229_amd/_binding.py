@@ -71,6 +71,7 @@ def load():
         "mpipe_merge_check_indices": (st, [P, i64, i64, P, P, P]),
         "mpipe_last_error": (C.c_char_p, []),
         "mpipe_profile_enable": (st, [P, i32]),
+        "mpipe_encoder_set_side_stream": (st, [P, i32]),
         "mpipe_profile_read": (i32, [P, P, i32, P, i32, P, P, P]),
         "mpipe_op_gemm": (st, [i32, i32, i32, i32, i32, i32, P, i64, P, i64, P, i64, P, P, i64,
                                P, i64, i32, i32, i64, P]),
@@ -191,6 +192,10 @@ class Encoder:
             self._h, _ptr(weights), _ptr(patches), cup, max(len(cu) - 1, 0), gp, g.shape[0],
             int(trainable), _ptr(tape), tb, _ptr(d_merged), _ptr(d_weights), _ptr(d_patches),
             _ptr(workspace), wb, _stream(stream)), allow=(OK, NOOP_FROZEN))
+
+    def set_side_stream(self, enable: bool):
+        """Backward weight-gradient work on the handle's internal stream (default) or not."""
+        _check(self.L.mpipe_encoder_set_side_stream(self._h, int(enable)))
 
     # -- kernel timing --
     def profile(self, enable: bool):

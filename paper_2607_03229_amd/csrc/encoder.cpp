@@ -50,6 +50,12 @@ struct mpipe_encoder {
   bool prof = false;
   std::vector<Rec> recs;
   std::vector<hipEvent_t> pool;
+  // Weight-gradient side stream of the backward (default priority) and its sync events:
+  // 0 fork (caller -> side), 1..4 buffer-free signals (side -> caller), 5 join.
+  bool side_on = true;
+  hipStream_t side = nullptr;
+  int side_dev = -1;
+  hipEvent_t sync[6] = {};
 
   hipEvent_t event() {
     if (!pool.empty()) {
@@ -117,19 +123,23 @@ struct Ctx {
   mpipe_encoder* e;
   const Cfg& c;
   const Plan& P;
-  hipStream_t s;
+  hipStream_t s;   // the caller's stream (critical path)
   const char* w;   // weights (device)
   char* ws;        // workspace (device)
   int dt;
   int64_t E;
+  hipStream_t s2 = nullptr;   // weight-gradient work (== s when there is no side stream)
   const char* W(int i) const { return w + e->params[i].off * E; }
   float* grad(float* dw, int i) const { return dw + e->params[i].off; }
 };
 
-mpipe_status gemm_call(Ctx& x, int layout, int epi, GemmArgs a) {
+mpipe_status gemm_on(Ctx& x, hipStream_t st, int layout, int epi, GemmArgs a) {
   const double fl = 2.0 * a.M * a.N * (double)a.K;
-  MP_CHECK(run(x.e, x.s, gemm_name(layout, epi), fl, [&] { return gemm(x.dt, layout, epi, a, x.s); }));
+  MP_CHECK(run(x.e, st, gemm_name(layout, epi), fl, [&] { return gemm(x.dt, layout, epi, a, st); }));
   return MPIPE_OK;
+}
+mpipe_status gemm_call(Ctx& x, int layout, int epi, GemmArgs a) {
+  return gemm_on(x, x.s, layout, epi, a);
 }
 
 GemmArgs ga(const void* A, int64_t lda, const void* B, int64_t ldb, int64_t M, int64_t N,
@@ -156,25 +166,84 @@ mpipe_status dw_gemm(Ctx& x, const void* A, int64_t lda, const void* B, int64_t 
     a.C = out;
     a.ldc = ldo;
     a.beta = 1;
-    return gemm_call(x, GEMM_TN, EPI_F32, a);
+    return gemm_on(x, x.s2, GEMM_TN, EPI_F32, a);
   }
   float* part = reinterpret_cast<float*>(x.ws + x.P.ws_dwpart);
   a.C = part;
   a.ldc = N;
   a.kps = sp.kps;
   a.split_stride = M * N;
-  mpipe_status st = gemm_call(x, GEMM_TN, EPI_F32, a);
+  mpipe_status st = gemm_on(x, x.s2, GEMM_TN, EPI_F32, a);
   if (st) return st;
-  MP_CHECK(run(x.e, x.s, "splitk_reduce", 0, [&] { return splitk_reduce(part, sp.splits, M, N, out, ldo, x.s); }));
+  MP_CHECK(run(x.e, x.s2, "splitk_reduce", 0,
+               [&] { return splitk_reduce(part, sp.splits, M, N, out, ldo, x.s2); }));
   return MPIPE_OK;
 }
 
 mpipe_status colsum(Ctx& x, int dtype_in, const void* X, int64_t ld, int64_t rows, int n,
                     float* out) {
-  float* part = reinterpret_cast<float*>(x.ws + x.P.ws_part);
-  MP_CHECK(run(x.e, x.s, "colsum", 0,
-               [&] { return colsum_accumulate(dtype_in, X, ld, rows, n, part, out, x.s); }));
+  float* part = reinterpret_cast<float*>(x.ws + x.P.ws_cpart);
+  MP_CHECK(run(x.e, x.s2, "colsum", 0,
+               [&] { return colsum_accumulate(dtype_in, X, ld, rows, n, part, out, x.s2); }));
   return MPIPE_OK;
+}
+
+// Stream hand-offs of the backward: fork makes everything enqueued on the caller's stream
+// so far visible to the side stream; release(i) marks on the side stream that the buffers
+// its gradient work reads are free again, and acquire(i) makes the caller's stream wait for
+// that before it overwrites them.
+struct SideSync {
+  Ctx& x;
+  bool on;
+  bool recorded[6] = {};
+  hipError_t fork() {
+    if (!on) return hipSuccess;
+    hipError_t r = hipEventRecord(x.e->sync[0], x.s);
+    return r != hipSuccess ? r : hipStreamWaitEvent(x.s2, x.e->sync[0], 0);
+  }
+  hipError_t release(int i) {
+    if (!on) return hipSuccess;
+    recorded[i] = true;
+    return hipEventRecord(x.e->sync[i], x.s2);
+  }
+  hipError_t acquire(int i) {
+    if (!on || !recorded[i]) return hipSuccess;
+    return hipStreamWaitEvent(x.s, x.e->sync[i], 0);
+  }
+  hipError_t join() {
+    if (!on) return hipSuccess;
+    hipError_t r = hipEventRecord(x.e->sync[5], x.s2);
+    return r != hipSuccess ? r : hipStreamWaitEvent(x.s, x.e->sync[5], 0);
+  }
+};
+enum { FREE_DU = 1, FREE_DH = 2, FREE_DHM = 3, FREE_DQKV = 4 };
+
+// Creates the side stream and its events on the current device (once per device).
+hipError_t ensure_side(mpipe_encoder* e) {
+  int dev = 0;
+  hipError_t r = hipGetDevice(&dev);
+  if (r != hipSuccess) return r;
+  if (e->side && e->side_dev == dev) return hipSuccess;
+  if (e->side) {
+    hipStreamSynchronize(e->side);
+    hipStreamDestroy(e->side);
+    for (auto& ev : e->sync) {
+      if (ev) hipEventDestroy(ev);
+      ev = nullptr;
+    }
+    e->side = nullptr;
+  }
+  r = hipStreamCreateWithFlags(&e->side, hipStreamNonBlocking);
+  if (r != hipSuccess) {
+    e->side = nullptr;
+    return r;
+  }
+  for (auto& ev : e->sync) {
+    r = hipEventCreateWithFlags(&ev, hipEventDisableTiming);
+    if (r != hipSuccess) return r;
+  }
+  e->side_dev = dev;
+  return hipSuccess;
 }
 
 mpipe_status upload_meta(mpipe_encoder* e, const Plan& P, char* ws, hipStream_t s) {
@@ -378,21 +447,28 @@ mpipe_status backward(Ctx& x, const void* patches, const char* tape, const void*
   int64_t ldx;
   pe_operands(x, patches, Xp, Wpe, ldx);
 
+  // Weight and bias gradients feed nothing else in the backward: they run on the side
+  // stream (x.s2), which forks off after each gradient buffer is produced; the caller's
+  // stream waits for a buffer's side readers only before it overwrites that buffer.
+  SideSync ss{x, x.s2 != x.s};
+  MP_CHECK(ss.fork());
   // merger
+  MP_RET(dw_gemm(x, dM, H, base + MS.gm, 4 * h, H, 4 * h, Tm, x.grad(dw, merger_param(c, M_FC2W)), 4 * h));
+  MP_RET(colsum(x, x.dt, dM, H, Tm, (int)H, x.grad(dw, merger_param(c, M_FC2B))));
   {
     GemmArgs a = ga(dM, H, x.W(merger_param(c, M_FC2W)), 4 * h, Tm, 4 * h, H, du, 4 * h);
     a.aux = base + MS.um;
     a.ld_aux = 4 * h;
     MP_RET(gemm_call(x, GEMM_NN, EPI_GELU_BWD, a));
   }
-  MP_RET(dw_gemm(x, dM, H, base + MS.gm, 4 * h, H, 4 * h, Tm, x.grad(dw, merger_param(c, M_FC2W)), 4 * h));
-  MP_RET(colsum(x, x.dt, dM, H, Tm, (int)H, x.grad(dw, merger_param(c, M_FC2B))));
+  MP_CHECK(ss.fork());
+  MP_RET(dw_gemm(x, du, 4 * h, base + MS.z, 4 * h, 4 * h, 4 * h, Tm, x.grad(dw, merger_param(c, M_FC1W)), 4 * h));
+  MP_RET(colsum(x, x.dt, du, 4 * h, Tm, (int)(4 * h), x.grad(dw, merger_param(c, M_FC1B))));
+  MP_CHECK(ss.release(FREE_DU));
   {
     GemmArgs a = ga(du, 4 * h, x.W(merger_param(c, M_FC1W)), 4 * h, Tm, 4 * h, 4 * h, dx32, 4 * h);
     MP_RET(gemm_call(x, GEMM_NN, EPI_F32, a));
   }
-  MP_RET(dw_gemm(x, du, 4 * h, base + MS.z, 4 * h, 4 * h, 4 * h, Tm, x.grad(dw, merger_param(c, M_FC1W)), 4 * h));
-  MP_RET(colsum(x, x.dt, du, 4 * h, Tm, (int)(4 * h), x.grad(dw, merger_param(c, M_FC1B))));
   MP_CHECK(run(x.e, x.s, "layernorm_bwd", 0, [&] {
     return layernorm_bwd(x.dt, dx32, h, reinterpret_cast<const float*>(base + MS.hfin), h,
                          reinterpret_cast<const float*>(base + MS.meanz),
@@ -407,20 +483,26 @@ mpipe_status backward(Ctx& x, const void* patches, const char* tape, const void*
     const float* hin = reinterpret_cast<const float*>(base + S.hin);
     const float* hmid = reinterpret_cast<const float*>(base + S.hmid);
     // MLP: H_out = H_mid + GELU(B W1^T + b1) W2^T + b2
+    MP_CHECK(ss.fork());   // dh, dht
+    MP_RET(dw_gemm(x, dht, h, base + S.g, m, h, m, N, x.grad(dw, blk_param(c, l, B_FC2W)), m));
+    MP_RET(colsum(x, DT_F32, dh, h, N, (int)h, x.grad(dw, blk_param(c, l, B_FC2B))));
+    MP_CHECK(ss.release(FREE_DH));
+    MP_CHECK(ss.acquire(FREE_DU));
     {
       GemmArgs a = ga(dht, h, x.W(blk_param(c, l, B_FC2W)), m, N, m, h, du, m);
       a.aux = base + S.u;
       a.ld_aux = m;
       MP_RET(gemm_call(x, GEMM_NN, EPI_GELU_BWD, a));
     }
-    MP_RET(dw_gemm(x, dht, h, base + S.g, m, h, m, N, x.grad(dw, blk_param(c, l, B_FC2W)), m));
-    MP_RET(colsum(x, DT_F32, dh, h, N, (int)h, x.grad(dw, blk_param(c, l, B_FC2B))));
+    MP_CHECK(ss.fork());   // du
+    MP_RET(dw_gemm(x, du, m, base + S.b, h, m, h, N, x.grad(dw, blk_param(c, l, B_FC1W)), h));
+    MP_RET(colsum(x, x.dt, du, m, N, (int)m, x.grad(dw, blk_param(c, l, B_FC1B))));
+    MP_CHECK(ss.release(FREE_DU));
     {
       GemmArgs a = ga(du, m, x.W(blk_param(c, l, B_FC1W)), h, N, h, m, dx32, h);
       MP_RET(gemm_call(x, GEMM_NN, EPI_F32, a));
     }
-    MP_RET(dw_gemm(x, du, m, base + S.b, h, m, h, N, x.grad(dw, blk_param(c, l, B_FC1W)), h));
-    MP_RET(colsum(x, x.dt, du, m, N, (int)m, x.grad(dw, blk_param(c, l, B_FC1B))));
+    MP_CHECK(ss.acquire(FREE_DHM));
     MP_CHECK(run(x.e, x.s, "layernorm_bwd", 0, [&] {
       return layernorm_bwd(x.dt, dx32, h, hmid, h, reinterpret_cast<const float*>(base + S.mean2),
                            reinterpret_cast<const float*>(base + S.rstd2),
@@ -429,12 +511,15 @@ mpipe_status backward(Ctx& x, const void* patches, const char* tape, const void*
                            x.grad(dw, blk_param(c, l, B_LN2B)), x.s);
     }));
     // attention: H_mid = H_in + O Wo^T + bo
+    MP_CHECK(ss.fork());   // dhm, dhmt
+    MP_RET(dw_gemm(x, dhmt, h, base + S.o, h, h, h, N, x.grad(dw, blk_param(c, l, B_PROJW)), h));
+    MP_RET(colsum(x, DT_F32, dhm, h, N, (int)h, x.grad(dw, blk_param(c, l, B_PROJB))));
+    MP_CHECK(ss.release(FREE_DHM));
     {
       GemmArgs a = ga(dhmt, h, x.W(blk_param(c, l, B_PROJW)), h, N, h, h, dO, h);
       MP_RET(gemm_call(x, GEMM_NN, EPI_STORE, a));
     }
-    MP_RET(dw_gemm(x, dhmt, h, base + S.o, h, h, h, N, x.grad(dw, blk_param(c, l, B_PROJW)), h));
-    MP_RET(colsum(x, DT_F32, dhm, h, N, (int)h, x.grad(dw, blk_param(c, l, B_PROJB))));
+    MP_CHECK(ss.acquire(FREE_DQKV));
     {
       const char* qkv = base + S.qkv;
       AttnArgs qa = attn_args(x, qkv, false), ka = attn_args(x, qkv, true);
@@ -457,12 +542,15 @@ mpipe_status backward(Ctx& x, const void* patches, const char* tape, const void*
     MP_CHECK(run(x.e, x.s, "rope", 0, [&] {
       return rope(x.dt, dqkv, 3 * h, N, c.heads, c.d, (int)h, pos, freq, 1, x.s);
     }));
+    MP_CHECK(ss.fork());   // dqkv
+    MP_RET(dw_gemm(x, dqkv, 3 * h, base + S.a, h, 3 * h, h, N, x.grad(dw, blk_param(c, l, B_QKVW)), h));
+    MP_RET(colsum(x, x.dt, dqkv, 3 * h, N, (int)(3 * h), x.grad(dw, blk_param(c, l, B_QKVB))));
+    MP_CHECK(ss.release(FREE_DQKV));
     {
       GemmArgs a = ga(dqkv, 3 * h, x.W(blk_param(c, l, B_QKVW)), h, N, h, 3 * h, dx32, h);
       MP_RET(gemm_call(x, GEMM_NN, EPI_F32, a));
     }
-    MP_RET(dw_gemm(x, dqkv, 3 * h, base + S.a, h, 3 * h, h, N, x.grad(dw, blk_param(c, l, B_QKVW)), h));
-    MP_RET(colsum(x, x.dt, dqkv, 3 * h, N, (int)(3 * h), x.grad(dw, blk_param(c, l, B_QKVB))));
+    MP_CHECK(ss.acquire(FREE_DH));
     MP_CHECK(run(x.e, x.s, "layernorm_bwd", 0, [&] {
       return layernorm_bwd(x.dt, dx32, h, hin, h, reinterpret_cast<const float*>(base + S.mean1),
                            reinterpret_cast<const float*>(base + S.rstd1),
@@ -472,6 +560,7 @@ mpipe_status backward(Ctx& x, const void* patches, const char* tape, const void*
     }));
   }
   // patch embedding (the trainable source: nothing goes upstream unless asked)
+  MP_CHECK(ss.fork());   // dh, dht
   MP_RET(dw_gemm(x, dht, h, Xp, ldx, h, c.kpe, N, x.grad(dw, P_PE_W), c.kpe));
   MP_RET(colsum(x, DT_F32, dh, h, N, (int)h, x.grad(dw, P_PE_B)));
   if (d_patches) {
@@ -515,7 +604,19 @@ void mpipe_encoder_destroy(mpipe_encoder* e) {
     hipEventDestroy(r.b);
   }
   for (auto ev : e->pool) hipEventDestroy(ev);
+  if (e->side) {
+    hipStreamSynchronize(e->side);
+    hipStreamDestroy(e->side);
+  }
+  for (auto ev : e->sync)
+    if (ev) hipEventDestroy(ev);
   delete e;
+}
+
+mpipe_status mpipe_encoder_set_side_stream(mpipe_encoder* e, int32_t enable) {
+  MP_RET(check_handle(e));
+  e->side_on = enable != 0;
+  return MPIPE_OK;
 }
 
 int64_t mpipe_param_count(const mpipe_encoder_cfg* cfg) {
@@ -581,6 +682,7 @@ mpipe_status mpipe_encoder_fwd(mpipe_encoder* e, const void* weights, const void
   MP_RET(upload_meta(e, P, reinterpret_cast<char*>(ws), s));
   Ctx x{e, e->cfg, P, s, reinterpret_cast<const char*>(weights), reinterpret_cast<char*>(ws),
         e->cfg.dtype, e->cfg.esz};
+  x.s2 = s;
   return forward(x, patches, merged, reinterpret_cast<char*>(tape));
 }
 
@@ -607,7 +709,19 @@ mpipe_status mpipe_encoder_bwd(mpipe_encoder* e, const void* weights, const void
   MP_RET(upload_meta(e, P, reinterpret_cast<char*>(ws), s));
   Ctx x{e, e->cfg, P, s, reinterpret_cast<const char*>(weights), reinterpret_cast<char*>(ws),
         e->cfg.dtype, e->cfg.esz};
-  return backward(x, patches, reinterpret_cast<const char*>(tape), d_merged, d_weights, d_patches);
+  x.s2 = s;
+  if (e->side_on) {
+    MP_CHECK(ensure_side(e));
+    x.s2 = e->side;
+  }
+  const mpipe_status st =
+      backward(x, patches, reinterpret_cast<const char*>(tape), d_merged, d_weights, d_patches);
+  // join on every path, so the caller's stream never runs ahead of gradient work
+  SideSync ss{x, x.s2 != x.s};
+  const hipError_t j = ss.join();
+  if (st != MPIPE_OK) return st;
+  MP_CHECK(j);
+  return MPIPE_OK;
 }
 
 static mpipe_status rows_common(int32_t row_elems, int32_t dtype, int64_t n_merged, int64_t n_rows,

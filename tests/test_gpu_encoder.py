@@ -153,6 +153,26 @@ def test_invariants_on_gpu():
                                   (base + host(t1["dw"]).astype(np.float32)))
 
 
+def test_side_stream_is_bitwise_neutral():
+    """The backward's weight-gradient work on the internal stream (default) gives the
+    same bits as running everything on the caller's stream, including accumulation
+    into a non-zero d_weights and the patch gradient."""
+    cfg, wl, dM = _small_problem("d64", seed=8)
+    w, X = wl.weights(), wl.patches()
+    rng = np.random.default_rng(5)
+    dw0 = rng.standard_normal(w.shape).astype(np.float32)
+    outs = []
+    for side in (True, False, True):
+        announce(f"side stream {'on' if side else 'off'}")
+        g = GpuRun(cfg, w, X, wl.cu_seqlens, wl.grid_thw)
+        g.enc.set_side_stream(side)
+        r = g.run(True, d_merged=dM, want_dx=True, dw_init=dw0)
+        outs.append((host(r["dw"]), host(r["dx"])))
+    for dw_, dx_ in outs[1:]:
+        assert np.array_equal(dw_, outs[0][0])
+        assert np.array_equal(dx_, outs[0][1])
+
+
 def test_relocation_owner_groups_on_gpu():
     """Encoding owner groups separately then scattering equals encoding at once."""
     import paper_2607_03229_amd as mp
