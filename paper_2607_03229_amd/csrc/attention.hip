@@ -15,7 +15,8 @@
 //   backward two deterministic kernels that recompute P from Q, K and the LSE:
 //            dK/dV per 128-key tile looping over query tiles, and dQ per
 //            128-query tile looping over key tiles.  No atomics.
-// head_dim 80 = 2 MFMA K-steps of 32 + one 16x16x16 step; output d-tiles of 16.
+// head_dim 80 = three 32-wide MFMA K-steps, the last zero-padded in the register
+// operand; output d-tiles of 16.
 // fp32 kernels (the small fp32 configuration): plain per-row loops.
 #include "common.h"
 #include "internal.h"
@@ -33,7 +34,8 @@ template <int D> struct AD {
   static constexpr int NC = D / 8;                          // 16-byte chunks per row
   static constexpr int PC = (NC % 2 == 0) ? NC + 1 : NC;    // odd pitch: conflict-free reads
   static constexpr int NF = D / 32;                         // full 32-wide K steps over d
-  static constexpr bool REM = (D % 32) != 0;                // one 16-wide remainder step
+  static constexpr bool REM = (D % 32) != 0;                // a last, partial 32-wide step
+  static constexpr int NS32 = (D + 31) / 32;                // 32-wide K steps, padded
   static constexpr int NDT = D / 16;                        // 16-wide output d tiles
 };
 
@@ -45,49 +47,38 @@ __device__ __forceinline__ bf16x8 frag_row(const uint4* rowt, int row, int f, in
   uint4 v = rowt[row * AD<D>::PC + 4 * f + g];
   return *reinterpret_cast<bf16x8*>(&v);
 }
-// 16x16x16 remainder fragment: d in [32 NF + 4g, +4)
-template <int D>
-__device__ __forceinline__ s16x4 frag_row_rem(const uint4* rowt, int row, int g) {
-  const uint2* p = reinterpret_cast<const uint2*>(rowt);
-  uint2 v = p[(row * AD<D>::PC + 4 * AD<D>::NF) * 2 + g];
-  return *reinterpret_cast<s16x4*>(&v);
-}
-// register fragments of one row (query/key) straight from global memory
+// Register fragments of one row (query/key) straight from global memory, as 32-wide K
+// steps over d.  For d = 80 the third step is padded: lane groups 0-1 hold d 64..79 and
+// groups 2-3 hold zeros, so the matching LDS operand may read any finite data there (its
+// tile's pad chunk and the next row's first chunk), and every product over d is one chain
+// of 16x16x32 MFMAs.
 template <int D> struct RowFrag {
-  bf16x8 f[AD<D>::NF > 0 ? AD<D>::NF : 1];
-  s16x4 rem;
+  bf16x8 f[AD<D>::NS32];
 };
 template <int D>
 __device__ __forceinline__ void load_rowfrag(RowFrag<D>& R, const bf16* X, int64_t ld, int row,
                                              int g) {
   const bf16* base = X + (int64_t)row * ld;
 #pragma unroll
-  for (int f = 0; f < AD<D>::NF; ++f) {
-    uint4 v = *reinterpret_cast<const uint4*>(base + 32 * f + 8 * g);
-    R.f[f] = *reinterpret_cast<bf16x8*>(&v);
-  }
-  if constexpr (AD<D>::REM) {
-    uint2 v = *reinterpret_cast<const uint2*>(base + 32 * AD<D>::NF + 4 * g);
-    R.rem = *reinterpret_cast<s16x4*>(&v);
+  for (int f = 0; f < AD<D>::NS32; ++f) {
+    const int col = 32 * f + 8 * g;
+    if (col < D) {
+      uint4 v = *reinterpret_cast<const uint4*>(base + col);
+      R.f[f] = *reinterpret_cast<bf16x8*>(&v);
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) R.f[f][e] = (bf16)0.f;
+    }
   }
 }
 
-// acc += A(row tile, rows arow..) x B(register fragment) over d.
-// The 16-wide remainder MFMA gets its own zero-initialised accumulator and is
-// added with a VALU add: an MFMA must never take the result of an MFMA of a
-// different shape as its accumulator input (the generated code then reads a
-// stale accumulator, because no wait states separate the two).
+// acc += A(row tile, rows arow..) x B(register fragment) over d
 template <int D>
 __device__ __forceinline__ f32x4 dot_d(const uint4* rowt, int arow, const RowFrag<D>& B, int g,
                                        f32x4 acc) {
 #pragma unroll
-  for (int f = 0; f < AD<D>::NF; ++f)
+  for (int f = 0; f < AD<D>::NS32; ++f)
     acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(frag_row<D>(rowt, arow, f, g), B.f[f], acc, 0, 0, 0);
-  if constexpr (AD<D>::REM) {
-    const f32x4 r = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(frag_row_rem<D>(rowt, arow, g), B.rem,
-                                                              f32x4{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
-    acc += r;
-  }
   return acc;
 }
 
@@ -269,8 +260,11 @@ __global__ __launch_bounds__(64 * (8 / NS), NS == 2 ? 2 : 1) void attn_fwd_kerne
           ps += e;
         }
       lsum[qs] = lsum[qs] * alpha + ps;
+      // the output rescale is skipped (uniformly) when no query's running max moved
+      if (__any(alpha != 1.0f)) {
 #pragma unroll
-      for (int dt = 0; dt < NDT; ++dt) o[qs][dt] *= alpha;
+        for (int dt = 0; dt < NDT; ++dt) o[qs][dt] *= alpha;
+      }
       pb[qs][0] = pack8(s[0][qs], s[1][qs]);
       pb[qs][1] = pack8(s[2][qs], s[3][qs]);
     }
@@ -476,15 +470,9 @@ __global__ __launch_bounds__(64 * (8 / NS), NS == 2 ? 2 : 1) void attn_bwd_dq_ke
     load_rowfrag<D>(of, O, p.ldo, qc, g);
     float dl = 0.f;
 #pragma unroll
-    for (int f = 0; f < AD<D>::NF; ++f)
+    for (int f = 0; f < AD<D>::NS32; ++f)   // (padded lanes hold zeros)
 #pragma unroll
       for (int e = 0; e < 8; ++e) dl += (float)of.f[f][e] * (float)dof[qs].f[f][e];
-    if constexpr (AD<D>::REM) {
-      const bf16* ro = reinterpret_cast<const bf16*>(&of.rem);
-      const bf16* rd = reinterpret_cast<const bf16*>(&dof[qs].rem);
-#pragma unroll
-      for (int e = 0; e < 4; ++e) dl += (float)ro[e] * (float)rd[e];
-    }
     dl += __shfl_xor(dl, 16);
     dl += __shfl_xor(dl, 32);
     del[qs] = dl;
