@@ -119,11 +119,38 @@ __device__ __forceinline__ void dma_tile(uint4* tile, const bf16* X, int64_t ld,
     const int slot = inst * 64 + lane;
     int row = slot / PC, ch = slot % PC;
     ch = ch < NC ? ch : 0;
+    row = row < 64 ? row : 63;   // slots past the 64 rows repeat the last row
     int grow = r0 + row;
     grow = grow < rlast ? grow : rlast;
     __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(X + (int64_t)grow * ld + 8 * ch),
                                      (lds_void*)(tile + inst * 64), 16, 0, 0);
   }
+}
+// The same DMA for a full tile (r0 + 63 <= rlast), from per-lane source offsets computed
+// once per kernel: one 64-bit add per instruction instead of the clamp and multiply.
+template <int D, int NW> struct TileSrc {
+  int64_t off[TG<D, NW>::NI];
+};
+template <int D, int NW>
+__device__ __forceinline__ void tile_src_init(TileSrc<D, NW>& S, int64_t ld) {
+  constexpr int PC = AD<D>::PC, NC = AD<D>::NC;
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+#pragma unroll
+  for (int i = 0; i < TG<D, NW>::NI; ++i) {
+    const int slot = (i * NW + w) * 64 + lane;
+    int row = slot / PC, ch = slot % PC;
+    ch = ch < NC ? ch : 0;
+    row = row < 64 ? row : 63;
+    S.off[i] = (int64_t)row * ld + 8 * ch;
+  }
+}
+template <int D, int NW>
+__device__ __forceinline__ void dma_tile_full(uint4* tile, const bf16* Xr0, const TileSrc<D, NW>& S) {
+  const int w = threadIdx.x >> 6;
+#pragma unroll
+  for (int i = 0; i < TG<D, NW>::NI; ++i)
+    __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(Xr0 + S.off[i]),
+                                     (lds_void*)(tile + (i * NW + w) * 64), 16, 0, 0);
 }
 // 64 floats (one per query of a tile, rows clamped) by a 4-byte DMA from wave 0
 __device__ __forceinline__ void dma_vec64(float* dst, const float* src, int r0, int rlast) {
@@ -207,10 +234,18 @@ __global__ __launch_bounds__(64 * (8 / NS), NS == 2 ? 2 : 1) void attn_fwd_kerne
     lsum[qs] = 0.f;
   }
 
+  TileSrc<D, NW> kvsrc;
+  tile_src_init<D, NW>(kvsrc, p.ld);
   auto issue = [&](int t, uint4* kt, uint4* vt) __attribute__((always_inline)) {
     if (t < nt) {
-      dma_tile<D, NW>(kt, K, p.ld, s0 + 64 * t, s1 - 1);
-      dma_tile<D, NW>(vt, V, p.ld, s0 + 64 * t, s1 - 1);
+      const int r0 = s0 + 64 * t;
+      if (r0 + 63 <= s1 - 1) {
+        dma_tile_full<D, NW>(kt, K + (int64_t)r0 * p.ld, kvsrc);
+        dma_tile_full<D, NW>(vt, V + (int64_t)r0 * p.ld, kvsrc);
+      } else {
+        dma_tile<D, NW>(kt, K, p.ld, r0, s1 - 1);
+        dma_tile<D, NW>(vt, V, p.ld, r0, s1 - 1);
+      }
     }
   };
   auto body = [&](int t, const uint4* kt_s, const uint4* vt_s, uint4* kn, uint4* vn)
@@ -343,13 +378,16 @@ __global__ __launch_bounds__(64 * (8 / NS), NS == 2 ? 2 : 1) void attn_bwd_dkdv_
 #pragma unroll
     for (int dt = 0; dt < NDT; ++dt) dk[ks][dt] = dv[ks][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
+  // (per-tile source arithmetic here: keeping precomputed offsets live measured slower,
+  // the extra registers spill in this kernel)
   auto issue = [&](int t, uint4* qt, uint4* dt_, float* lt, float* et)
       __attribute__((always_inline)) {
     if (t < nt) {
-      dma_tile<D, NW>(qt, Q, p.ld, s0 + 64 * t, s1 - 1);
-      dma_tile<D, NW>(dt_, dO, p.ldo, s0 + 64 * t, s1 - 1);
-      dma_vec64(lt, LSE, s0 + 64 * t, s1 - 1);
-      dma_vec64(et, DEL, s0 + 64 * t, s1 - 1);
+      const int r0 = s0 + 64 * t;
+      dma_tile<D, NW>(qt, Q, p.ld, r0, s1 - 1);
+      dma_tile<D, NW>(dt_, dO, p.ldo, r0, s1 - 1);
+      dma_vec64(lt, LSE, r0, s1 - 1);
+      dma_vec64(et, DEL, r0, s1 - 1);
     }
   };
   auto body = [&](int t, const uint4* q_s, const uint4* do_s, const float* lse_s,
@@ -484,10 +522,18 @@ __global__ __launch_bounds__(64 * (8 / NS), NS == 2 ? 2 : 1) void attn_bwd_dq_ke
 #pragma unroll
     for (int dt = 0; dt < NDT; ++dt) dq[qs][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
+  TileSrc<D, NW> kvsrc;
+  tile_src_init<D, NW>(kvsrc, p.ld);
   auto issue = [&](int t, uint4* kt, uint4* vt) __attribute__((always_inline)) {
     if (t < nt) {
-      dma_tile<D, NW>(kt, K, p.ld, s0 + 64 * t, s1 - 1);
-      dma_tile<D, NW>(vt, V, p.ld, s0 + 64 * t, s1 - 1);
+      const int r0 = s0 + 64 * t;
+      if (r0 + 63 <= s1 - 1) {
+        dma_tile_full<D, NW>(kt, K + (int64_t)r0 * p.ld, kvsrc);
+        dma_tile_full<D, NW>(vt, V + (int64_t)r0 * p.ld, kvsrc);
+      } else {
+        dma_tile<D, NW>(kt, K, p.ld, r0, s1 - 1);
+        dma_tile<D, NW>(vt, V, p.ld, r0, s1 - 1);
+      }
     }
   };
   auto body = [&](int t, const uint4* k_s, const uint4* v_s, uint4* kn, uint4* vn)
