@@ -45,6 +45,21 @@ def model_flops(cfg, n_patches: int, sum_len2: int, trainable: bool) -> float:
     return float(3 * F - 2 * N * kpe * h) if trainable else float(F)
 
 
+def hardware_flops(cfg, n_patches: int, sum_len2: int, trainable: bool) -> float:
+    """MFMA work the kernels actually issue: the model FLOPs plus the attention backward's
+    recompute (the dQ kernel recomputes S and dP, the dK/dV kernel S: 6 h d sum L^2 per
+    layer) and the head-dim padding of the products over d (d rounded up to 32 for S and
+    dP: one in the forward, four in the backward).  Ragged GEMM tile edges are not counted."""
+    h, d, L = cfg.hidden, cfg.hidden // cfg.heads, cfg.layers
+    dpad = (d + 31) // 32 * 32
+    extra = 2.0 * h * sum_len2 * (dpad - d) / d      # one S-type product, padding only
+    per_layer = extra
+    if trainable:
+        per_layer += 6.0 * h * sum_len2 + 4 * (2.0 * h * sum_len2 * dpad / d)
+        per_layer -= 4 * (2.0 * h * sum_len2)        # those four products' unpadded share
+    return model_flops(cfg, n_patches, sum_len2, trainable) + L * per_layer
+
+
 # ---- HBM traffic of the dominant kernel (rocprofv3 PMC counters) ---------------------
 # FETCH_SIZE / WRITE_SIZE are read in two separate `rocprofv3 --pmc` runs of this script
 # (one counter per run), each scaled by what the same counter reads for a plain copy of
@@ -273,12 +288,18 @@ def main():
     profile = not args.no_profile
     if profile:
         enc.profile(True)
+    # per-step HIP events on the stream (median / min); the whole-job figure is the host
+    # clock over all K steps, bracketed by device synchronisation
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
+    evs[0].record(stream)
     for i in range(args.steps):
         step()
+        evs[i + 1].record(stream)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
+    per_step = sorted(evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps))
     log(f"timed {args.steps} steps: {elapsed * 1e3 / args.steps:.1f} ms/step")
     kern = enc.profile_read(stream) if profile else {}
     enc.profile(False)
@@ -298,6 +319,7 @@ def main():
 
     sum_len2 = int(np.sum(np.diff(wl.cu_seqlens).astype(np.int64) ** 2))
     flops = model_flops(cfg, wl.n_patches, sum_len2, trainable)
+    hw_flops = hardware_flops(cfg, wl.n_patches, sum_len2, trainable)
     ms_step = elapsed * 1e3 / args.steps
     achieved = flops / (ms_step * 1e-3) / 1e12
     peak = PEAK_BF16_TFLOPS if cfg.dtype == "bf16" else PEAK_F32_TFLOPS
@@ -324,6 +346,8 @@ def main():
         "unit": "patch-tokens/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": round(ms_step, 3),
+        "ms_per_step_median": round(per_step[len(per_step) // 2], 3),
+        "ms_per_step_min": round(per_step[0], 3),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": cfg.dtype, "data": "synthetic",
         "config": {"workload": wl.name, "seed": args.seed, "mode": "trained" if trainable else "frozen",
@@ -335,6 +359,8 @@ def main():
         "model_tflop_per_step": round(flops / 1e12, 3),
         "achieved_tflops": round(achieved, 1),
         "mfma_pct_of_peak": round(100 * achieved / peak, 2),
+        "hw_tflop_per_step": round(hw_flops / 1e12, 3),
+        "hw_mfma_pct_of_peak": round(100 * hw_flops / (ms_step * 1e-3) / 1e12 / peak, 2),
         "peak_tflops": peak,
         "scatter_GBps": round(scatter_gbps, 1),
         "scatter_pct_of_hbm": round(100 * scatter_gbps / PEAK_HBM_GBPS, 1),
