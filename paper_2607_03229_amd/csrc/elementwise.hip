@@ -354,6 +354,61 @@ __global__ void pad_cols_kernel(const T* src, int64_t rows, int K, T* dst, int K
   dst[i] = c < K ? src[r * K + c] : from_f<T>(0.f);
 }
 
+// ---- batched transpose: dst[c][r] = src[r][c], element bits copied ------------------
+// 64x64 tiles through LDS; block b takes tile b - first_tile of the job it falls in.
+// VEC elements per 16-byte access when every job allows it (VEC = 1: scalar accesses).
+struct TJobs {
+  TJob j[kMaxTJobs];
+  int64_t first[kMaxTJobs + 1];   // first tile of each job; first[n] = total tiles
+  int n;
+};
+
+template <class U, int VEC>
+__global__ __launch_bounds__(256) void transpose_kernel(TJobs jb) {
+  __shared__ U tile[64][65];
+  const int64_t b = blockIdx.x;
+  int ji = 0;
+  while (ji + 1 < jb.n && b >= jb.first[ji + 1]) ++ji;
+  const TJob& J = jb.j[ji];
+  const int64_t tix = b - jb.first[ji];
+  const int tiles_c = (J.cols + 63) / 64;
+  const int r0 = (int)(tix / tiles_c) * 64, c0 = (int)(tix % tiles_c) * 64;
+  const U* src = reinterpret_cast<const U*>(J.src);
+  U* dst = reinterpret_cast<U*>(J.dst);
+  constexpr int TPR = 64 / VEC;          // threads per 64-element line
+  constexpr int LPP = 256 / TPR;         // lines per pass
+  const int t = threadIdx.x;
+  const int li = t / TPR, ci = (t % TPR) * VEC;
+  for (int rr = li; rr < 64; rr += LPP) {       // load src rows r0+rr, cols c0+ci..
+    const int r = r0 + rr, c = c0 + ci;
+    if constexpr (VEC > 1) {
+      if (r < J.rows && c < J.cols) {
+        const uint4 v = *reinterpret_cast<const uint4*>(src + (int64_t)r * J.lds + c);
+        const U* e = reinterpret_cast<const U*>(&v);
+#pragma unroll
+        for (int k = 0; k < VEC; ++k) tile[rr][ci + k] = e[k];
+      }
+    } else {
+      if (r < J.rows && c < J.cols) tile[rr][ci] = src[(int64_t)r * J.lds + c];
+    }
+  }
+  __syncthreads();
+  for (int cc = li; cc < 64; cc += LPP) {       // store dst rows c0+cc, cols r0+ci..
+    const int c = c0 + cc, r = r0 + ci;
+    if constexpr (VEC > 1) {
+      if (c < J.cols && r < J.rows) {
+        uint4 v;
+        U* e = reinterpret_cast<U*>(&v);
+#pragma unroll
+        for (int k = 0; k < VEC; ++k) e[k] = tile[ci + k][cc];
+        *reinterpret_cast<uint4*>(dst + (int64_t)c * J.ldd + r) = v;
+      }
+    } else {
+      if (c < J.cols && r < J.rows) dst[(int64_t)c * J.ldd + r] = tile[ci][cc];
+    }
+  }
+}
+
 // ---- 2D rotary position, in place on the q and k column blocks -------------------
 // pos[r] = y << 16 | x.  tab[p * q4 + k] = (cos, sin) of p * theta^(-4k/d) (k < q4 = d/4,
 // computed on the host in double).  Pair (j, j + d/2) of each head rotates by the
@@ -614,6 +669,38 @@ hipError_t pad_cols(int dtype, const void* src, int64_t rows, int K, void* dst, 
   else
     hipLaunchKernelGGL(pad_cols_kernel<float>, dim3(blocks_for(n)), dim3(256), 0, s,
                        (const float*)src, rows, K, (float*)dst, Kp);
+  return hipGetLastError();
+}
+
+hipError_t transpose_batch(int dtype, const TJob* jobs, int n, hipStream_t s) {
+  if (n < 0 || n > kMaxTJobs) return hipErrorInvalidValue;
+  TJobs jb{};
+  jb.n = 0;
+  int64_t tiles = 0;
+  const int esz = dtype == DT_BF16 ? 2 : 4;
+  const int vec = 16 / esz;
+  bool vok = true;
+  for (int i = 0; i < n; ++i) {
+    const TJob& J = jobs[i];
+    if (J.rows <= 0 || J.cols <= 0) continue;
+    if (J.lds < J.cols || J.ldd < J.rows) return hipErrorInvalidValue;
+    jb.j[jb.n] = J;
+    jb.first[jb.n] = tiles;
+    tiles += (int64_t)((J.rows + 63) / 64) * ((J.cols + 63) / 64);
+    ++jb.n;
+    vok = vok && J.rows % vec == 0 && J.cols % vec == 0 && J.lds % vec == 0 && J.ldd % vec == 0 &&
+          (reinterpret_cast<uintptr_t>(J.src) & 15) == 0 && (reinterpret_cast<uintptr_t>(J.dst) & 15) == 0;
+  }
+  jb.first[jb.n] = tiles;
+  if (tiles == 0) return hipSuccess;
+  const dim3 grid((unsigned)tiles);
+  if (dtype == DT_BF16) {
+    if (vok) hipLaunchKernelGGL((transpose_kernel<uint16_t, 8>), grid, dim3(256), 0, s, jb);
+    else hipLaunchKernelGGL((transpose_kernel<uint16_t, 1>), grid, dim3(256), 0, s, jb);
+  } else {
+    if (vok) hipLaunchKernelGGL((transpose_kernel<uint32_t, 4>), grid, dim3(256), 0, s, jb);
+    else hipLaunchKernelGGL((transpose_kernel<uint32_t, 1>), grid, dim3(256), 0, s, jb);
+  }
   return hipGetLastError();
 }
 

@@ -309,6 +309,27 @@ mpipe_status pad_pe(Ctx& x, const void* patches) {
   return MPIPE_OK;
 }
 
+// Transposed copies of the [out][in] weights the next GEMMs multiply by, back to back in
+// the workspace: wt[i] = W_i^T ([in][out], row stride out), so that every forward GEMM
+// reads its weight operand K-major (whole 128-byte lines per DMA row).
+mpipe_status weights_t(Ctx& x, int n, const void* const* W, const int64_t* out_f,
+                       const int64_t* in_f, const int64_t* ld, const void** wt) {
+  TJob jobs[kMaxTJobs];
+  char* dst = x.ws + x.P.ws_wt;
+  for (int i = 0; i < n; ++i) {
+    jobs[i].src = W[i];
+    jobs[i].lds = ld[i];
+    jobs[i].dst = dst;
+    jobs[i].ldd = out_f[i];
+    jobs[i].rows = (int)out_f[i];
+    jobs[i].cols = (int)in_f[i];
+    wt[i] = dst;
+    dst += out_f[i] * in_f[i] * x.E;
+  }
+  MP_CHECK(run(x.e, x.s, "transpose", 0, [&] { return transpose_batch(x.dt, jobs, n, x.s); }));
+  return MPIPE_OK;
+}
+
 #define MP_RET(expr)                  \
   do {                                \
     mpipe_status _s = (expr);         \
@@ -332,9 +353,12 @@ mpipe_status forward(Ctx& x, const void* patches, void* merged, char* tape) {
   pe_operands(x, patches, Xp, Wpe, ldx);
   const size_t h0 = c.layers > 0 ? act(0).hin : MS.hfin;
   {
-    GemmArgs a = ga(Xp, ldx, Wpe, ldx, N, h, c.kp, base + h0, h);
+    const void* wt[1];
+    const int64_t of[1] = {h}, inf[1] = {c.kp}, ld[1] = {ldx};
+    MP_RET(weights_t(x, 1, &Wpe, of, inf, ld, wt));
+    GemmArgs a = ga(Xp, ldx, wt[0], h, N, h, c.kp, base + h0, h);
     a.bias = x.W(P_PE_B);
-    MP_RET(gemm_call(x, GEMM_NT, EPI_RESID, a));
+    MP_RET(gemm_call(x, GEMM_NN, EPI_RESID, a));
   }
   for (int l = 0; l < c.layers; ++l) {
     const ActSet& S = act(l);
@@ -346,6 +370,14 @@ mpipe_status forward(Ctx& x, const void* patches, void* merged, char* tape) {
     char* O = base + S.o;
     char* B = base + S.b;
     char* G = base + S.g;
+    // W^T of qkv, proj, fc1, fc2
+    const void* wt[4];
+    {
+      const void* W[4] = {x.W(blk_param(c, l, B_QKVW)), x.W(blk_param(c, l, B_PROJW)),
+                          x.W(blk_param(c, l, B_FC1W)), x.W(blk_param(c, l, B_FC2W))};
+      const int64_t of[4] = {3 * h, h, m, h}, inf[4] = {h, h, h, m};
+      MP_RET(weights_t(x, 4, W, of, inf, inf, wt));
+    }
     MP_CHECK(run(x.e, x.s, "layernorm", 0, [&] {
       return layernorm_fwd(x.dt, hin, h, N, (int)h, x.W(blk_param(c, l, B_LN1G)),
                            x.W(blk_param(c, l, B_LN1B)), c.eps, A, h,
@@ -353,9 +385,9 @@ mpipe_status forward(Ctx& x, const void* patches, void* merged, char* tape) {
                            reinterpret_cast<float*>(base + S.rstd1), x.s);
     }));
     {
-      GemmArgs a = ga(A, h, x.W(blk_param(c, l, B_QKVW)), h, N, 3 * h, h, qkv, 3 * h);
+      GemmArgs a = ga(A, h, wt[0], 3 * h, N, 3 * h, h, qkv, 3 * h);
       a.bias = x.W(blk_param(c, l, B_QKVB));
-      MP_RET(gemm_call(x, GEMM_NT, EPI_STORE, a));
+      MP_RET(gemm_call(x, GEMM_NN, EPI_STORE, a));
     }
     MP_CHECK(run(x.e, x.s, "rope", 0, [&] {
       return rope(x.dt, qkv, 3 * h, N, c.heads, c.d, (int)h, pos, freq, 0, x.s);
@@ -369,11 +401,11 @@ mpipe_status forward(Ctx& x, const void* patches, void* merged, char* tape) {
       MP_CHECK(run(x.e, x.s, "attn_fwd", fl, [&] { return attention_fwd(x.dt, c.d, a, x.s); }));
     }
     {
-      GemmArgs a = ga(O, h, x.W(blk_param(c, l, B_PROJW)), h, N, h, h, hmid, h);
+      GemmArgs a = ga(O, h, wt[1], h, N, h, h, hmid, h);
       a.bias = x.W(blk_param(c, l, B_PROJB));
       a.aux = hin;
       a.ld_aux = h;
-      MP_RET(gemm_call(x, GEMM_NT, EPI_RESID, a));
+      MP_RET(gemm_call(x, GEMM_NN, EPI_RESID, a));
     }
     MP_CHECK(run(x.e, x.s, "layernorm", 0, [&] {
       return layernorm_fwd(x.dt, hmid, h, N, (int)h, x.W(blk_param(c, l, B_LN2G)),
@@ -382,23 +414,29 @@ mpipe_status forward(Ctx& x, const void* patches, void* merged, char* tape) {
                            reinterpret_cast<float*>(base + S.rstd2), x.s);
     }));
     {
-      GemmArgs a = ga(B, h, x.W(blk_param(c, l, B_FC1W)), h, N, m, h, G, m);
+      GemmArgs a = ga(B, h, wt[2], m, N, m, h, G, m);
       a.bias = x.W(blk_param(c, l, B_FC1B));
       a.C2 = tr ? base + S.u : nullptr;
       a.ldc2 = m;
-      MP_RET(gemm_call(x, GEMM_NT, EPI_GELU, a));
+      MP_RET(gemm_call(x, GEMM_NN, EPI_GELU, a));
     }
     {
-      GemmArgs a = ga(G, m, x.W(blk_param(c, l, B_FC2W)), m, N, h, m, hout, h);
+      GemmArgs a = ga(G, m, wt[3], h, N, h, m, hout, h);
       a.bias = x.W(blk_param(c, l, B_FC2B));
       a.aux = hmid;
       a.ld_aux = h;
-      MP_RET(gemm_call(x, GEMM_NT, EPI_RESID, a));
+      MP_RET(gemm_call(x, GEMM_NN, EPI_RESID, a));
     }
   }
   // 2x2 merger: LN, the four window rows side by side ([Tm][4h] view), fc1+GELU, fc2
   char* Z = base + MS.z;
   char* Gm = base + MS.gm;
+  const void* wtm[2];
+  {
+    const void* W[2] = {x.W(merger_param(c, M_FC1W)), x.W(merger_param(c, M_FC2W))};
+    const int64_t of[2] = {4 * h, H}, inf[2] = {4 * h, 4 * h};
+    MP_RET(weights_t(x, 2, W, of, inf, inf, wtm));
+  }
   MP_CHECK(run(x.e, x.s, "layernorm", 0, [&] {
     return layernorm_fwd(x.dt, reinterpret_cast<float*>(base + MS.hfin), h, N, (int)h,
                          x.W(merger_param(c, M_LNG)), x.W(merger_param(c, M_LNB)), c.eps, Z, h,
@@ -406,16 +444,16 @@ mpipe_status forward(Ctx& x, const void* patches, void* merged, char* tape) {
                          reinterpret_cast<float*>(base + MS.rstdz), x.s);
   }));
   {
-    GemmArgs a = ga(Z, 4 * h, x.W(merger_param(c, M_FC1W)), 4 * h, P.Tm, 4 * h, 4 * h, Gm, 4 * h);
+    GemmArgs a = ga(Z, 4 * h, wtm[0], 4 * h, P.Tm, 4 * h, 4 * h, Gm, 4 * h);
     a.bias = x.W(merger_param(c, M_FC1B));
     a.C2 = tr ? base + MS.um : nullptr;
     a.ldc2 = 4 * h;
-    MP_RET(gemm_call(x, GEMM_NT, EPI_GELU, a));
+    MP_RET(gemm_call(x, GEMM_NN, EPI_GELU, a));
   }
   {
-    GemmArgs a = ga(Gm, 4 * h, x.W(merger_param(c, M_FC2W)), 4 * h, P.Tm, H, 4 * h, merged, H);
+    GemmArgs a = ga(Gm, 4 * h, wtm[1], H, P.Tm, H, 4 * h, merged, H);
     a.bias = x.W(merger_param(c, M_FC2B));
-    MP_RET(gemm_call(x, GEMM_NT, EPI_STORE, a));
+    MP_RET(gemm_call(x, GEMM_NN, EPI_STORE, a));
   }
   (void)E;
   return MPIPE_OK;

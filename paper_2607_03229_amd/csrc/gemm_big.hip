@@ -1,37 +1,42 @@
-// Large-tile bf16 GEMM for gfx950: the encoder's Linear layers at full size.
+// Large-tile bf16 GEMMs for gfx950: the encoder's Linear layers at full size.
 //
 // C[M,N] = sum_k A(m,k) B(n,k) with the same operand layouts and epilogues as the
 // general kernel (NT forward, NN input gradient, TN weight gradient).
 //
-// Block tile 256x256, 256 threads = 4 wave64 in a 2x2 grid; each wave owns a
-// 128x128 tile of 4x4 v_mfma_f32_32x32x16_bf16 accumulators (256 AGPRs).  A
-// 128x128 wave tile keeps the LDS traffic (fragment reads + tile fills) under what
-// the LDS delivers at the full MFMA rate; smaller wave tiles would not.
+// Two block shapes share one kernel template, both 256 threads = 4 wave64 in a 2x2 grid
+// of v_mfma_f32_32x32x16_bf16 accumulators and the same K order, so a given output
+// element gets bitwise the same value from either:
+//   MT = 4: block tile 256x256, each wave 128x128 (4x4 accumulators, 256 AGPRs), a
+//           4-stage ring (128 KB of LDS), one block per CU.  A 128x128 wave tile keeps
+//           the LDS traffic (fragment reads + tile fills) well under what the LDS
+//           delivers at the full MFMA rate.
+//   MT = 2: block tile 128x256, each wave 64x128 (2x4 accumulators), a 3-stage ring
+//           (72 KB), two blocks per CU.  Twice the tile count rounds the last wave of
+//           tiles more finely, and one block's epilogue overlaps the other's main loop.
 //
-// Operand tiles (256 rows x 32 k, 16 KB each) are filled by 16-byte global->LDS DMA
-// (global_load_lds) in a 4-stage ring, so tiles t+1..t+3 are in flight while tile t
-// is multiplied and no tile data passes through VGPRs.  Each lane of a DMA
-// instruction owns one fixed LDS slot and picks the source element of that slot,
-// which is how the tiles get their bank-conflict-free XOR swizzles:
+// Operand tiles (rows x 32 k) are filled by 16-byte global->LDS DMA (global_load_lds)
+// in the ring, so the next tiles are in flight while tile t is multiplied and no tile
+// data passes through VGPRs.  Each lane of a DMA instruction owns one fixed LDS slot and
+// picks the source element of that slot, which is how the tiles get their
+// bank-conflict-free XOR swizzles:
 //   K-contiguous operand ([rows][k]): 64-byte rows, chunk c of row r at c ^ fkc(r);
 //      fragment reads are 16-byte ds_read_b128.
-//   K-major operand ([k][cols]):      512-byte k-rows, chunk c of k-row k at c ^ gkm(k);
-//      fragments come straight from the raw tile through ds_read_b64_tr_b16, so no
-//      operand is ever transposed in registers.
+//   K-major operand ([k][cols], 256 cols): 512-byte k-rows, chunk c of k-row k at
+//      c ^ gkm(k); fragments come straight from the raw tile through
+//      ds_read_b64_tr_b16, so no operand is ever transposed in registers.
 // Both swizzles keep every fragment read conflict-free whether the LDS serves 128
 // or 256 bytes per cycle.
 //
-// Pipeline per K tile t (stage t % 4): the fragments of its first 16-wide K half are
-// already in registers; the second half's fragments are read while the first half's
-// 16 MFMAs run; then one barrier (tile t+1 landed for every wave, stage t%4 no longer
-// read), the DMA of tile t+4 into stage t%4, and tile t+1's first fragments are read
-// while the second half's MFMAs run.  One barrier per 1024 MFMA cycles per wave.
-// Ragged M/N edges read clamped (valid) rows; a ragged K tail reads clamped rows and
-// zeroes the A fragments past the end.  The epilogue stages each wave's accumulators
-// through LDS, 16 rows at a time, so all epilogue global accesses are 16-byte vectors
-// (the dispatcher sends ragged-N or misaligned problems to the general kernel); the
-// operands it reads (GELU' factor, residual, accumulate target) are fetched one staging
-// pass ahead.
+// Pipeline per K tile t: the fragments of its first 16-wide K half are already in
+// registers; the second half's fragments are read while the first half's MFMAs run;
+// then one barrier (tile t+1 landed for every wave, stage t no longer read), the DMA
+// of tile t+NST into stage t, and tile t+1's first fragments are read while the second
+// half's MFMAs run.  Ragged M/N edges read clamped (valid) rows; a ragged K tail reads
+// clamped rows and zeroes the A fragments past the end.  The epilogue stages each
+// wave's accumulators through its own LDS region, 16 rows at a time, so all epilogue
+// global accesses are 16-byte vectors (the dispatcher sends ragged-N or misaligned
+// problems to the general kernel); the operands it reads (GELU' factor, residual,
+// accumulate target) are fetched one staging pass ahead.
 #include <type_traits>
 
 #include "common.h"
@@ -43,8 +48,8 @@
 namespace mpipe {
 namespace {
 
-constexpr int BM = 256, BN = 256, BK = 32, NTHR = 256, GROUP_M = 8;
-constexpr int TILE_U4 = BM * BK * 2 / 16;   // 16-byte slots per operand tile (1024)
+constexpr int BN = 256, BK = 32, NTHR = 256, GROUP_M = 8;
+constexpr int B_U4 = BN * BK * 2 / 16;      // 16-byte slots of a B operand tile (1024)
 constexpr int SP = 136;                     // epilogue staging pitch in floats
 
 typedef __attribute__((ext_vector_type(16))) float f32x16;
@@ -70,20 +75,24 @@ __device__ __forceinline__ void wait_vm() {
 __device__ __forceinline__ void lds_barrier() {
   asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
+// Orders this wave's LDS writes before its later LDS reads (a wave's LDS operations
+// execute in issue order; the clobber keeps the compiler from moving accesses across).
+__device__ __forceinline__ void lds_wave_fence() {
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+}
 __device__ __forceinline__ uint32_t lds_addr(const void* p) {
   return (uint32_t)(size_t)(lds_void*)p;
 }
 
 // ---- DMA sources ---------------------------------------------------------------------
-// Wave w issues instructions q = 4w + i (i < 4) of each operand tile; instruction q
-// fills LDS slots 64q..64q+63, lane l slot 64q + l.
+// DMA instruction q of an operand tile fills LDS slots 64q..64q+63, lane l slot 64q + l;
+// wave w issues instructions q = n*w .. n*w + n-1 of a tile that takes 4n instructions.
 
 // K-contiguous operand X[rows][ld], tile rows r0.., k from k0: slot (row 16q + l/4,
 // physical chunk l%4) holds logical chunk (l%4) ^ fkc(row).
 __device__ __forceinline__ const bf16* src_kc(const bf16* X, int64_t ld, int rows, int r0, int k0,
-                                              int kend, int i) {
-  const int w = threadIdx.x >> 6, l = threadIdx.x & 63;
-  const int q = 4 * w + i;
+                                              int kend, int q) {
+  const int l = threadIdx.x & 63;
   const int row = 16 * q + (l >> 2);
   int k = k0 + 8 * ((l & 3) ^ fkc(row));
   k = k < kend ? k : kend - 8;
@@ -91,12 +100,11 @@ __device__ __forceinline__ const bf16* src_kc(const bf16* X, int64_t ld, int row
   gr = gr < rows ? gr : rows - 1;
   return X + (int64_t)gr * ld + k;
 }
-// K-major operand X[k][ld], tile cols c0.., k-rows from k0: slot (k-row 2q + l/32,
+// K-major operand X[k][ld], 256-col tile from c0, k-rows from k0: slot (k-row 2q + l/32,
 // physical chunk l%32) holds logical chunk (l%32) ^ gkm(k-row).
 __device__ __forceinline__ const bf16* src_km(const bf16* X, int64_t ld, int cols, int c0, int k0,
-                                              int kend, int i) {
-  const int w = threadIdx.x >> 6, l = threadIdx.x & 63;
-  const int q = 4 * w + i;
+                                              int kend, int q) {
+  const int l = threadIdx.x & 63;
   const int kr = 2 * q + (l >> 5);
   int col = c0 + 8 * ((l & 31) ^ gkm(kr));
   col = col < cols ? col : cols - 8;
@@ -104,11 +112,11 @@ __device__ __forceinline__ const bf16* src_km(const bf16* X, int64_t ld, int col
   k = k < kend ? k : kend - 1;
   return X + (int64_t)k * ld + col;
 }
-// 16-byte global->LDS DMA of instruction q = 4w + i: lane l writes LDS byte
-// tile + 1024 q + 16 l (M0 holds the wave-uniform base).
+// 16-byte global->LDS DMA of instruction q: lane l writes LDS byte tile + 1024 q + 16 l
+// (M0 holds the wave-uniform base).
 // M0 is declared clobbered; nothing else in these kernels keeps a value in it.
-__device__ __forceinline__ void dma16(const bf16* src, const uint4* tile, int i) {
-  const uint32_t base = lds_addr(tile) + 1024u * (4 * (threadIdx.x >> 6) + i);
+__device__ __forceinline__ void dma16(const bf16* src, const uint4* tile, int q) {
+  const uint32_t base = lds_addr(tile) + 1024u * q;
   asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
                ::"v"(src), "s"(__builtin_amdgcn_readfirstlane(base)) : "memory", "m0");
 }
@@ -190,12 +198,28 @@ __device__ __forceinline__ void epi8_vec(const GemmArgs& p, int split, int m, in
 
 // ---- the kernel ----------------------------------------------------------------------
 
-template <bool AK, bool BKM, int EPI>
-__global__ __launch_bounds__(NTHR, 1) void gemm_big_kernel(GemmArgs p) {
-  // one LDS object per stage and operand, so the compiler can tell a fragment read
-  // of one stage from the DMAs still writing another
-  __shared__ uint4 sa0[TILE_U4], sa1[TILE_U4], sa2[TILE_U4], sa3[TILE_U4];
-  __shared__ uint4 sb0[TILE_U4], sb1[TILE_U4], sb2[TILE_U4], sb3[TILE_U4];
+// Block-shape constants of the MT-tiles-per-wave variant.
+template <int MT>
+struct Shape {
+  static_assert(MT == 2 || MT == 4, "block shapes: 128x256 or 256x256");
+  static constexpr int BM = 64 * MT;                 // block rows
+  static constexpr int NST = MT == 4 ? 4 : 3;        // ring stages
+  static constexpr int A_U4 = BM * BK * 2 / 16;      // 16-byte slots of an A tile
+  static constexpr int IA = MT;                      // A-tile DMA instructions per wave
+  static constexpr int IPT = IA + 4;                 // DMA instructions per wave per K tile
+  static constexpr int LDS_U4 = NST * (A_U4 + B_U4);
+  static constexpr int OCC = MT == 4 ? 1 : 2;        // resident blocks per CU
+};
+
+template <int MT, bool AK, bool BKM, int EPI>
+__global__ __launch_bounds__(NTHR, Shape<MT>::OCC) void gemm_big_kernel(GemmArgs p) {
+  using SH = Shape<MT>;
+  constexpr int BM = SH::BM, NST = SH::NST, A_U4 = SH::A_U4, IA = SH::IA, IPT = SH::IPT;
+  static_assert(!AK || MT == 4, "a K-major A operand needs 256-row tiles");
+  // the ring: stage s of A at smem + s*A_U4, of B at smem + NST*A_U4 + s*B_U4.  The DMAs
+  // are assembly with a memory clobber, so no fragment read moves across one.
+  __shared__ uint4 smem[SH::LDS_U4];
+  static_assert(4 * 16 * SP * 4 <= SH::LDS_U4 * 16, "epilogue staging must fit in the ring");
 
   // XCD-aware block order (consecutive block ids go round-robin to the 8 XCDs), then
   // groups of GROUP_M tile-rows for L2 reuse
@@ -219,42 +243,48 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_big_kernel(GemmArgs p) {
   const int w = threadIdx.x >> 6, l = threadIdx.x & 63;
   const int wm = w >> 1, wn = w & 1;
 
-  f32x16 acc[4][4];
+  f32x16 acc[MT][4];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < MT; ++i)
 #pragma unroll
     for (int j = 0; j < 4; ++j)
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
 
+  auto stage_a = [&](int s) { return smem + s * A_U4; };
+  auto stage_b = [&](int s) { return smem + NST * A_U4 + s * B_U4; };
+
   // per-lane DMA sources of the first K tile; a full tile t adds t*BK (K-contiguous)
   // or t*BK*ld (K-major) elements
-  const bf16* sA[4];
+  auto srcA = [&](int k0, int i) {
+    return AK ? src_km(A, p.lda, p.M, m0, k0, kend, IA * w + i)
+              : src_kc(A, p.lda, p.M, m0, k0, kend, IA * w + i);
+  };
+  auto srcB = [&](int k0, int i) {
+    return BKM ? src_km(B, p.ldb, p.N, n0, k0, kend, 4 * w + i)
+               : src_kc(B, p.ldb, p.N, n0, k0, kend, 4 * w + i);
+  };
+  const bf16* sA[IA];
   const bf16* sB[4];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    sA[i] = AK ? src_km(A, p.lda, p.M, m0, kbeg, kend, i) : src_kc(A, p.lda, p.M, m0, kbeg, kend, i);
-    sB[i] = BKM ? src_km(B, p.ldb, p.N, n0, kbeg, kend, i) : src_kc(B, p.ldb, p.N, n0, kbeg, kend, i);
-  }
+  for (int i = 0; i < IA; ++i) sA[i] = srcA(kbeg, i);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) sB[i] = srcB(kbeg, i);
   const int64_t stepA = AK ? (int64_t)BK * p.lda : BK;
   const int64_t stepB = BKM ? (int64_t)BK * p.ldb : BK;
 
-  auto dma_tile = [&](uint4* ta, uint4* tb, int t) __attribute__((always_inline)) {
+  auto dma_tile = [&](int s, int t) __attribute__((always_inline)) {
     const int k0 = kbeg + t * BK;
     if (k0 + BK <= kend) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        dma16(sA[i] + t * stepA, ta, i);
-        dma16(sB[i] + t * stepB, tb, i);
-      }
+      for (int i = 0; i < IA; ++i) dma16(sA[i] + t * stepA, stage_a(s), IA * w + i);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) dma16(sB[i] + t * stepB, stage_b(s), 4 * w + i);
     } else {   // ragged last tile: clamped sources
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        dma16(AK ? src_km(A, p.lda, p.M, m0, k0, kend, i) : src_kc(A, p.lda, p.M, m0, k0, kend, i),
-              ta, i);
-        dma16(BKM ? src_km(B, p.ldb, p.N, n0, k0, kend, i) : src_kc(B, p.ldb, p.N, n0, k0, kend, i),
-              tb, i);
-      }
+      for (int i = 0; i < IA; ++i) dma16(srcA(k0, i), stage_a(s), IA * w + i);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) dma16(srcB(k0, i), stage_b(s), 4 * w + i);
     }
   };
 
@@ -296,108 +326,121 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_big_kernel(GemmArgs p) {
     }
     return v;
   };
-  bf16x8 fa[2][4], fb[2][4];
-  auto read_frags = [&](const uint4* ta, const uint4* tb, int h, int t, bf16x8 (&a)[4],
-                        bf16x8 (&bb)[4]) __attribute__((always_inline)) {
+  auto frag_a = [&](int s, int i, int h) __attribute__((always_inline)) -> bf16x8 {
+    return AK ? frag_km(stage_a(s), wm, i, h) : frag_kc(stage_a(s), wm * (32 * MT) + 32 * i, h);
+  };
+  auto frag_b = [&](int s, int j, int h) __attribute__((always_inline)) -> bf16x8 {
+    return BKM ? frag_km(stage_b(s), wn, j, h) : frag_kc(stage_b(s), wn * 128 + 32 * j, h);
+  };
+  bf16x8 fa[2][MT], fb[2][4];
+  auto read_frags = [&](int s, int h, int t, bf16x8 (&a)[MT], bf16x8 (&bb)[4])
+      __attribute__((always_inline)) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      a[i] = AK ? frag_km(ta, wm, i, h) : frag_kc(ta, wm * 128 + 32 * i, h);
-      bb[i] = BKM ? frag_km(tb, wn, i, h) : frag_kc(tb, wn * 128 + 32 * i, h);
-    }
+    for (int i = 0; i < MT; ++i) a[i] = frag_a(s, i, h);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) bb[j] = frag_b(s, j, h);
     // ragged K tail: zero the A elements past kend (B there holds clamped, finite data)
     const int kr = kend - (kbeg + t * BK) - 16 * h - 8 * (l >> 5);
     if (kend - (kbeg + t * BK) < BK) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+      for (int i = 0; i < MT; ++i)
 #pragma unroll
         for (int e = 0; e < 8; ++e)
           if (e >= kr) a[i][e] = (bf16)0.f;
     }
   };
-  auto mma = [&](const bf16x8 (&a)[4], const bf16x8 (&bb)[4]) __attribute__((always_inline)) {
+  auto mma = [&](const bf16x8 (&a)[MT], const bf16x8 (&bb)[4]) __attribute__((always_inline)) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < MT; ++i)
 #pragma unroll
       for (int j = 0; j < 4; ++j)
         acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], bb[j], acc[i][j], 0, 0, 0);
   };
-  auto stage_a = [&](auto S) -> uint4* {
-    constexpr int s = decltype(S)::value;
-    if constexpr (s == 0) return sa0;
-    else if constexpr (s == 1) return sa1;
-    else if constexpr (s == 2) return sa2;
-    else return sa3;
-  };
-  auto stage_b = [&](auto S) -> uint4* {
-    constexpr int s = decltype(S)::value;
-    if constexpr (s == 0) return sb0;
-    else if constexpr (s == 1) return sb1;
-    else if constexpr (s == 2) return sb2;
-    else return sb3;
+  // wait until tile t+1 has landed for this wave: only DMAs of later tiles (at most
+  // NST-2 of them, issued before tile t+NST) may stay pending
+  auto wait_next = [&](int t) __attribute__((always_inline)) {
+    const int later = nk - 2 - t;
+    if constexpr (NST == 4) {
+      if (later >= 2) wait_vm<2 * IPT>();
+      else if (later == 1) wait_vm<IPT>();
+      else wait_vm<0>();
+    } else {
+      if (later >= 1) wait_vm<IPT>();
+      else wait_vm<0>();
+    }
   };
 
-  // one K tile t in stage S; fa[0]/fb[0] hold its first half on entry and the next
-  // tile's first half on exit
+  // one K tile t in stage S = t % NST; fa[0]/fb[0] hold its first half on entry and the
+  // next tile's first half on exit
   auto body = [&](auto S, int t) __attribute__((always_inline)) {
     constexpr int s = decltype(S)::value;
-    using SN = std::integral_constant<int, (s + 1) & 3>;
-    read_frags(stage_a(S), stage_b(S), 1, t, fa[1], fb[1]);
+    constexpr int sn = (s + 1) % NST;
+    read_frags(s, 1, t, fa[1], fb[1]);
     mma(fa[0], fb[0]);
-    // tile t+1 has landed for this wave once at most the later tiles' DMAs are pending
-    const int later = nk - 2 - t;   // tiles issued after t+1 (at most 2)
-    if (later >= 2) wait_vm<16>();
-    else if (later == 1) wait_vm<8>();
-    else wait_vm<0>();
+    wait_next(t);
     lds_barrier();
-    if (t + 4 < nk) dma_tile(stage_a(S), stage_b(S), t + 4);
-    if (t + 1 < nk) read_frags(stage_a(SN{}), stage_b(SN{}), 0, t + 1, fa[0], fb[0]);
+    if (t + NST < nk) dma_tile(s, t + NST);
+    if (t + 1 < nk) read_frags(sn, 0, t + 1, fa[0], fb[0]);
     mma(fa[1], fb[1]);
   };
 
-  // Steady-state tile (t + 9 <= nk at the start of the pass): the same work as body(),
-  // with each fragment read and DMA placed between two MFMAs in a fixed order
-  // (sched_barrier fences), so the MFMA pipe never waits behind a burst of memory
-  // instructions.
-  auto rd1 = [&](const uint4* ta, const uint4* tb, int h, int k, bf16x8 (&a)[4],
-                 bf16x8 (&bb)[4]) __attribute__((always_inline)) {
-    // in the order the MFMAs (i-major) first use them: A0, B0, B1, B2, B3, A1, A2, A3
+  // Steady-state tile (every tile read or DMA'd precedes the last, possibly ragged,
+  // tile): the same work as body(), with each fragment read and DMA placed between two
+  // MFMAs in a fixed order (sched_barrier fences), so the MFMA pipe never waits behind a
+  // burst of memory instructions.  Fragment reads go in the order the MFMAs (i-major)
+  // first use them: A0, B0..B3, A1..
+  constexpr int NMF = 4 * MT;      // MFMAs per K half
+  constexpr int NRD = MT + 4;      // fragment reads per K half
+  auto rd1 = [&](int s, int h, int k, bf16x8 (&a)[MT], bf16x8 (&bb)[4])
+      __attribute__((always_inline)) {
     const bool isb = k >= 1 && k <= 4;
     const int i = k == 0 ? 0 : isb ? k - 1 : k - 4;
-    if (isb) bb[i] = BKM ? frag_km(tb, wn, i, h) : frag_kc(tb, wn * 128 + 32 * i, h);
-    else a[i] = AK ? frag_km(ta, wm, i, h) : frag_kc(ta, wm * 128 + 32 * i, h);
+    if (isb) bb[i] = frag_b(s, i, h);
+    else a[i] = frag_a(s, i, h);
   };
-  auto mf1 = [&](int n, const bf16x8 (&a)[4], const bf16x8 (&bb)[4]) __attribute__((always_inline)) {
+  auto mf1 = [&](int n, const bf16x8 (&a)[MT], const bf16x8 (&bb)[4]) __attribute__((always_inline)) {
     acc[n >> 2][n & 3] =
         __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[n >> 2], bb[n & 3], acc[n >> 2][n & 3], 0, 0, 0);
   };
-  auto dm1 = [&](uint4* ta, uint4* tb, int t, int q) __attribute__((always_inline)) {
-    if (q < 4) dma16(sA[q] + t * stepA, ta, q);
-    else dma16(sB[q - 4] + t * stepB, tb, q - 4);
+  auto dm1 = [&](int s, int t, int q) __attribute__((always_inline)) {
+    if (q < IA) dma16(sA[q] + t * stepA, stage_a(s), IA * w + q);
+    else dma16(sB[q - IA] + t * stepB, stage_b(s), 4 * w + (q - IA));
   };
   auto body_full = [&](auto S, int t) __attribute__((always_inline)) {
     constexpr int s = decltype(S)::value;
-    using SN = std::integral_constant<int, (s + 1) & 3>;
+    constexpr int sn = (s + 1) % NST;
+    // first half: second-half reads of this tile, read r before MFMA r*NMF/NRD
 #pragma unroll
-    for (int q = 0; q < 8; ++q) {
-      rd1(stage_a(S), stage_b(S), 1, q, fa[1], fb[1]);
-      __builtin_amdgcn_sched_barrier(0);
-      mf1(2 * q, fa[0], fb[0]);
-      __builtin_amdgcn_sched_barrier(0);
-      mf1(2 * q + 1, fa[0], fb[0]);
+    for (int n = 0; n < NMF; ++n) {
+#pragma unroll
+      for (int r = 0; r < NRD; ++r)
+        if (r * NMF / NRD == n) {
+          rd1(s, 1, r, fa[1], fb[1]);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      mf1(n, fa[0], fb[0]);
       __builtin_amdgcn_sched_barrier(0);
     }
-    wait_vm<16>();
+    wait_vm<(NST - 2) * IPT>();
     lds_barrier();
+    // second half: DMA d of tile t+NST before MFMA d*NMF/IPT, read r of the next tile's
+    // first half right after MFMA r*NMF/NRD
 #pragma unroll
-    for (int q = 0; q < 8; ++q) {
-      dm1(stage_a(S), stage_b(S), t + 4, q);
+    for (int n = 0; n < NMF; ++n) {
+#pragma unroll
+      for (int d = 0; d < IPT; ++d)
+        if (d * NMF / IPT == n) {
+          dm1(s, t + NST, d);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      mf1(n, fa[1], fb[1]);
       __builtin_amdgcn_sched_barrier(0);
-      mf1(2 * q, fa[1], fb[1]);
-      __builtin_amdgcn_sched_barrier(0);
-      rd1(stage_a(SN{}), stage_b(SN{}), 0, q, fa[0], fb[0]);
-      __builtin_amdgcn_sched_barrier(0);
-      mf1(2 * q + 1, fa[1], fb[1]);
-      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int r = 0; r < NRD; ++r)
+        if (r * NMF / NRD == n) {
+          rd1(sn, 0, r, fa[0], fb[0]);
+          __builtin_amdgcn_sched_barrier(0);
+        }
     }
   };
 
@@ -406,41 +449,46 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_big_kernel(GemmArgs p) {
   using S2 = std::integral_constant<int, 2>;
   using S3 = std::integral_constant<int, 3>;
   if (nk > 0) {
-    dma_tile(sa0, sb0, 0);
-    if (nk > 1) dma_tile(sa1, sb1, 1);
-    if (nk > 2) dma_tile(sa2, sb2, 2);
-    if (nk > 3) dma_tile(sa3, sb3, 3);
-    if (nk > 3) wait_vm<24>();
-    else if (nk == 3) wait_vm<16>();
-    else if (nk == 2) wait_vm<8>();
-    else wait_vm<0>();
+#pragma unroll
+    for (int s = 0; s < NST; ++s)
+      if (s < nk) dma_tile(s, s);
+    // tile 0 landed: the prologue's later tiles may stay pending
+    if constexpr (NST == 4) {
+      if (nk > 3) wait_vm<3 * IPT>();
+      else if (nk == 3) wait_vm<2 * IPT>();
+      else if (nk == 2) wait_vm<IPT>();
+      else wait_vm<0>();
+    } else {
+      if (nk > 2) wait_vm<2 * IPT>();
+      else if (nk == 2) wait_vm<IPT>();
+      else wait_vm<0>();
+    }
     lds_barrier();
-    read_frags(sa0, sb0, 0, 0, fa[0], fb[0]);
+    read_frags(0, 0, 0, fa[0], fb[0]);
     int t = 0;
-    // steady state: the tiles read (<= t+4) and the tiles DMA'd (<= t+7) all precede the
-    // last, possibly ragged, tile, so every source is unclamped and in bounds
-    for (; t + 9 <= nk; t += 4) {
+    // steady state: the tiles read (<= t+NST) and the tiles DMA'd (<= t+2NST-1) all
+    // precede the last, possibly ragged, tile, so every source is unclamped and in bounds
+    for (; t + 2 * NST + 1 <= nk; t += NST) {
       body_full(S0{}, t);
       body_full(S1{}, t + 1);
       body_full(S2{}, t + 2);
-      body_full(S3{}, t + 3);
+      if constexpr (NST == 4) body_full(S3{}, t + 3);
     }
-    for (; t < nk; t += 4) {
+    for (; t < nk; t += NST) {
       body(S0{}, t);
       if (t + 1 < nk) body(S1{}, t + 1);
       if (t + 2 < nk) body(S2{}, t + 2);
-      if (t + 3 < nk) body(S3{}, t + 3);
+      if constexpr (NST == 4)
+        if (t + 3 < nk) body(S3{}, t + 3);
     }
   }
 
-  // epilogue: each wave stages 16x128 accumulator rows at a time in its own LDS tile
-  // (the last barrier of the loop ended every fragment read).  Pass pi = 2i + hh covers
+  // epilogue: each wave stages 16x128 accumulator rows at a time in its own LDS region
+  // (after the barrier below no wave reads the ring any more).  Pass pi = 2i + hh covers
   // rows 32i + 16hh .. +15 of the wave tile; lane (u, cg) takes row (l/16) + 4u, columns
   // 8cg..8cg+7.
   __syncthreads();
-  uint4* own = w == 0 ? sa0 : w == 1 ? sa1 : w == 2 ? sa2 : sa3;
-  float* stage = reinterpret_cast<float*>(own);
-  static_assert(16 * SP * 4 <= TILE_U4 * 16, "epilogue staging must fit in one tile");
+  float* stage = reinterpret_cast<float*>(smem) + w * 16 * SP;
   const int cg = l & 15;
   const int n = n0 + wn * 128 + 8 * cg;   // N % 8 == 0: all eight columns or none in range
   const bool vec = n < p.N;
@@ -453,7 +501,7 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_big_kernel(GemmArgs p) {
 #pragma unroll
     for (int e = 0; e < 8; ++e) bias8[e] = (float)b8[e];
   }
-  auto row_of = [&](int pi, int u) { return m0 + wm * 128 + 16 * pi + (l >> 4) + 4 * u; };
+  auto row_of = [&](int pi, int u) { return m0 + wm * (32 * MT) + 16 * pi + (l >> 4) + 4 * u; };
   constexpr bool kAux = EPI == EPI_GELU_BWD || EPI == EPI_RESID || EPI == EPI_F32;
   AuxV ax[2][4];
   auto fetch = [&](int pi, AuxV (&dst)[4]) __attribute__((always_inline)) {
@@ -467,12 +515,12 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_big_kernel(GemmArgs p) {
   };
   fetch(0, ax[0]);
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {     // (acc[i] must be indexed statically)
+  for (int i = 0; i < MT; ++i) {     // (acc[i] must be indexed statically)
 #pragma unroll
     for (int hh = 0; hh < 2; ++hh) {
       const int pi = 2 * i + hh;
-      if (pi + 1 < 8) fetch(pi + 1, ax[(pi + 1) & 1]);
-      __syncthreads();
+      if (pi + 1 < 2 * MT) fetch(pi + 1, ax[(pi + 1) & 1]);
+      lds_wave_fence();   // the previous pass's staging reads are done
 #pragma unroll
       for (int j = 0; j < 4; ++j)
 #pragma unroll
@@ -480,7 +528,7 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_big_kernel(GemmArgs p) {
           const int rr = 8 * ((e >> 2) & 1) + 4 * (l >> 5) + (e & 3);
           stage[rr * SP + 32 * j + (l & 31)] = acc[i][j][e];
         }
-      __syncthreads();
+      lds_wave_fence();   // this pass's staging writes are visible to the whole wave
       auto out_row = [&](int u, const AuxV& a) __attribute__((always_inline)) {
         const int rr = (l >> 4) + 4 * u;
         const int m = row_of(pi, u);
@@ -503,39 +551,43 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_big_kernel(GemmArgs p) {
   }
 }
 
-template <bool AK, bool BKM, int EPI>
+template <int MT, bool AK, bool BKM, int EPI>
 hipError_t launch_big(const GemmArgs& a0, hipStream_t s) {
   GemmArgs a = a0;
-  a.tiles_m = (a.M + BM - 1) / BM;
+  a.tiles_m = (a.M + Shape<MT>::BM - 1) / Shape<MT>::BM;
   a.tiles_n = (a.N + BN - 1) / BN;
   const int nt = a.tiles_m * a.tiles_n;
   const int nb = (nt + 7) / 8 * 8;
   int splits = a.kps > 0 ? (a.K + a.kps - 1) / a.kps : 1;
   if (a.kps <= 0) a.kps = a.K;
   if (splits < 1) splits = 1;
-  hipLaunchKernelGGL((gemm_big_kernel<AK, BKM, EPI>), dim3(nb, splits), dim3(NTHR), 0, s, a);
+  hipLaunchKernelGGL((gemm_big_kernel<MT, AK, BKM, EPI>), dim3(nb, splits), dim3(NTHR), 0, s, a);
   return hipGetLastError();
 }
 
-template <bool AK, bool BKM>
+template <int MT, bool AK, bool BKM>
 hipError_t dispatch_big(const GemmArgs& a, int epi, hipStream_t s) {
   switch (epi) {
-    case EPI_STORE: return launch_big<AK, BKM, EPI_STORE>(a, s);
-    case EPI_GELU: return launch_big<AK, BKM, EPI_GELU>(a, s);
-    case EPI_RESID: return launch_big<AK, BKM, EPI_RESID>(a, s);
-    case EPI_GELU_BWD: return launch_big<AK, BKM, EPI_GELU_BWD>(a, s);
-    case EPI_F32: return launch_big<AK, BKM, EPI_F32>(a, s);
+    case EPI_STORE: return launch_big<MT, AK, BKM, EPI_STORE>(a, s);
+    case EPI_GELU: return launch_big<MT, AK, BKM, EPI_GELU>(a, s);
+    case EPI_RESID: return launch_big<MT, AK, BKM, EPI_RESID>(a, s);
+    case EPI_GELU_BWD: return launch_big<MT, AK, BKM, EPI_GELU_BWD>(a, s);
+    case EPI_F32: return launch_big<MT, AK, BKM, EPI_F32>(a, s);
   }
   return hipErrorInvalidValue;
 }
 
 }  // namespace
 
+// Tile shape per layout, from timings of the encoder's products on MI355X: with a K-major
+// B operand (NN) the 128x256 tiles at two blocks per CU are faster on every encoder shape
+// (both short and long K); with a K-contiguous B (NT) the 256x256 tiles mostly win; the
+// weight gradient (TN, K-major A) splits K to fill the chip and takes 256x256 tiles.
 hipError_t gemm_big(int layout, int epi, const GemmArgs& a, hipStream_t s) {
   switch (layout) {
-    case GEMM_NT: return dispatch_big<false, false>(a, epi, s);
-    case GEMM_NN: return dispatch_big<false, true>(a, epi, s);
-    case GEMM_TN: return dispatch_big<true, true>(a, epi, s);
+    case GEMM_NT: return dispatch_big<4, false, false>(a, epi, s);
+    case GEMM_NN: return dispatch_big<2, false, true>(a, epi, s);
+    case GEMM_TN: return dispatch_big<4, true, true>(a, epi, s);
   }
   return hipErrorInvalidValue;
 }

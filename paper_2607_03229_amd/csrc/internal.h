@@ -81,6 +81,17 @@ hipError_t colsum_accumulate(int dtype_in, const void* X, int64_t ld, int64_t ro
                              float* part, float* out, hipStream_t s);
 hipError_t splitk_reduce(const float* part, int splits, int64_t M, int64_t N, float* out,
                          int64_t ldo, hipStream_t s);
+// Batched transpose of up to kMaxTJobs matrices in one launch: dst[c][r] = src[r][c]
+// for r < rows, c < cols (row strides lds, ldd in elements; element bits are copied).
+struct TJob {
+  const void* src = nullptr;
+  int64_t lds = 0;
+  void* dst = nullptr;
+  int64_t ldd = 0;
+  int rows = 0, cols = 0;
+};
+constexpr int kMaxTJobs = 4;
+hipError_t transpose_batch(int dtype, const TJob* jobs, int n, hipStream_t s);
 hipError_t pad_cols(int dtype, const void* src, int64_t rows, int K, void* dst, int Kp,
                     hipStream_t s);
 // tab: (cos, sin) pairs [positions][d/4] of p * theta^(-4k/d); requires d % 8 == 0

@@ -245,6 +245,11 @@ int build_plan(const Cfg& c, const int32_t* cu, int n_seg, const int32_t* thw, i
     p.ws_xp = ws.take((size_t)N * c.kp * E);
     p.ws_wpe = ws.take((size_t)h * c.kp * E);
   }
+  // The forward multiplies by transposed weights ([in][out], so the GEMM's weight
+  // operand is K-major); they are transposed one layer (or the merger, or the patch
+  // embedding) at a time into this region.
+  p.ws_wt = ws.take((size_t)E * std::max({3 * h * h + h * h + 2 * h * m, 16 * h * h + 4 * h * H,
+                                          (int64_t)c.kp * h}));
   auto act_set = [&](Arena& a, bool keep_u, bool share_h) {
     ActSet s{};
     s.hin = a.take((size_t)N * h * 4);

@@ -83,6 +83,7 @@ struct Plan {
   // workspace layout
   size_t ws_pos = 0, ws_qwork = 0, ws_kwork = 0, ws_rope = 0;
   size_t ws_xp = 0, ws_wpe = 0;
+  size_t ws_wt = 0;                // the forward's transposed weights, one layer at a time
   ActSet ws_act{};                 // frozen forward activations
   MergerSet ws_mrg{};
   size_t ws_dh = 0, ws_dht = 0, ws_dhm = 0, ws_dhmt = 0, ws_dx32 = 0, ws_du = 0, ws_do = 0,

@@ -60,46 +60,57 @@ def test_gemm_layouts(dtype, layout):
         assert err < (2e-5 if dtype == "f32" else 1e-5), (M, N, K, err)
 
 
+@pytest.mark.parametrize("layout", [NT, NN])
 @pytest.mark.parametrize("dtype,M,N,K", [("bf16", 333, 264, 192), ("f32", 333, 264, 192),
-                                         ("bf16", 700, 392, 256), ("bf16", 530, 300, 64)])
-def test_gemm_epilogues(dtype, M, N, K):
-    """Fused epilogues; (700, 392) runs the 256x256 kernel; (530, 300) has N % 8 != 0
-    (rows that break 16-byte alignment), which the dispatcher sends to the general kernel."""
+                                         ("bf16", 700, 392, 256), ("bf16", 530, 300, 64),
+                                         ("bf16", 1100, 520, 360)])
+def test_gemm_epilogues(dtype, M, N, K, layout):
+    """Fused epilogues; (700, 392) and (1100, 520) run the large-tile kernels (256x256
+    tiles for NT, 128x256 for NN); (530, 300) has N % 8 != 0 (rows that break 16-byte
+    alignment), which the dispatcher sends to the general kernel.  NN takes the weight
+    as [K][N]."""
     import paper_2607_03229_amd as mp
     torch, dev = torch_dev()
     rng = np.random.default_rng(7)
     A, B, bias = rnd(rng, (M, K), dtype), rnd(rng, (N, K), dtype, 0.1), rnd(rng, (N,), dtype)
-    dA, dB, db = to_dev(A, dtype), to_dev(B, dtype), to_dev(bias, dtype)
+    dA, db = to_dev(A, dtype), to_dev(bias, dtype)
+    if layout == NT:
+        dB, ldb = to_dev(B, dtype), K
+    else:   # [K][N] in rows padded to a multiple of 8 (a K-major operand's stride rule)
+        ldb = (N + 7) // 8 * 8
+        BT = np.zeros((K, ldb), np.float32)
+        BT[:, :N] = B.T
+        dB = to_dev(BT, dtype)
     pre = oracle.linear(A, B, bias)
     # store with bias
-    announce(f"gemm epilogue store {dtype}")
+    announce(f"gemm epilogue store {dtype} layout={layout}")
     C = zeros((M, N), dtype)
-    mp.op_gemm(_dt(dtype), NT, E_STORE, M, N, K, dA, K, dB, K, C, N, bias=db)
+    mp.op_gemm(_dt(dtype), layout, E_STORE, M, N, K, dA, K, dB, ldb, C, N, bias=db)
     assert max_rel(host(C), pre) < TOL[dtype]
     # GELU, with GELU' of the pre-activation stored for the backward
-    announce(f"gemm epilogue gelu {dtype}")
+    announce(f"gemm epilogue gelu {dtype} layout={layout}")
     C, C2 = zeros((M, N), dtype), zeros((M, N), dtype)
-    mp.op_gemm(_dt(dtype), NT, E_GELU, M, N, K, dA, K, dB, K, C, N, bias=db, C2=C2, ldc2=N)
+    mp.op_gemm(_dt(dtype), layout, E_GELU, M, N, K, dA, K, dB, ldb, C, N, bias=db, C2=C2, ldc2=N)
     assert max_rel(host(C2), oracle.gelu_grad(pre)) < TOL[dtype]
     assert max_rel(host(C), oracle.gelu(pre)) < TOL[dtype]
     # residual update in place (aux aliases C)
-    announce(f"gemm epilogue resid {dtype}")
+    announce(f"gemm epilogue resid {dtype} layout={layout}")
     R = rng.standard_normal((M, N)).astype(np.float32)
     C = to_dev(R, "f32")
-    mp.op_gemm(_dt(dtype), NT, E_RESID, M, N, K, dA, K, dB, K, C, N, bias=db, aux=C, ld_aux=N)
+    mp.op_gemm(_dt(dtype), layout, E_RESID, M, N, K, dA, K, dB, ldb, C, N, bias=db, aux=C, ld_aux=N)
     assert max_rel(host(C), R + pre) < 2e-5
     # GELU backward: acc * aux, aux = GELU'(u) as the forward epilogue stores it
-    announce(f"gemm epilogue gelu-bwd {dtype}")
+    announce(f"gemm epilogue gelu-bwd {dtype} layout={layout}")
     U = rnd(rng, (M, N), dtype)
     Gd = oracle.gelu_grad(U).astype(np.float32)
     C = zeros((M, N), dtype)
-    mp.op_gemm(_dt(dtype), NT, E_GELUBWD, M, N, K, dA, K, dB, K, C, N, aux=to_dev(Gd, dtype),
+    mp.op_gemm(_dt(dtype), layout, E_GELUBWD, M, N, K, dA, K, dB, ldb, C, N, aux=to_dev(Gd, dtype),
                ld_aux=N)
     assert max_rel(host(C), oracle.linear(A, B) * oracle.gelu_grad(U)) < TOL[dtype]
     # fp32 accumulate (beta = 1)
-    announce(f"gemm epilogue f32 accumulate {dtype}")
+    announce(f"gemm epilogue f32 accumulate {dtype} layout={layout}")
     C = to_dev(R, "f32")
-    mp.op_gemm(_dt(dtype), NT, E_F32, M, N, K, dA, K, dB, K, C, N, beta=1)
+    mp.op_gemm(_dt(dtype), layout, E_F32, M, N, K, dA, K, dB, ldb, C, N, beta=1)
     assert max_rel(host(C), R + oracle.linear(A, B)) < 2e-5
 
 
