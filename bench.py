@@ -88,10 +88,13 @@ def kernel_class(name: str):
     """Library profiling class of a dispatched kernel symbol (mangled or demangled)."""
     import re
     lay = {(0, 0): "NT", (0, 1): "NN", (1, 1): "TN"}
-    m = re.search(r"gemm_big_kernel<(?:\d, )?(true|false), (true|false), (\d)>", name)
+    m = re.search(r"gemm_big_kernel<(true|false), (true|false), (\d)>", name)
     if m:
         return f"gemm_{lay[(int(m.group(1) == 'true'), int(m.group(2) == 'true'))]}_{EPI_NAMES[int(m.group(3))]}"
-    m = re.search(r"gemm_(?:big_)?kernelI(?:Li\dE)?(?:DF16b|f)?Lb([01])ELb([01])ELi(\d)E", name)
+    m = re.search(r"gemm_nn_kernel(?:<|ILi)(\d)", name)
+    if m:
+        return f"gemm_NN_{EPI_NAMES[int(m.group(1))]}"
+    m = re.search(r"gemm_(?:big_)?kernelI(?:DF16b|f)?Lb([01])ELb([01])ELi(\d)E", name)
     if m:
         return f"gemm_{lay[(int(m.group(1)), int(m.group(2)))]}_{EPI_NAMES[int(m.group(3))]}"
     for key, cls in (("attn_fwd_kernel", "attn_fwd"), ("attn_bwd_dq_kernel", "attn_bwd_dq"),

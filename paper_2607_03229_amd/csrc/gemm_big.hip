@@ -3,19 +3,17 @@
 // C[M,N] = sum_k A(m,k) B(n,k) with the same operand layouts and epilogues as the
 // general kernel (NT forward, NN input gradient, TN weight gradient).
 //
-// Two block shapes share one kernel template, both 256 threads = 4 wave64 in a 2x2 grid
-// of v_mfma_f32_32x32x16_bf16 accumulators and the same K order, so a given output
-// element gets bitwise the same value from either:
-//   MT = 4: block tile 256x256, each wave 128x128 (4x4 accumulators, 256 AGPRs), a
-//           4-stage ring (128 KB of LDS), one block per CU.  A 128x128 wave tile keeps
-//           the LDS traffic (fragment reads + tile fills) well under what the LDS
-//           delivers at the full MFMA rate.
-//   MT = 2: block tile 128x256, each wave 64x128 (2x4 accumulators), a 3-stage ring
-//           (72 KB), two blocks per CU.  Twice the tile count rounds the last wave of
-//           tiles more finely, and one block's epilogue overlaps the other's main loop.
+// Two kernels, both 256 threads = 4 wave64 in a 2x2 grid of v_mfma_f32_32x32x16_bf16
+// accumulators with the same K order, so a given output element gets bitwise the same
+// value from either:
+//   gemm_big_kernel (NT, TN): block tile 256x256, each wave 128x128 (4x4 accumulators,
+//     256 AGPRs), a 4-stage ring (128 KB of LDS), one block per CU.  A 128x128 wave tile
+//     keeps the LDS traffic (fragment reads + tile fills) well under what the LDS
+//     delivers at the full MFMA rate.
+//   gemm_nn_kernel (NN, described with it below): block tile 128x256, two blocks per CU.
 //
 // Operand tiles (rows x 32 k) are filled by 16-byte global->LDS DMA (global_load_lds)
-// in the ring, so the next tiles are in flight while tile t is multiplied and no tile
+// in a ring, so the next tiles are in flight while tile t is multiplied and no tile
 // data passes through VGPRs.  Each lane of a DMA instruction owns one fixed LDS slot and
 // picks the source element of that slot, which is how the tiles get their
 // bank-conflict-free XOR swizzles:
@@ -198,28 +196,19 @@ __device__ __forceinline__ void epi8_vec(const GemmArgs& p, int split, int m, in
 
 // ---- the kernel ----------------------------------------------------------------------
 
-// Block-shape constants of the MT-tiles-per-wave variant.
-template <int MT>
-struct Shape {
-  static_assert(MT == 2 || MT == 4, "block shapes: 128x256 or 256x256");
-  static constexpr int BM = 64 * MT;                 // block rows
-  static constexpr int NST = MT == 4 ? 4 : 3;        // ring stages
-  static constexpr int A_U4 = BM * BK * 2 / 16;      // 16-byte slots of an A tile
-  static constexpr int IA = MT;                      // A-tile DMA instructions per wave
-  static constexpr int IPT = IA + 4;                 // DMA instructions per wave per K tile
-  static constexpr int LDS_U4 = NST * (A_U4 + B_U4);
-  static constexpr int OCC = MT == 4 ? 1 : 2;        // resident blocks per CU
-};
+// 256x256 tiles: MT 32-row MFMA tiles per wave in M, NST ring stages, IA / IPT DMA
+// instructions per wave for an A tile / a whole K tile.
+constexpr int BM = 256, MT = 4, NST = 4;
+constexpr int A_U4 = BM * BK * 2 / 16;   // 16-byte slots of an A tile (1024)
+constexpr int IA = 4, IPT = IA + 4;
+constexpr int BIG_LDS_U4 = NST * (A_U4 + B_U4);
 
-template <int MT, bool AK, bool BKM, int EPI>
-__global__ __launch_bounds__(NTHR, Shape<MT>::OCC) void gemm_big_kernel(GemmArgs p) {
-  using SH = Shape<MT>;
-  constexpr int BM = SH::BM, NST = SH::NST, A_U4 = SH::A_U4, IA = SH::IA, IPT = SH::IPT;
-  static_assert(!AK || MT == 4, "a K-major A operand needs 256-row tiles");
+template <bool AK, bool BKM, int EPI>
+__global__ __launch_bounds__(NTHR, 1) void gemm_big_kernel(GemmArgs p) {
   // the ring: stage s of A at smem + s*A_U4, of B at smem + NST*A_U4 + s*B_U4.  The DMAs
   // are assembly with a memory clobber, so no fragment read moves across one.
-  __shared__ uint4 smem[SH::LDS_U4];
-  static_assert(4 * 16 * SP * 4 <= SH::LDS_U4 * 16, "epilogue staging must fit in the ring");
+  __shared__ uint4 smem[BIG_LDS_U4];
+  static_assert(4 * 16 * SP * 4 <= BIG_LDS_U4 * 16, "epilogue staging must fit in the ring");
 
   // XCD-aware block order (consecutive block ids go round-robin to the 8 XCDs), then
   // groups of GROUP_M tile-rows for L2 reuse
@@ -360,14 +349,9 @@ __global__ __launch_bounds__(NTHR, Shape<MT>::OCC) void gemm_big_kernel(GemmArgs
   // NST-2 of them, issued before tile t+NST) may stay pending
   auto wait_next = [&](int t) __attribute__((always_inline)) {
     const int later = nk - 2 - t;
-    if constexpr (NST == 4) {
-      if (later >= 2) wait_vm<2 * IPT>();
-      else if (later == 1) wait_vm<IPT>();
-      else wait_vm<0>();
-    } else {
-      if (later >= 1) wait_vm<IPT>();
-      else wait_vm<0>();
-    }
+    if (later >= 2) wait_vm<2 * IPT>();
+    else if (later == 1) wait_vm<IPT>();
+    else wait_vm<0>();
   };
 
   // one K tile t in stage S = t % NST; fa[0]/fb[0] hold its first half on entry and the
@@ -453,16 +437,10 @@ __global__ __launch_bounds__(NTHR, Shape<MT>::OCC) void gemm_big_kernel(GemmArgs
     for (int s = 0; s < NST; ++s)
       if (s < nk) dma_tile(s, s);
     // tile 0 landed: the prologue's later tiles may stay pending
-    if constexpr (NST == 4) {
-      if (nk > 3) wait_vm<3 * IPT>();
-      else if (nk == 3) wait_vm<2 * IPT>();
-      else if (nk == 2) wait_vm<IPT>();
-      else wait_vm<0>();
-    } else {
-      if (nk > 2) wait_vm<2 * IPT>();
-      else if (nk == 2) wait_vm<IPT>();
-      else wait_vm<0>();
-    }
+    if (nk > 3) wait_vm<3 * IPT>();
+    else if (nk == 3) wait_vm<2 * IPT>();
+    else if (nk == 2) wait_vm<IPT>();
+    else wait_vm<0>();
     lds_barrier();
     read_frags(0, 0, 0, fa[0], fb[0]);
     int t = 0;
@@ -472,14 +450,13 @@ __global__ __launch_bounds__(NTHR, Shape<MT>::OCC) void gemm_big_kernel(GemmArgs
       body_full(S0{}, t);
       body_full(S1{}, t + 1);
       body_full(S2{}, t + 2);
-      if constexpr (NST == 4) body_full(S3{}, t + 3);
+      body_full(S3{}, t + 3);
     }
     for (; t < nk; t += NST) {
       body(S0{}, t);
       if (t + 1 < nk) body(S1{}, t + 1);
       if (t + 2 < nk) body(S2{}, t + 2);
-      if constexpr (NST == 4)
-        if (t + 3 < nk) body(S3{}, t + 3);
+      if (t + 3 < nk) body(S3{}, t + 3);
     }
   }
 
@@ -551,43 +528,419 @@ __global__ __launch_bounds__(NTHR, Shape<MT>::OCC) void gemm_big_kernel(GemmArgs
   }
 }
 
-template <int MT, bool AK, bool BKM, int EPI>
-hipError_t launch_big(const GemmArgs& a0, hipStream_t s) {
+// ---- NN kernel: 128x256 tiles, paired A stages ---------------------------------------
+//
+// The input-gradient and forward products (A = activations [M][K], B = weight [K][N]).  A
+// is filled two K tiles at a time: each DMA instruction fetches 8 rows x 64 k, whole
+// 128-byte lines of A (64-byte rows would send half-line requests, which the memory
+// pipeline serves at a markedly lower rate).  Its 1 KB of LDS holds the 8 rows' first 32 k
+// (tile 2P) and then their second 32 k (tile 2P+1), each as 64-byte rows with the same
+// chunk swizzle as the 256x256 kernel, so a tile's fragments sit at a fixed offset in the
+// pair stage.  Two pair stages (2 x 16 KB) and three B stages (3 x 16 KB of 512-byte
+// K-major rows) make 80 KB, so two blocks share a CU and each one's barriers and epilogue
+// overlap the other's main loop.  Waves 2x2, each a 64x128 tile of 2x4 32x32 accumulators.
+//
+// body(t): the second half's fragments of tile t are read beside the first half's
+// MFMAs; wait until tile t+1 has landed; barrier; DMA of B tile t+3 into tile t's B stage
+// and, after the second tile of a pair, of A pair (t+3, t+4) into the pair stage just
+// consumed; tile t+1's first-half fragments are read beside tile t's second-half MFMAs.
+// In issue order the DMAs are B(0) A(0,1) B(1) B(2) A(2,3) B(3) B(4) A(4,5) ..., so when
+// tile t+1 is needed the later DMAs still allowed in flight are B(t+2) and, for even t,
+// A(t+2, t+3).  Pair stages repeat every 4 tiles: the steady loop is unrolled over that
+// period, so A fragment addresses are constant offsets; the B stage rotates at run time.
+
+constexpr int NN_BM = 128;
+constexpr int NN_A_U4 = NN_BM * 2 * BK * 2 / 16;   // 16-byte slots of an A pair stage (1024)
+constexpr int NN_LDS_U4 = 2 * NN_A_U4 + 3 * B_U4;  // 80 KB
+constexpr int NN_IA = 4;                           // A pair DMA instructions per wave
+constexpr int NN_IB = 4;                           // B tile DMA instructions per wave
+constexpr int NN_PERIOD = 4;
+
+// A pair source of instruction q: lane l fetches row 8q + (l%32)/4, tile half l/32,
+// physical chunk l%4, which holds logical chunk (l%4) ^ fkc(row): k = k0 + 32 (l/32) +
+// 8 ((l%4) ^ fkc(row)) of the pair's 64-wide K range.
+__device__ __forceinline__ const bf16* src_pair(const bf16* X, int64_t ld, int rows, int r0, int k0,
+                                                int kend, int q) {
+  const int l = threadIdx.x & 63;
+  const int row = 8 * q + ((l & 31) >> 2);
+  int k = k0 + 32 * (l >> 5) + 8 * ((l & 3) ^ fkc(row));
+  k = k < kend ? k : kend - 8;
+  int gr = r0 + row;
+  gr = gr < rows ? gr : rows - 1;
+  return X + (int64_t)gr * ld + k;
+}
+
+template <int EPI>
+__global__ __launch_bounds__(NTHR, 2) void gemm_nn_kernel(GemmArgs p) {
+  __shared__ uint4 smem[NN_LDS_U4];
+  static_assert(4 * 16 * SP * 4 <= NN_LDS_U4 * 16, "epilogue staging must fit in the ring");
+
+  const int ntiles = p.tiles_m * p.tiles_n;
+  const int nb = gridDim.x;
+  const int b = blockIdx.x;
+  const int pid = (b % 8) * (nb / 8) + (b / 8);
+  if (pid >= ntiles) return;
+  const int group = pid / (GROUP_M * p.tiles_n);
+  const int first_m = group * GROUP_M;
+  const int gsize = min(p.tiles_m - first_m, GROUP_M);
+  const int tm = first_m + (pid % gsize);
+  const int tn = (pid % (GROUP_M * p.tiles_n)) / gsize;
+  const int split = blockIdx.y;
+  const int m0 = tm * NN_BM, n0 = tn * BN;
+  const int kbeg = split * p.kps;
+  const int kend = min(p.K, kbeg + p.kps);
+  const int nk = kend > kbeg ? (kend - kbeg + BK - 1) / BK : 0;
+  const bf16* A = reinterpret_cast<const bf16*>(p.A);
+  const bf16* B = reinterpret_cast<const bf16*>(p.B);
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), l = threadIdx.x & 63;
+  const int wm = w >> 1, wn = w & 1;
+
+  f32x16 acc[2][4];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+
+  const char* const lds = reinterpret_cast<const char*>(smem);
+  // B stages first, so B fragment offsets fit the 16-bit LDS immediate
+  auto pair_stage = [&](int pa) { return smem + 3 * B_U4 + pa * NN_A_U4; };
+  auto b_stage = [&](int sb) { return smem + sb * B_U4; };
+
+  // DMA sources of the first A pair / B tile (a full pair P adds 64P elements, a full
+  // B tile t adds t*BK rows)
+  const bf16* sA[NN_IA];
+  const bf16* sB[NN_IB];
+#pragma unroll
+  for (int i = 0; i < NN_IA; ++i) sA[i] = src_pair(A, p.lda, p.M, m0, kbeg, kend, NN_IA * w + i);
+#pragma unroll
+  for (int i = 0; i < NN_IB; ++i) sB[i] = src_km(B, p.ldb, p.N, n0, kbeg, kend, NN_IB * w + i);
+  const int64_t stepB = (int64_t)BK * p.ldb;
+  auto dma_b = [&](int sb, int t) __attribute__((always_inline)) {
+    const int k0 = kbeg + t * BK;
+    if (k0 + BK <= kend) {
+#pragma unroll
+      for (int i = 0; i < NN_IB; ++i) dma16(sB[i] + t * stepB, b_stage(sb), NN_IB * w + i);
+    } else {
+#pragma unroll
+      for (int i = 0; i < NN_IB; ++i)
+        dma16(src_km(B, p.ldb, p.N, n0, k0, kend, NN_IB * w + i), b_stage(sb), NN_IB * w + i);
+    }
+  };
+  auto dma_a = [&](int pa, int t) __attribute__((always_inline)) {   // pair (t, t+1), t even
+    const int k0 = kbeg + t * BK;
+    if (k0 + 2 * BK <= kend) {
+#pragma unroll
+      for (int i = 0; i < NN_IA; ++i) dma16(sA[i] + (t >> 1) * (2 * BK), pair_stage(pa), NN_IA * w + i);
+    } else {
+#pragma unroll
+      for (int i = 0; i < NN_IA; ++i)
+        dma16(src_pair(A, p.lda, p.M, m0, k0, kend, NN_IA * w + i), pair_stage(pa), NN_IA * w + i);
+    }
+  };
+
+  // A fragment i of K half h of the tile with parity par in pair stage pa: rows
+  // rb = wm*64 + 32i + l%32 live in instruction slots rb/8 (1 KB each), half par, 64-byte
+  // row rb%8, logical chunk 2h + l/32 at physical chunk (2h + l/32) ^ fkc(rb).
+  const int kcA = 1024 * ((l & 31) >> 3) + 64 * (l & 7) + 16 * ((l >> 5) ^ fkc(l & 31));
+  // B (K-major, as in the 256x256 kernel)
+  int km_off[4];
+  {
+    const int G = l >> 4, j = l & 15;
+    const int kr = 8 * (G >> 1) + (j >> 2);
+    const int gg = gkm(j >> 2);
+    const int lo = 2 * (G & 1) + ((j & 3) >> 1);
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      km_off[i] = kr * 512 + 16 * ((4 * (i ^ (gg >> 2))) + (lo ^ (gg & 3))) + 8 * (j & 1);
+  }
+  auto frag_a = [&](int pa, int par, int i, int h) __attribute__((always_inline)) -> bf16x8 {
+    const char* base = lds + (3 * B_U4 + pa * NN_A_U4) * 16 + par * 512 + (wm * 64 + 32 * i) * 128;
+    const uint4 v = *reinterpret_cast<const uint4*>(base + (kcA ^ (32 * h)));
+    return *reinterpret_cast<const bf16x8*>(&v);
+  };
+  auto frag_b = [&](int sb, int j, int h) __attribute__((always_inline)) -> bf16x8 {
+    const char* base = lds + sb * B_U4 * 16 + 16 * 16 * wn + h * 16 * 512 + km_off[j];
+    const s16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(base));
+    const s16x4 c = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(base + 4 * 512));
+    bf16x8 v;
+    const bf16* pa_ = reinterpret_cast<const bf16*>(&a);
+    const bf16* pc = reinterpret_cast<const bf16*>(&c);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      v[e] = pa_[e];
+      v[4 + e] = pc[e];
+    }
+    return v;
+  };
+  bf16x8 fa[2][2], fb[2][4];
+  // fragments of K half h of tile t = period slot I (ragged last tile: A zeroed past kend)
+  auto read_frags = [&](auto II, int t, int h, bf16x8 (&a)[2], bf16x8 (&bb)[4])
+      __attribute__((always_inline)) {
+    constexpr int I = decltype(II)::value;
+    constexpr int pa = (I >> 1) & 1, par = I & 1;
+    const int sb = t % 3;
+#pragma unroll
+    for (int i = 0; i < 2; ++i) a[i] = frag_a(pa, par, i, h);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) bb[j] = frag_b(sb, j, h);
+    const int rem = kend - (kbeg + t * BK);
+    if (rem < BK) {
+      const int kr = rem - 16 * h - 8 * (l >> 5);
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          if (e >= kr) a[i][e] = (bf16)0.f;
+    }
+  };
+  auto mma = [&](const bf16x8 (&a)[2], const bf16x8 (&bb)[4]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], bb[j], acc[i][j], 0, 0, 0);
+  };
+  auto mf1 = [&](int n, const bf16x8 (&a)[2], const bf16x8 (&bb)[4]) __attribute__((always_inline)) {
+    acc[n >> 2][n & 3] =
+        __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[n >> 2], bb[n & 3], acc[n >> 2][n & 3], 0, 0, 0);
+  };
+  // read k (0..5) of a half in first-use order A0, B0..B3, A1
+  auto rd1 = [&](int pa, int par, int sb, int h, int k, bf16x8 (&a)[2], bf16x8 (&bb)[4])
+      __attribute__((always_inline)) {
+    if (k >= 1 && k <= 4) bb[k - 1] = frag_b(sb, k - 1, h);
+    else a[k == 0 ? 0 : 1] = frag_a(pa, par, k == 0 ? 0 : 1, h);
+  };
+
+  // steady-state tile t = period slot I (t + 6 <= nk), B stage sb = t % 3, next sbn:
+  // every DMA full, no ragged read
+  auto body_fast = [&](auto II, int t, int sb, int sbn) __attribute__((always_inline)) {
+    constexpr int I = decltype(II)::value;
+    constexpr int P = I & 1, pa = (I >> 1) & 1;
+    constexpr int In = (I + 1) % NN_PERIOD;
+    constexpr int pan = (In >> 1) & 1, parn = In & 1;
+    constexpr int ND = P ? NN_IA + NN_IB : NN_IB;   // DMA instructions after the barrier
+#pragma unroll
+    for (int n = 0; n < 8; ++n) {
+#pragma unroll
+      for (int r = 0; r < 6; ++r)
+        if (r * 8 / 6 == n) {
+          rd1(pa, P, sb, 1, r, fa[1], fb[1]);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      mf1(n, fa[0], fb[0]);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    if constexpr (P == 0) wait_vm<NN_IB + NN_IA>();
+    else wait_vm<NN_IB>();
+    lds_barrier();
+#pragma unroll
+    for (int n = 0; n < 8; ++n) {
+#pragma unroll
+      for (int d = 0; d < ND; ++d)
+        if (d * 8 / ND == n) {
+          if (d < NN_IB) dma16(sB[d] + (t + 3) * stepB, b_stage(sb), NN_IB * w + d);
+          else dma16(sA[d - NN_IB] + ((t + 3) >> 1) * (2 * BK), pair_stage(pa), NN_IA * w + (d - NN_IB));
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      mf1(n, fa[1], fb[1]);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int r = 0; r < 6; ++r)
+        if (r * 8 / 6 == n) {
+          rd1(pan, parn, sbn, 0, r, fa[0], fb[0]);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+    }
+  };
+  // tile t = period slot I near the end: guarded DMAs, masked reads
+  auto body_slow = [&](auto II, int t) __attribute__((always_inline)) {
+    constexpr int I = decltype(II)::value;
+    constexpr int pa = (I >> 1) & 1;
+    using INext = std::integral_constant<int, (I + 1) % NN_PERIOD>;
+    read_frags(II, t, 1, fa[1], fb[1]);
+    mma(fa[0], fb[0]);
+    if (t + 2 < nk) {
+      if constexpr (I & 1) wait_vm<NN_IB>();
+      else wait_vm<NN_IB + NN_IA>();
+    } else {
+      wait_vm<0>();
+    }
+    lds_barrier();
+    if (t + 3 < nk) {
+      dma_b(t % 3, t + 3);
+      if constexpr (I & 1) dma_a(pa, t + 3);
+    }
+    if (t + 1 < nk) read_frags(INext{}, t + 1, 0, fa[0], fb[0]);
+    mma(fa[1], fb[1]);
+  };
+
+  using S0 = std::integral_constant<int, 0>;
+  using S1 = std::integral_constant<int, 1>;
+  using S2 = std::integral_constant<int, 2>;
+  using S3 = std::integral_constant<int, 3>;
+  if (nk > 0) {
+    dma_b(0, 0);
+    dma_a(0, 0);
+    if (nk > 1) dma_b(1, 1);
+    if (nk > 2) {
+      dma_b(2, 2);
+      dma_a(1, 2);
+    }
+    if (nk > 2) wait_vm<2 * NN_IB + NN_IA>();
+    else if (nk == 2) wait_vm<NN_IB>();
+    else wait_vm<0>();
+    lds_barrier();
+    read_frags(S0{}, 0, 0, fa[0], fb[0]);
+    // steady state: tiles t with t + 6 <= nk, four at a time (t % 4 == slot); then the
+    // last tiles (at most 8)
+    const int nfast = nk >= 6 ? (nk - 5) / 4 * 4 : 0;
+    int t = 0;
+    for (; t < nfast; t += 4) {
+      const int s0 = t % 3;
+      const int s1 = s0 == 2 ? 0 : s0 + 1;
+      const int s2 = s1 == 2 ? 0 : s1 + 1;
+      body_fast(S0{}, t, s0, s1);
+      body_fast(S1{}, t + 1, s1, s2);
+      body_fast(S2{}, t + 2, s2, s0);
+      body_fast(S3{}, t + 3, s0, s1);
+    }
+    for (; t < nk; t += 4) {
+      body_slow(S0{}, t);
+      if (t + 1 < nk) body_slow(S1{}, t + 1);
+      if (t + 2 < nk) body_slow(S2{}, t + 2);
+      if (t + 3 < nk) body_slow(S3{}, t + 3);
+    }
+  }
+
+  // epilogue (as in the 256x256 kernel, 64-row wave tiles)
+  __syncthreads();
+  float* stage = reinterpret_cast<float*>(smem) + w * 16 * SP;
+  const int cg = l & 15;
+  const int n = n0 + wn * 128 + 8 * cg;
+  const bool vec = n < p.N;
+  float bias8[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) bias8[e] = 0.f;
+  if (vec && p.bias != nullptr && split == 0) {
+    const uint4 bb = *reinterpret_cast<const uint4*>(reinterpret_cast<const bf16*>(p.bias) + n);
+    const bf16* b8 = reinterpret_cast<const bf16*>(&bb);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) bias8[e] = (float)b8[e];
+  }
+  auto row_of = [&](int pi, int u) { return m0 + wm * 64 + 16 * pi + (l >> 4) + 4 * u; };
+  constexpr bool kAux = EPI == EPI_GELU_BWD || EPI == EPI_RESID || EPI == EPI_F32;
+  AuxV ax[2][4];
+  auto fetch = [&](int pi, AuxV (&dst)[4]) __attribute__((always_inline)) {
+    if constexpr (kAux) {
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int m = row_of(pi, u);
+        if (vec && m < p.M) aux_fetch<EPI>(p, split, m, n, dst[u]);
+      }
+    }
+  };
+  fetch(0, ax[0]);
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh) {
+      const int pi = 2 * i + hh;
+      if (pi + 1 < 4) fetch(pi + 1, ax[(pi + 1) & 1]);
+      lds_wave_fence();
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int e = 8 * hh; e < 8 * hh + 8; ++e) {
+          const int rr = 8 * ((e >> 2) & 1) + 4 * (l >> 5) + (e & 3);
+          stage[rr * SP + 32 * j + (l & 31)] = acc[i][j][e];
+        }
+      lds_wave_fence();
+      auto out_row = [&](int u, const AuxV& a) __attribute__((always_inline)) {
+        const int rr = (l >> 4) + 4 * u;
+        const int m = row_of(pi, u);
+        if (m >= p.M || n >= p.N) return;
+        float v[8];
+        const float4 x0 = *reinterpret_cast<const float4*>(stage + rr * SP + 8 * cg);
+        const float4 x1 = *reinterpret_cast<const float4*>(stage + rr * SP + 8 * cg + 4);
+        v[0] = x0.x; v[1] = x0.y; v[2] = x0.z; v[3] = x0.w;
+        v[4] = x1.x; v[5] = x1.y; v[6] = x1.z; v[7] = x1.w;
+        epi8_vec<EPI>(p, split, m, n, v, bias8, a);
+      };
+      if constexpr (kAux) {
+#pragma unroll
+        for (int u = 0; u < 4; ++u) out_row(u, ax[pi & 1][u]);
+      } else {
+#pragma unroll 1
+        for (int u = 0; u < 4; ++u) out_row(u, ax[0][0]);
+      }
+    }
+  }
+}
+
+template <int EPI>
+hipError_t launch_nn(const GemmArgs& a0, hipStream_t s) {
   GemmArgs a = a0;
-  a.tiles_m = (a.M + Shape<MT>::BM - 1) / Shape<MT>::BM;
+  a.tiles_m = (a.M + NN_BM - 1) / NN_BM;
   a.tiles_n = (a.N + BN - 1) / BN;
   const int nt = a.tiles_m * a.tiles_n;
   const int nb = (nt + 7) / 8 * 8;
   int splits = a.kps > 0 ? (a.K + a.kps - 1) / a.kps : 1;
   if (a.kps <= 0) a.kps = a.K;
   if (splits < 1) splits = 1;
-  hipLaunchKernelGGL((gemm_big_kernel<MT, AK, BKM, EPI>), dim3(nb, splits), dim3(NTHR), 0, s, a);
+  hipLaunchKernelGGL((gemm_nn_kernel<EPI>), dim3(nb, splits), dim3(NTHR), 0, s, a);
   return hipGetLastError();
 }
 
-template <int MT, bool AK, bool BKM>
+hipError_t dispatch_nn(const GemmArgs& a, int epi, hipStream_t s) {
+  switch (epi) {
+    case EPI_STORE: return launch_nn<EPI_STORE>(a, s);
+    case EPI_GELU: return launch_nn<EPI_GELU>(a, s);
+    case EPI_RESID: return launch_nn<EPI_RESID>(a, s);
+    case EPI_GELU_BWD: return launch_nn<EPI_GELU_BWD>(a, s);
+    case EPI_F32: return launch_nn<EPI_F32>(a, s);
+  }
+  return hipErrorInvalidValue;
+}
+
+template <bool AK, bool BKM, int EPI>
+hipError_t launch_big(const GemmArgs& a0, hipStream_t s) {
+  GemmArgs a = a0;
+  a.tiles_m = (a.M + BM - 1) / BM;
+  a.tiles_n = (a.N + BN - 1) / BN;
+  const int nt = a.tiles_m * a.tiles_n;
+  const int nb = (nt + 7) / 8 * 8;
+  int splits = a.kps > 0 ? (a.K + a.kps - 1) / a.kps : 1;
+  if (a.kps <= 0) a.kps = a.K;
+  if (splits < 1) splits = 1;
+  hipLaunchKernelGGL((gemm_big_kernel<AK, BKM, EPI>), dim3(nb, splits), dim3(NTHR), 0, s, a);
+  return hipGetLastError();
+}
+
+template <bool AK, bool BKM>
 hipError_t dispatch_big(const GemmArgs& a, int epi, hipStream_t s) {
   switch (epi) {
-    case EPI_STORE: return launch_big<MT, AK, BKM, EPI_STORE>(a, s);
-    case EPI_GELU: return launch_big<MT, AK, BKM, EPI_GELU>(a, s);
-    case EPI_RESID: return launch_big<MT, AK, BKM, EPI_RESID>(a, s);
-    case EPI_GELU_BWD: return launch_big<MT, AK, BKM, EPI_GELU_BWD>(a, s);
-    case EPI_F32: return launch_big<MT, AK, BKM, EPI_F32>(a, s);
+    case EPI_STORE: return launch_big<AK, BKM, EPI_STORE>(a, s);
+    case EPI_GELU: return launch_big<AK, BKM, EPI_GELU>(a, s);
+    case EPI_RESID: return launch_big<AK, BKM, EPI_RESID>(a, s);
+    case EPI_GELU_BWD: return launch_big<AK, BKM, EPI_GELU_BWD>(a, s);
+    case EPI_F32: return launch_big<AK, BKM, EPI_F32>(a, s);
   }
   return hipErrorInvalidValue;
 }
 
 }  // namespace
 
-// Tile shape per layout, from timings of the encoder's products on MI355X: with a K-major
-// B operand (NN) the 128x256 tiles at two blocks per CU are faster on every encoder shape
-// (both short and long K); with a K-contiguous B (NT) the 256x256 tiles mostly win; the
-// weight gradient (TN, K-major A) splits K to fill the chip and takes 256x256 tiles.
+// Kernel per layout, from timings of the encoder's products on MI355X: NN (the forward
+// with transposed weights, and the input gradient) runs faster on the 128x256 kernel at
+// every encoder shape; NT and the weight gradient (TN, split over K to fill the chip)
+// take the 256x256 kernel.
 hipError_t gemm_big(int layout, int epi, const GemmArgs& a, hipStream_t s) {
   switch (layout) {
-    case GEMM_NT: return dispatch_big<4, false, false>(a, epi, s);
-    case GEMM_NN: return dispatch_big<2, false, true>(a, epi, s);
-    case GEMM_TN: return dispatch_big<4, true, true>(a, epi, s);
+    case GEMM_NT: return dispatch_big<false, false>(a, epi, s);
+    case GEMM_NN: return dispatch_nn(a, epi, s);
+    case GEMM_TN: return dispatch_big<true, true>(a, epi, s);
   }
   return hipErrorInvalidValue;
 }
