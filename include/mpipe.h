@@ -181,10 +181,16 @@ mpipe_status mpipe_merge_check_indices(const int64_t* placeholder_idx, int64_t n
 const char* mpipe_last_error(void);
 
 /* Kernel timing: when enabled, every kernel launch of the handle is bracketed
- * by HIP events on the caller's stream.  mpipe_profile_read synchronizes the
- * stream, then reports per kernel class the launch count, total milliseconds
- * and algorithmic FLOPs (class names: "gemm", "attn_fwd", "attn_bwd", "other"),
- * and resets the counters.  Returns the number of classes written. */
+ * by HIP events on the stream it runs on.  mpipe_profile_read synchronizes the
+ * caller's stream (the backward joins its side stream into it before returning),
+ * then reports per kernel class the launch count, total milliseconds and
+ * algorithmic FLOPs, and resets the counters.  Class names are the kernel kind
+ * ("gemm_<layout>_<epilogue>", "attn_fwd", "attn_bwd_dq", "attn_bwd_dkdv",
+ * "layernorm", "layernorm_bwd", "rope", "colsum", "splitk_reduce", "transpose",
+ * "pad"); launches on the side stream carry the suffix "@side", and their times
+ * include the sharing of compute units with the caller's stream.  names receives
+ * up to cap NUL-terminated names of name_stride bytes each.  Returns the number of
+ * classes written, or -1 on a null handle or a failed synchronization. */
 mpipe_status mpipe_profile_enable(mpipe_encoder* enc, int32_t enable);
 int32_t mpipe_profile_read(mpipe_encoder* enc, void* hip_stream, int32_t cap, char* names,
                            int32_t name_stride, int64_t* launches, double* ms, double* flops);

@@ -108,11 +108,14 @@ template <int D, int NW> struct TG {
 typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 
-template <int D, int NW>
+// UW: take the wave index as a uniform (scalar) value; which choice gives the better
+// code differs by kernel (measured: the forward and dQ kernels prefer it, dK/dV does not).
+template <int D, int NW, bool UW = true>
 __device__ __forceinline__ void dma_tile(uint4* tile, const bf16* X, int64_t ld, int r0,
                                          int rlast) {
   constexpr int PC = AD<D>::PC, NC = AD<D>::NC;
-  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int w = UW ? __builtin_amdgcn_readfirstlane(threadIdx.x >> 6) : threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63;
 #pragma unroll
   for (int i = 0; i < TG<D, NW>::NI; ++i) {
     const int inst = i * NW + w;
@@ -146,7 +149,7 @@ __device__ __forceinline__ void tile_src_init(TileSrc<D, NW>& S, int64_t ld) {
 }
 template <int D, int NW>
 __device__ __forceinline__ void dma_tile_full(uint4* tile, const bf16* Xr0, const TileSrc<D, NW>& S) {
-  const int w = threadIdx.x >> 6;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
 #pragma unroll
   for (int i = 0; i < TG<D, NW>::NI; ++i)
     __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(Xr0 + S.off[i]),
@@ -197,9 +200,12 @@ __device__ __forceinline__ bf16x8 frag_trt(const uint4* tile, int k0a, int k0b, 
 }
 
 // ---- forward ----------------------------------------------------------------------
-
-// ---- forward ----------------------------------------------------------------------
 // 3-stage pipeline over 64-key tiles: tile t+2 is in flight while tile t is used.
+// The softmax offset m of a query (log2 domain) moves only when the tile's maximum
+// exceeds it by more than kRescaleLog2: weights exp2(s - m) then stay below 2^8, exact in
+// fp32 and as representable in bf16 as any weight <= 1, and the output rescale (a
+// multiply per accumulator) runs on a few tiles instead of most.  Row sums of the bf16
+// weights come from the PV MFMAs themselves, with a ones operand in place of V.
 template <int D, int NS>
 __global__ __launch_bounds__(64 * (8 / NS), NS == 2 ? 2 : 1) void attn_fwd_kernel(AttnArgs p) {
   constexpr int NW = 8 / NS, RW = 16 * NS;   // waves per block, rows per wave
@@ -214,6 +220,10 @@ __global__ __launch_bounds__(64 * (8 / NS), NS == 2 ? 2 : 1) void attn_fwd_kerne
   const bf16* V = reinterpret_cast<const bf16*>(p.v) + head * D;
   const float sl2 = p.scale * kLog2e;
   const int nt = (s1 - s0 + 63) / 64;
+  constexpr float kRescaleLog2 = 8.0f;
+  bf16x8 ones;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) ones[e] = (bf16)1.0f;
 
   RowFrag<D> qf[NS];
   int qrow[NS];
@@ -222,16 +232,14 @@ __global__ __launch_bounds__(64 * (8 / NS), NS == 2 ? 2 : 1) void attn_fwd_kerne
     qrow[qs] = q0 + RW * w + 16 * qs + r;
     load_rowfrag<D>(qf[qs], Q, p.ld, min(qrow[qs], s1 - 1), g);
   }
-  float m[NS], lsum[NS];
-  f32x4 o[NS][NDT];
-#pragma unroll
-  for (int qs = 0; qs < NS; ++qs)
-#pragma unroll
-    for (int dt = 0; dt < NDT; ++dt) o[qs][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float m[NS];
+  f32x4 o[NS][NDT], osum[NS];   // osum: every element holds the query's weight sum
 #pragma unroll
   for (int qs = 0; qs < NS; ++qs) {
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt) o[qs][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    osum[qs] = f32x4{0.f, 0.f, 0.f, 0.f};
     m[qs] = -INFINITY;
-    lsum[qs] = 0.f;
   }
 
   TileSrc<D, NW> kvsrc;
@@ -282,24 +290,22 @@ __global__ __launch_bounds__(64 * (8 / NS), NS == 2 ? 2 : 1) void attn_fwd_kerne
         for (int v = 0; v < 4; ++v) mx = fmaxf(mx, s[kq][qs][v]);
       mx = fmaxf(mx, __shfl_xor(mx, 16));
       mx = fmaxf(mx, __shfl_xor(mx, 32));
-      const float mn = fmaxf(m[qs], mx * sl2);
-      const float alpha = fast_exp2(m[qs] - mn);
-      m[qs] = mn;
-      float ps = 0.f;
+      // move the offset (and rescale, uniformly skipped when no query needs it) only
+      // when the tile's maximum exceeds it by more than kRescaleLog2
+      const float mt = mx * sl2;
+      if (__any(mt > m[qs] + kRescaleLog2)) {
+        const float mn = mt > m[qs] + kRescaleLog2 ? mt : m[qs];
+        const float alpha = fast_exp2(m[qs] - mn);
+        m[qs] = mn;
+#pragma unroll
+        for (int dt = 0; dt < NDT; ++dt) o[qs][dt] *= alpha;
+        osum[qs] *= alpha;
+      }
+      const float mq = m[qs];
 #pragma unroll
       for (int kq = 0; kq < 4; ++kq)
 #pragma unroll
-        for (int v = 0; v < 4; ++v) {
-          const float e = fast_exp2(fmaf(s[kq][qs][v], sl2, -mn));
-          s[kq][qs][v] = e;
-          ps += e;
-        }
-      lsum[qs] = lsum[qs] * alpha + ps;
-      // the output rescale is skipped (uniformly) when no query's running max moved
-      if (__any(alpha != 1.0f)) {
-#pragma unroll
-        for (int dt = 0; dt < NDT; ++dt) o[qs][dt] *= alpha;
-      }
+        for (int v = 0; v < 4; ++v) s[kq][qs][v] = fast_exp2(fmaf(s[kq][qs][v], sl2, -mq));
       pb[qs][0] = pack8(s[0][qs], s[1][qs]);
       pb[qs][1] = pack8(s[2][qs], s[3][qs]);
     }
@@ -312,6 +318,11 @@ __global__ __launch_bounds__(64 * (8 / NS), NS == 2 ? 2 : 1) void attn_fwd_kerne
         for (int qs = 0; qs < NS; ++qs)
           o[qs][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb[qs][kk], o[qs][dt], 0, 0, 0);
       }
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+      for (int qs = 0; qs < NS; ++qs)
+        osum[qs] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pb[qs][kk], osum[qs], 0, 0, 0);
   };
   issue(0, k0s, v0s);
   issue(1, k1s, v1s);
@@ -323,9 +334,7 @@ __global__ __launch_bounds__(64 * (8 / NS), NS == 2 ? 2 : 1) void attn_fwd_kerne
   bf16* O = reinterpret_cast<bf16*>(p.out) + head * D;
 #pragma unroll
   for (int qs = 0; qs < NS; ++qs) {
-    float tot = lsum[qs];
-    tot += __shfl_xor(tot, 16);
-    tot += __shfl_xor(tot, 32);
+    const float tot = osum[qs][0];
     const int q = qrow[qs];
     if (q < s1) {
       const float inv = 1.0f / tot;
@@ -384,8 +393,8 @@ __global__ __launch_bounds__(64 * (8 / NS), NS == 2 ? 2 : 1) void attn_bwd_dkdv_
       __attribute__((always_inline)) {
     if (t < nt) {
       const int r0 = s0 + 64 * t;
-      dma_tile<D, NW>(qt, Q, p.ld, r0, s1 - 1);
-      dma_tile<D, NW>(dt_, dO, p.ldo, r0, s1 - 1);
+      dma_tile<D, NW, false>(qt, Q, p.ld, r0, s1 - 1);
+      dma_tile<D, NW, false>(dt_, dO, p.ldo, r0, s1 - 1);
       dma_vec64(lt, LSE, r0, s1 - 1);
       dma_vec64(et, DEL, r0, s1 - 1);
     }

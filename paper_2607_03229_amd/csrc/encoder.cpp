@@ -37,6 +37,7 @@ struct Rec {
   std::string cls;
   hipEvent_t a, b;
   double flops;
+  bool side;   // launched on the handle's side stream (overlaps the caller's stream)
 };
 }  // namespace
 
@@ -79,7 +80,7 @@ hipError_t run(mpipe_encoder* e, hipStream_t s, const char* cls, double flops, F
   if (a) hipEventRecord(a, s);
   hipError_t r = f();
   if (b) hipEventRecord(b, s);
-  if (a && b) e->recs.push_back({cls, a, b, flops});
+  if (a && b) e->recs.push_back({cls, a, b, flops, e->side != nullptr && s == e->side});
   return r;
 }
 
@@ -816,7 +817,7 @@ int32_t mpipe_profile_read(mpipe_encoder* e, void* stream, int32_t cap, char* na
   for (auto& r : e->recs) {
     float t = 0.f;
     hipEventElapsedTime(&t, r.a, r.b);
-    auto& v = agg[r.cls];
+    auto& v = agg[r.side ? r.cls + "@side" : r.cls];
     std::get<0>(v) += 1;
     std::get<1>(v) += t;
     std::get<2>(v) += r.flops;
