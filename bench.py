@@ -32,16 +32,20 @@ def log(msg: str):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
-def model_flops(cfg, n_patches: int, sum_len2: int, trainable: bool) -> float:
+def model_flops(cfg, n_patches: int, sum_len2: int, trainable: int) -> float:
     """Algorithmic FLOPs of one step (recompute and padding excluded).
 
     forward F = 2 N Kpe h + L (8 N h^2 + 4 N h m + 4 h sum_i L_i^2) + 8 N h^2 + 2 N h H;
-    trained = 3 F minus the patch-gradient GEMM (2 N Kpe h), which the trainable
-    source does not compute (nothing is sent upstream); frozen = F."""
+    trained (mode 1) = 3 F minus the patch-gradient GEMM (2 N Kpe h), which the trainable
+    source does not compute (nothing is sent upstream); only the merger trainable
+    (mode 2) = F plus the merger's input and weight gradients, 2 (8 N h^2 + 2 N h H);
+    frozen = F."""
     N, h, m, H, L = n_patches, cfg.hidden, cfg.mlp, cfg.llm_hidden, cfg.layers
     kpe = cfg.k_pe
-    F = (2 * N * kpe * h + L * (8 * N * h * h + 4 * N * h * m + 4 * h * sum_len2)
-         + 8 * N * h * h + 2 * N * h * H)
+    merger = 8 * N * h * h + 2 * N * h * H
+    F = (2 * N * kpe * h + L * (8 * N * h * h + 4 * N * h * m + 4 * h * sum_len2) + merger)
+    if int(trainable) == 2:
+        return float(F + 2 * merger)
     return float(3 * F - 2 * N * kpe * h) if trainable else float(F)
 
 
@@ -54,7 +58,7 @@ def hardware_flops(cfg, n_patches: int, sum_len2: int, trainable: bool) -> float
     dpad = (d + 31) // 32 * 32
     extra = 2.0 * h * sum_len2 * (dpad - d) / d      # one S-type product, padding only
     per_layer = extra
-    if trainable:
+    if int(trainable) == 1:
         per_layer += 6.0 * h * sum_len2 + 4 * (2.0 * h * sum_len2 * dpad / d)
         per_layer -= 4 * (2.0 * h * sum_len2)        # those four products' unpadded share
     return model_flops(cfg, n_patches, sum_len2, trainable) + L * per_layer
@@ -281,8 +285,8 @@ def main():
         mp.merge_scatter(merged, idx, emb)
         if trainable:
             mp.merge_gather(d_emb, idx, d_merged)
-            enc.bwd(weights, patches, wl.cu_seqlens, wl.grid_thw, True, tape, d_merged, d_w,
-                    None, ws)
+            enc.bwd(weights, patches, wl.cu_seqlens, wl.grid_thw, trainable, tape, d_merged,
+                    d_w, None, ws)
 
     for i in range(args.warmup):
         step()
@@ -360,7 +364,7 @@ def main():
         "ms_per_step_min": round(per_step[0], 3),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": cfg.dtype, "data": "synthetic",
-        "config": {"workload": wl.name, "seed": args.seed, "mode": "trained" if trainable else "frozen",
+        "config": {"workload": wl.name, "seed": args.seed, "mode": {0: "frozen", 1: "trained", 2: "merger-trained"}[int(trainable)],
                    "n_items": wl.n_items, "n_patches": wl.n_patches, "n_merged": wl.n_merged,
                    "sum_seg_len2": sum_len2,
                    "encoder": f"h{cfg.hidden} L{cfg.layers} heads{cfg.heads} mlp{cfg.mlp} "

@@ -86,6 +86,26 @@ typedef enum {
 
 typedef enum { MPIPE_F32 = 0, MPIPE_BF16 = 1 } mpipe_dtype;
 
+/* The `trainable` argument of the size, forward and backward calls.  Lemma 1 fixes
+ * a region's backward work from which regions are trainable; here it is applied to
+ * the encoder's own parts, ordered input-to-loss: the patch embedding and blocks,
+ * then the merger (the projector that aligns the encoder's features with the LLM;
+ * Sec. 2 notes that an alignment stage often trains only such layers while the
+ * encoder stays frozen).
+ *   MPIPE_FROZEN       nothing trainable: no tape, and the backward is a no-op.
+ *   MPIPE_TRAINED      every part trainable: the backward produces the gradient of
+ *                      every weight tensor (and of the patches on request).
+ *   MPIPE_TRAIN_MERGER only the merger trainable.  The merger is then the trainable
+ *                      source: it receives the gradient of the merged rows, reduces
+ *                      its own weight gradients and sends nothing upstream, so the
+ *                      blocks and the patch embedding run no backward and their
+ *                      gradient entries are not written.  The tape holds the merger's
+ *                      inputs only.
+ * The forward result is bitwise the same in every mode (Corollary 1: the mode
+ * decides which backward work exists, not what the forward computes).  Any other
+ * value is rejected with MPIPE_ERR_INVALID_ARG. */
+typedef enum { MPIPE_FROZEN = 0, MPIPE_TRAINED = 1, MPIPE_TRAIN_MERGER = 2 } mpipe_train_mode;
+
 typedef struct {
   int32_t in_chans;        /* 3 */
   int32_t patch;           /* P = 14 */
@@ -114,18 +134,20 @@ int32_t mpipe_param_tensors(const mpipe_encoder_cfg* cfg);
 mpipe_status mpipe_param_info(const mpipe_encoder_cfg* cfg, int32_t i, char* name, int32_t cap,
                               int64_t* offset, int64_t* rows, int64_t* cols);
 
-/* Buffer sizes for one micro-batch: device workspace, tape (0 when frozen),
- * merged rows and packed patch rows.  Validates the metadata. */
+/* Buffer sizes for one micro-batch in a trainability mode (mpipe_train_mode):
+ * device workspace, tape (0 when frozen, the merger's inputs only for
+ * MPIPE_TRAIN_MERGER), merged rows and packed patch rows.  Validates the metadata. */
 mpipe_status mpipe_encoder_sizes(const mpipe_encoder* enc, const int32_t* cu_seqlens,
                                  int32_t n_seg, const int32_t* grid_thw, int32_t n_items,
                                  int32_t trainable, size_t* workspace_bytes, size_t* tape_bytes,
                                  int64_t* n_merged, int64_t* n_patches);
 
 /* Fwd(enc, m).  weights, patches: device, cfg dtype.  merged: device
- * [n_merged][llm_hidden], cfg dtype, overwritten.  trainable != 0 records the
- * activations the backward needs into `tape` (tape_bytes from
- * mpipe_encoder_sizes); frozen passes tape = NULL, 0.  The forward result is the
- * same either way (Corollary 1).  workspace: device scratch, not kept.
+ * [n_merged][llm_hidden], cfg dtype, overwritten.  trainable (mpipe_train_mode)
+ * != MPIPE_FROZEN records the activations that mode's backward needs into `tape`
+ * (tape_bytes from mpipe_encoder_sizes with the same mode); frozen passes
+ * tape = NULL, 0.  The forward result is the same in every mode (Corollary 1).
+ * workspace: device scratch, not kept.
  * n_items == 0 (a text-only micro-batch) is a valid no-op. */
 mpipe_status mpipe_encoder_fwd(mpipe_encoder* enc, const void* weights, const void* patches,
                                const int32_t* cu_seqlens, int32_t n_seg, const int32_t* grid_thw,
@@ -133,11 +155,13 @@ mpipe_status mpipe_encoder_fwd(mpipe_encoder* enc, const void* weights, const vo
                                size_t tape_bytes, void* workspace, size_t workspace_bytes,
                                void* hip_stream);
 
-/* Bwd(enc, m)^?.  trainable == 0 returns MPIPE_NOOP_FROZEN and writes nothing.
- * tape: as recorded by the matching trained forward (same weights, patches and
- * metadata).  d_merged: device [n_merged][llm_hidden], cfg dtype.  d_weights:
- * device fp32, flat layout of the weights, ACCUMULATED (+=).  d_patches:
- * nullable; if given, overwritten with dL/dpatches [N][C*T*P*P] in cfg dtype. */
+/* Bwd(enc, m)^?.  trainable == MPIPE_FROZEN returns MPIPE_NOOP_FROZEN and writes
+ * nothing.  tape: as recorded by the matching forward (same mode, weights, patches
+ * and metadata).  d_merged: device [n_merged][llm_hidden], cfg dtype.  d_weights:
+ * device fp32, flat layout of the weights, ACCUMULATED (+=): every tensor's entries
+ * for MPIPE_TRAINED, the merger's only (its LayerNorm, fc1 and fc2) for
+ * MPIPE_TRAIN_MERGER.  d_patches: nullable; if given (MPIPE_TRAINED only, else
+ * MPIPE_ERR_INVALID_ARG), overwritten with dL/dpatches [N][C*T*P*P] in cfg dtype. */
 mpipe_status mpipe_encoder_bwd(mpipe_encoder* enc, const void* weights, const void* patches,
                                const int32_t* cu_seqlens, int32_t n_seg, const int32_t* grid_thw,
                                int32_t n_items, int32_t trainable, const void* tape,

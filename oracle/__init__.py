@@ -142,10 +142,11 @@ def positions(grid_thw: np.ndarray) -> Tuple[np.ndarray, np.ndarray]:
 # Whole encoder
 # --------------------------------------------------------------------------
 
-def encoder(cfg, weights, patches, cu_seqlens, grid_thw, trainable: bool,
+def encoder(cfg, weights, patches, cu_seqlens, grid_thw, trainable,
             d_merged=None, want_d_patches: bool = False, d_w_init=None,
             precision: str = "f64"):
-    """Run the oracle encoder.
+    """Run the oracle encoder.  trainable: False/0 frozen, True/1 every part trainable,
+    2 only the merger trainable (its backward stops at the merger's LayerNorm).
 
     Returns (status, merged, d_w, d_patches); d_w / d_patches are None unless a
     backward ran.  d_w starts from ``d_w_init`` (zeros by default): the oracle

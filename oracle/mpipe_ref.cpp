@@ -397,7 +397,10 @@ int encoder(const ref_cfg& c, const T* w, const T* X, const int32_t* cu, int n_s
   int rc = validate(cu, n_seg, thw, n_items, &N);
   if (rc) return rc;
   if (c.hidden % c.heads || (c.hidden / c.heads) % 4 || c.merge != 2) return -1;
+  if (trainable < 0 || trainable > 2) return -1;
+  if (trainable == 2 && dX) return -1;   // the trainable source sends nothing upstream
   if (dM && !trainable) return 1;  // Lemma 1: a frozen encoder has no backward
+  const bool merger_only = trainable == 2;
   if (N == 0) return 0;
 
   const int64_t h = c.hidden, m = c.mlp, Hl = c.llm_hidden, nh = c.heads, d = h / nh;
@@ -446,7 +449,7 @@ int encoder(const ref_cfg& c, const T* w, const T* X, const int32_t* cu, int n_s
     for (size_t i = 0; i < S.u.size(); ++i) S.g[i] = gelu(S.u[i]);
     linear(S.g.data(), P(b0 + 10), P(b0 + 11), N, m, h, tmp.data());
     for (size_t i = 0; i < H.size(); ++i) H[i] += tmp[i];
-    if (!dM) { Layer<T> empty; std::swap(st[l], empty); }  // nothing kept without a backward
+    if (!dM || merger_only) { Layer<T> empty; std::swap(st[l], empty); }  // no block backward
   }
   // merger
   Vec<T> Z((size_t)N * h), meanz(N), rstdz(N);
@@ -488,6 +491,9 @@ int encoder(const ref_cfg& c, const T* w, const T* X, const int32_t* cu, int n_s
   Vec<T> dH((size_t)N * h);
   layernorm_bwd(dZ.data(), H.data(), P(MG + 0), meanz.data(), rstdz.data(), N, h, dH.data(),
                 G(MG + 0), G(MG + 1));
+  // only the merger trainable: it is the trainable source (Lemma 1 over the encoder's
+  // parts), so the frozen blocks and patch embedding below it run no backward
+  if (merger_only) return 0;
 
   Vec<T> dG((size_t)N * m), dB((size_t)N * h), dHm((size_t)N * h), dO((size_t)N * h);
   Vec<T> dqkv((size_t)N * 3 * h), dA((size_t)N * h);

@@ -21,7 +21,7 @@
  *
  * Every floating-point routine exists in double (suffix _f64) and float (_f32).
  * Return codes: 0 ok, 1 frozen no-op (backward requested on a frozen encoder),
- * negative on invalid metadata.
+ * negative on invalid metadata or arguments.
  */
 #ifndef MPIPE_REF_H
 #define MPIPE_REF_H
@@ -44,9 +44,14 @@ int32_t ref_param_tensors(const ref_cfg* c);
 /* Patch position (y, x) of every packed row, from the window-major row order. */
 int ref_positions(const int32_t* grid_thw, int32_t n_items, int32_t* pos_y, int32_t* pos_x);
 
-/* Whole encoder.  merged: [n_merged][llm_hidden].  If d_merged is non-NULL the
- * backward runs (only when trainable; otherwise returns 1 and writes nothing to
- * d_w / d_patches): d_w += dL/dw, and d_patches (if non-NULL) = dL/dpatches. */
+/* Whole encoder.  merged: [n_merged][llm_hidden].  trainable: 0 nothing trainable,
+ * 1 every part trainable, 2 only the merger trainable.  If d_merged is non-NULL the
+ * backward runs (trainable == 0 returns 1 and writes nothing to d_w / d_patches):
+ * d_w += dL/dw for the trainable parts, and d_patches (if non-NULL; trainable == 1
+ * only) = dL/dpatches.  With only the merger trainable, Lemma 1 read over the
+ * encoder's parts (patch embedding and blocks, then merger) makes the merger the
+ * trainable source: its backward stops at its own LayerNorm, nothing before it runs
+ * a backward, and their d_w entries are not touched. */
 int ref_encoder_f64(const ref_cfg* c, const double* w, const double* patches,
                     const int32_t* cu_seqlens, int32_t n_seg,
                     const int32_t* grid_thw, int32_t n_items, int32_t trainable,

@@ -186,6 +186,7 @@ __global__ __launch_bounds__(256) void ln_bwd_kernel(const float* dY, int64_t ld
         ab[i].x += dy[i].x; ab[i].y += dy[i].y; ab[i].z += dy[i].z; ab[i].w += dy[i].w;
       }
     }
+    if (!dX) continue;   // affine gradients only (no input gradient wanted)
     s1 = warp_sum(s1) / (float)n;
     s2 = warp_sum(s2) / (float)n;
 #pragma unroll

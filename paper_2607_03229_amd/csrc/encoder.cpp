@@ -341,10 +341,12 @@ mpipe_status forward(Ctx& x, const void* patches, void* merged, char* tape) {
   const Cfg& c = x.c;
   const Plan& P = x.P;
   const int64_t N = P.N, h = c.hidden, m = c.mlp, H = c.llm, E = x.E;
-  const bool tr = P.trainable;
+  const bool tr = P.mode == MODE_TRAINED;     // every layer records its activations
+  const bool mt = P.mode != MODE_FROZEN;      // the merger records its inputs
   char* base = tr ? tape : x.ws;
+  char* mbase = mt ? tape : x.ws;
   auto act = [&](int l) -> const ActSet& { return tr ? P.tape_act[l] : P.ws_act; };
-  const MergerSet& MS = tr ? P.tape_mrg : P.ws_mrg;
+  const MergerSet& MS = mt ? P.tape_mrg : P.ws_mrg;
   const int32_t* pos = reinterpret_cast<const int32_t*>(x.ws + P.ws_pos);
   const float* freq = reinterpret_cast<const float*>(x.ws + P.ws_rope);
 
@@ -352,12 +354,12 @@ mpipe_status forward(Ctx& x, const void* patches, void* merged, char* tape) {
   const void *Xp, *Wpe;
   int64_t ldx;
   pe_operands(x, patches, Xp, Wpe, ldx);
-  const size_t h0 = c.layers > 0 ? act(0).hin : MS.hfin;
+  char* h0 = c.layers > 0 ? base + act(0).hin : mbase + MS.hfin;
   {
     const void* wt[1];
     const int64_t of[1] = {h}, inf[1] = {c.kp}, ld[1] = {ldx};
     MP_RET(weights_t(x, 1, &Wpe, of, inf, ld, wt));
-    GemmArgs a = ga(Xp, ldx, wt[0], h, N, h, c.kp, base + h0, h);
+    GemmArgs a = ga(Xp, ldx, wt[0], h, N, h, c.kp, h0, h);
     a.bias = x.W(P_PE_B);
     MP_RET(gemm_call(x, GEMM_NN, EPI_RESID, a));
   }
@@ -365,7 +367,10 @@ mpipe_status forward(Ctx& x, const void* patches, void* merged, char* tape) {
     const ActSet& S = act(l);
     float* hin = reinterpret_cast<float*>(base + S.hin);
     float* hmid = reinterpret_cast<float*>(base + S.hmid);
-    float* hout = reinterpret_cast<float*>(base + (tr ? S.hout : S.hin));
+    // (with only the merger trainable, the last layer writes the merger's tape input)
+    float* hout = reinterpret_cast<float*>(
+        P.mode == MODE_MERGER && l == c.layers - 1 ? mbase + MS.hfin
+                                                   : base + (tr ? S.hout : S.hin));
     char* A = base + S.a;
     char* qkv = base + S.qkv;
     char* O = base + S.o;
@@ -430,8 +435,8 @@ mpipe_status forward(Ctx& x, const void* patches, void* merged, char* tape) {
     }
   }
   // 2x2 merger: LN, the four window rows side by side ([Tm][4h] view), fc1+GELU, fc2
-  char* Z = base + MS.z;
-  char* Gm = base + MS.gm;
+  char* Z = mbase + MS.z;
+  char* Gm = mbase + MS.gm;
   const void* wtm[2];
   {
     const void* W[2] = {x.W(merger_param(c, M_FC1W)), x.W(merger_param(c, M_FC2W))};
@@ -439,15 +444,15 @@ mpipe_status forward(Ctx& x, const void* patches, void* merged, char* tape) {
     MP_RET(weights_t(x, 2, W, of, inf, inf, wtm));
   }
   MP_CHECK(run(x.e, x.s, "layernorm", 0, [&] {
-    return layernorm_fwd(x.dt, reinterpret_cast<float*>(base + MS.hfin), h, N, (int)h,
+    return layernorm_fwd(x.dt, reinterpret_cast<float*>(mbase + MS.hfin), h, N, (int)h,
                          x.W(merger_param(c, M_LNG)), x.W(merger_param(c, M_LNB)), c.eps, Z, h,
-                         reinterpret_cast<float*>(base + MS.meanz),
-                         reinterpret_cast<float*>(base + MS.rstdz), x.s);
+                         reinterpret_cast<float*>(mbase + MS.meanz),
+                         reinterpret_cast<float*>(mbase + MS.rstdz), x.s);
   }));
   {
     GemmArgs a = ga(Z, 4 * h, wtm[0], 4 * h, P.Tm, 4 * h, 4 * h, Gm, 4 * h);
     a.bias = x.W(merger_param(c, M_FC1B));
-    a.C2 = tr ? base + MS.um : nullptr;
+    a.C2 = mt ? mbase + MS.um : nullptr;
     a.ldc2 = 4 * h;
     MP_RET(gemm_call(x, GEMM_NN, EPI_GELU, a));
   }
@@ -481,10 +486,15 @@ mpipe_status backward(Ctx& x, const void* patches, const char* tape, const void*
   float* part = reinterpret_cast<float*>(x.ws + P.ws_part);
   const int64_t part_half = kPartialRowsMax * std::max({3 * h, m, 4 * h, H, (int64_t)c.kpe});
 
-  MP_RET(pad_pe(x, patches));
-  const void *Xp, *Wpe;
-  int64_t ldx;
-  pe_operands(x, patches, Xp, Wpe, ldx);
+  // Only the merger trainable: it is the trainable source (Lemma 1 applied to the
+  // encoder's parts), so its backward ends with its own LayerNorm's affine gradients.
+  const bool merger_only = P.mode == MODE_MERGER;
+  const void *Xp = nullptr, *Wpe = nullptr;
+  int64_t ldx = 0;
+  if (!merger_only) {
+    MP_RET(pad_pe(x, patches));
+    pe_operands(x, patches, Xp, Wpe, ldx);
+  }
 
   // Weight and bias gradients feed nothing else in the backward: they run on the side
   // stream (x.s2), which forks off after each gradient buffer is produced; the caller's
@@ -512,10 +522,12 @@ mpipe_status backward(Ctx& x, const void* patches, const char* tape, const void*
     return layernorm_bwd(x.dt, dx32, h, reinterpret_cast<const float*>(base + MS.hfin), h,
                          reinterpret_cast<const float*>(base + MS.meanz),
                          reinterpret_cast<const float*>(base + MS.rstdz),
-                         x.W(merger_param(c, M_LNG)), N, (int)h, nullptr, dh, dht, part,
+                         x.W(merger_param(c, M_LNG)), N, (int)h, nullptr,
+                         merger_only ? nullptr : dh, merger_only ? nullptr : dht, part,
                          part + part_half, x.grad(dw, merger_param(c, M_LNG)),
                          x.grad(dw, merger_param(c, M_LNB)), x.s);
   }));
+  if (merger_only) return MPIPE_OK;
 
   for (int l = c.layers - 1; l >= 0; --l) {
     const ActSet& S = P.tape_act[l];
@@ -692,7 +704,7 @@ mpipe_status mpipe_encoder_sizes(const mpipe_encoder* e, const int32_t* cu, int3
   MP_RET(check_handle(e));
   Plan P;
   std::string err;
-  const int rc = build_plan(e->cfg, cu, n_seg, thw, n_items, trainable != 0, P, err);
+  const int rc = build_plan(e->cfg, cu, n_seg, thw, n_items, trainable, P, err);
   if (rc) return fail((mpipe_status)rc, err);
   if (ws_bytes) *ws_bytes = P.ws_bytes;
   if (tape_bytes) *tape_bytes = P.tape_bytes;
@@ -708,7 +720,7 @@ mpipe_status mpipe_encoder_fwd(mpipe_encoder* e, const void* weights, const void
   MP_RET(check_handle(e));
   Plan P;
   std::string err;
-  const int rc = build_plan(e->cfg, cu, n_seg, thw, n_items, trainable != 0, P, err);
+  const int rc = build_plan(e->cfg, cu, n_seg, thw, n_items, trainable, P, err);
   if (rc) return fail((mpipe_status)rc, err);
   if (P.N == 0) return MPIPE_OK;
   if (!weights || !patches || !merged) return fail(MPIPE_ERR_INVALID_ARG, "null device buffer");
@@ -731,11 +743,15 @@ mpipe_status mpipe_encoder_bwd(mpipe_encoder* e, const void* weights, const void
                                size_t tape_bytes, const void* d_merged, float* d_weights,
                                void* d_patches, void* ws, size_t ws_bytes, void* stream) {
   MP_RET(check_handle(e));
-  if (!trainable) return fail(MPIPE_NOOP_FROZEN, "frozen encoder: no backward (Lemma 1)");
+  if (trainable == MODE_FROZEN)
+    return fail(MPIPE_NOOP_FROZEN, "frozen encoder: no backward (Lemma 1)");
   Plan P;
   std::string err;
-  const int rc = build_plan(e->cfg, cu, n_seg, thw, n_items, true, P, err);
+  const int rc = build_plan(e->cfg, cu, n_seg, thw, n_items, trainable, P, err);
   if (rc) return fail((mpipe_status)rc, err);
+  if (P.mode == MODE_MERGER && d_patches)
+    return fail(MPIPE_ERR_INVALID_ARG,
+                "only the merger is trainable: it sends nothing upstream, d_patches must be NULL");
   if (P.N == 0) return MPIPE_OK;
   if (!weights || !patches || !d_merged || !d_weights)
     return fail(MPIPE_ERR_INVALID_ARG, "null device buffer");

@@ -71,7 +71,8 @@ hipError_t layernorm_fwd(int dtype, const float* X, int64_t ldx, int64_t rows, i
                          const void* g, const void* b, float eps, void* Y, int64_t ldy,
                          float* mean, float* rstd, hipStream_t s);
 int64_t layernorm_bwd_partial_rows(int64_t rows);
-// dX, dres and dXt use the row stride ldx of X.
+// dX, dres and dXt use the row stride ldx of X.  dX == nullptr computes only the affine
+// gradients (dXt and dres are then ignored).
 hipError_t layernorm_bwd(int dtype, const float* dY, int64_t ldd, const float* X, int64_t ldx,
                          const float* mean, const float* rstd, const void* g, int64_t rows, int n,
                          const float* dres, float* dX, void* dXt, float* part_g, float* part_b,

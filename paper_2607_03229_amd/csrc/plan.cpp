@@ -128,9 +128,14 @@ GemmSplit choose_split(int64_t M, int64_t N, int64_t K) {
 }
 
 int build_plan(const Cfg& c, const int32_t* cu, int n_seg, const int32_t* thw, int n_items,
-               bool trainable, Plan& p, std::string& err) {
+               int mode, Plan& p, std::string& err) {
   p = Plan();
-  p.trainable = trainable;
+  if (mode != MODE_FROZEN && mode != MODE_TRAINED && mode != MODE_MERGER) {
+    err = "trainable must be 0 (frozen), 1 (trained) or 2 (merger only)";
+    return -1;
+  }
+  p.mode = mode;
+  p.trainable = mode == MODE_TRAINED;
   if (n_items < 0 || n_seg < 0) {
     err = "negative item or segment count";
     return -1;
@@ -278,10 +283,11 @@ int build_plan(const Cfg& c, const int32_t* cu, int n_seg, const int32_t* thw, i
     s.gm = a.take((size_t)Tm * 4 * h * E);
     return s;
   };
-  if (!trainable) {
+  if (mode != MODE_TRAINED) {   // blocks without a tape: activations shared by all layers
     p.ws_act = act_set(ws, false, true);
     p.ws_mrg = merger_set(ws, p.ws_act.hin, false);
-  } else {
+  }
+  if (mode != MODE_FROZEN) {
     // backward scratch
     p.ws_dh = ws.take((size_t)N * h * 4);
     p.ws_dht = ws.take((size_t)N * h * E);
@@ -315,7 +321,11 @@ int build_plan(const Cfg& c, const int32_t* cu, int n_seg, const int32_t* thw, i
   p.ws_bytes = ws.top;
 
   // ---- tape ----
-  if (trainable) {
+  if (mode == MODE_MERGER) {   // the merger's inputs only: the blocks run no backward
+    Arena tp;
+    p.tape_mrg = merger_set(tp, tp.take((size_t)N * h * 4), true);
+    p.tape_bytes = tp.top;
+  } else if (mode == MODE_TRAINED) {
     Arena tp;
     p.tape_act.resize(c.layers);
     size_t h_in = tp.take((size_t)N * h * 4);

@@ -69,10 +69,15 @@ struct GemmSplit {
 };
 GemmSplit choose_split(int64_t M, int64_t N, int64_t K);
 
+// Trainability modes (the C ABI's mpipe_train_mode): nothing, everything, or only the
+// merger trainable.
+enum { MODE_FROZEN = 0, MODE_TRAINED = 1, MODE_MERGER = 2 };
+
 struct Plan {
   int64_t N = 0, Tm = 0;
   int n_items = 0, n_seg = 0;
-  bool trainable = false;
+  int mode = MODE_FROZEN;
+  bool trainable = false;          // mode == MODE_TRAINED: every layer records a tape
   int64_t sum_len2 = 0;          // sum over segments of len^2 (attention FLOPs)
   // host metadata, uploaded into the workspace head
   std::vector<int32_t> pos;        // N: y << 16 | x
@@ -89,7 +94,7 @@ struct Plan {
   size_t ws_dh = 0, ws_dht = 0, ws_dhm = 0, ws_dhmt = 0, ws_dx32 = 0, ws_du = 0, ws_do = 0,
          ws_delta = 0, ws_dqkv = 0, ws_part = 0, ws_cpart = 0, ws_dwpart = 0;
   size_t ws_bytes = 0;
-  // tape layout (trainable)
+  // tape layout: every layer and the merger (MODE_TRAINED), the merger only (MODE_MERGER)
   std::vector<ActSet> tape_act;
   MergerSet tape_mrg{};
   size_t tape_bytes = 0;
@@ -98,9 +103,9 @@ struct Plan {
 // (cos, sin) table of the rotary angles p * theta^(-4k/d) for p < positions, k < d/4.
 std::vector<float> rope_table(const Cfg& c, int positions);
 
-// Validate metadata and build the plan.  Returns 0 or a negative mpipe_status;
-// `err` receives the reason.
+// Validate metadata and build the plan for a trainability mode (MODE_*).  Returns 0 or
+// a negative mpipe_status; `err` receives the reason.
 int build_plan(const Cfg& c, const int32_t* cu, int n_seg, const int32_t* thw, int n_items,
-               bool trainable, Plan& p, std::string& err);
+               int mode, Plan& p, std::string& err);
 
 }  // namespace mpipe

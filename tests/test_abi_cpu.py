@@ -143,3 +143,31 @@ def test_gemm_op_argument_checks(L):
                            None, 0, 0, 0, 0, None) == -1
     assert L.mpipe_op_gemm(1, 3, 0, 16, 16, 16, fake, 16, fake, 16, fake, 16, None, None, 0,
                            None, 0, 0, 0, 0, None) == -1
+
+
+def test_merger_only_mode_host_side(L):
+    """Trainability modes on the host: the merger-only tape holds the merger's inputs
+    only (far smaller than the full tape, larger than nothing), an unknown mode is
+    rejected, and the merger as trainable source refuses to send a patch gradient."""
+    wl = W.make_workload("c4_qwen2vl_trained", 0)
+    enc = B.Encoder(wl.cfg)
+    full = enc.sizes(wl.cu_seqlens, wl.grid_thw, 1)
+    part = enc.sizes(wl.cu_seqlens, wl.grid_thw, 2)
+    N, h, Tm = wl.n_patches, wl.cfg.hidden, wl.n_merged
+    # final residual (fp32), LN output (bf16), LN stats, GELU' and GELU of fc1 (bf16)
+    expect = N * h * 4 + N * h * 2 + 2 * N * 4 + 2 * Tm * 4 * h * 2
+    assert expect <= part["tape"] <= expect + 4 * 256
+    assert part["tape"] * 20 < full["tape"]
+    assert part["n_merged"] == full["n_merged"]
+    for bad in (3, -1):
+        with pytest.raises(B.MpipeError) as e:
+            enc.sizes(wl.cu_seqlens, wl.grid_thw, bad)
+        assert e.value.status == -1
+    fake = C.c_void_p(0x1000)
+    cu = np.ascontiguousarray(wl.cu_seqlens, np.int32)
+    g = np.ascontiguousarray(wl.grid_thw, np.int32)
+    rc = L.mpipe_encoder_bwd(enc._h, fake, fake, cu.ctypes.data_as(C.c_void_p), len(cu) - 1,
+                             g.ctypes.data_as(C.c_void_p), g.shape[0], 2, fake, part["tape"],
+                             fake, fake, fake, fake, part["workspace"], None)
+    assert rc == -1 and "d_patches" in B.last_error()
+    enc.close()

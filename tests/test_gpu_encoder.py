@@ -244,3 +244,89 @@ def test_full_depth_gradients_one_item():
     dM = W.round_bf16(rng.standard_normal((wl.n_merged, cfg.llm_hidden)).astype(np.float32))
     _check_full(cfg, wl.weights(), wl.patches(), wl.cu_seqlens, wl.grid_thw, dM, TOL["bf16"],
                 "c4-shape one item")
+
+
+# ---------------------------------------------------------------------------
+# only the merger trainable (mpipe_train_mode MPIPE_TRAIN_MERGER)
+# ---------------------------------------------------------------------------
+
+MERGER_ONLY = 2
+
+
+def _merger_slice(cfg):
+    off, lo = 0, None
+    for name, shape, _ in W.param_table(cfg):
+        if name.startswith("merger.") and lo is None:
+            lo = off
+        off += int(np.prod(shape))
+    return slice(lo, off)
+
+
+def _check_merger_only(cfg, w, X, cu, grid, dM, tol, label):
+    """The merger is the trainable source: its gradients match the oracle, every other
+    entry of d_weights keeps its bits, the forward is the frozen one bit for bit, and no
+    patch gradient can be asked for."""
+    import paper_2607_03229_amd as mp
+    announce(f"merger-only fwd+bwd {label} N={len(X)}")
+    ms = _merger_slice(cfg)
+    init = np.full(w.shape, 7.25, np.float32)
+    init[ms] = 0.0
+    g = GpuRun(cfg, w, X, cu, grid)
+    out = g.run(MERGER_ONLY, d_merged=dM, dw_init=init)
+    frozen = g.run(False)
+    assert out["status"] == 0
+    assert g.torch.equal(out["merged"], frozen["merged"])
+    dw = host(out["dw"])
+    np.testing.assert_array_equal(dw[:ms.start], init[:ms.start])
+    rc, rM, rdw, _ = oracle.encoder(cfg, w, X, cu, grid, MERGER_ONLY, d_merged=dM)
+    assert rc == 0
+    em = max_rel(host(out["merged"]), rM)
+    assert em < tol, f"merged max-rel {em}"
+    errs = {k: v for k, v in _per_tensor_errors(cfg, dw, rdw).items() if k.startswith("merger.")}
+    worst = max(errs, key=errs.get)
+    assert errs[worst] < tol, f"merger d_weights worst {worst}: {errs[worst]}"
+    with pytest.raises(mp.MpipeError) as e:
+        g.run(MERGER_ONLY, d_merged=dM, want_dx=True)
+    assert e.value.status == -1
+    print(f"{label} merger-only: merged {em:.2e}  merger d_w worst {worst} {errs[worst]:.2e}")
+
+
+def test_merger_only_tiny_fp32():
+    wl = W.make_workload("c1_tiny_fp32", 1)
+    _check_merger_only(wl.cfg, wl.weights(), wl.patches(), wl.cu_seqlens, wl.grid_thw,
+                       wl.d_merged(), TOL["f32"], "c1")
+
+
+def test_merger_only_small_bf16():
+    cfg, wl, dM = _small_problem("d80", seed=2)
+    _check_merger_only(cfg, wl.weights(), wl.patches(), wl.cu_seqlens, wl.grid_thw, dM,
+                       TOL["bf16"], "small-d80")
+
+
+def test_merger_only_full_depth_one_item():
+    cfg = W.CONFIGS["c4_qwen2vl_trained"].cfg
+    wl = W.make_workload("c4_qwen2vl_trained", 0, grid_thw=np.array([[1, 16, 16]]))
+    rng = np.random.default_rng(10)
+    dM = W.round_bf16(rng.standard_normal((wl.n_merged, cfg.llm_hidden)).astype(np.float32))
+    _check_merger_only(cfg, wl.weights(), wl.patches(), wl.cu_seqlens, wl.grid_thw, dM,
+                       TOL["bf16"], "c4-shape one item")
+
+
+def test_merger_only_equals_full_backward_on_merger_full_size():
+    """On the full Qwen2-VL-shaped micro-batch (the benchmark's launch configuration),
+    the merger's gradients do not depend on whether the blocks train: bitwise the
+    merger entries of the full backward."""
+    wl = W.make_workload("c4_qwen2vl_trained", 0)
+    cfg = wl.cfg
+    w, X, dM = wl.weights(), wl.patches(), wl.d_merged()
+    announce(f"merger-only vs trained, full size N={wl.n_patches}")
+    ms = _merger_slice(cfg)
+    g = GpuRun(cfg, w, X, wl.cu_seqlens, wl.grid_thw)
+    part = g.run(MERGER_ONLY, d_merged=dM)
+    part_dw = host(part["dw"])
+    del part
+    full = g.run(True, d_merged=dM)
+    full_dw = host(full["dw"])
+    np.testing.assert_array_equal(part_dw[ms], full_dw[ms])
+    assert not part_dw[:ms.start].any()
+    assert np.isfinite(part_dw[ms]).all() and part_dw[ms].any()

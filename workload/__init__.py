@@ -100,7 +100,7 @@ class EncoderConfig:
 class WorkloadSpec:
     name: str
     cfg: EncoderConfig
-    trainable: bool
+    trainable: int                  # 0 frozen, 1 every part trainable, 2 only the merger
     # image sizes: ("choice", values) | ("uniform28", lo, hi) | ("loguniform28", lo, hi)
     image_sizes: tuple
     n_images: int                   # fixed count, or -1 for budget-driven draws
@@ -131,6 +131,10 @@ CONFIGS: Dict[str, WorkloadSpec] = {
     "c4_qwen2vl_trained": WorkloadSpec("c4_qwen2vl_trained", _QWEN, True,
                                        ("loguniform28", 224, 1344), 24,
                                        emb_seqs=8, emb_seq_len=8192),
+    # the same micro-batch with only the merger (projector) trainable: frozen blocks
+    "c4_qwen2vl_merger": WorkloadSpec("c4_qwen2vl_merger", _QWEN, 2,
+                                      ("loguniform28", 224, 1344), 24,
+                                      emb_seqs=8, emb_seq_len=8192),
 }
 for _f, _tag in ((0.0, "f0"), (0.5, "f05"), (1.0, "f1")):
     for _tr in (False, True):
@@ -252,8 +256,9 @@ class Workload:
         return self.spec.name
 
     @property
-    def trainable(self) -> bool:
-        return self.spec.trainable
+    def trainable(self) -> int:
+        """Trainability mode: 0 frozen, 1 every part trainable, 2 only the merger."""
+        return int(self.spec.trainable)
 
     @property
     def n_items(self) -> int:
