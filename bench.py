@@ -215,6 +215,40 @@ def cpu_baseline(sample_layers: int = 8):
             "cpu": _cpu_model()}
 
 
+def owner_scenario(enc, wl, flops_per_s: float) -> dict:
+    """The ByMicrobatch owner on encode costs of this workload: 16 micro-batches (seeds
+    0..15 of the same size draw), each costed by the roofline model at the FLOP rate this
+    run measured, assigned to 8 pipeline ranks whose warmup bubbles follow a 1F1B fill,
+    w_r = r * (median encode) / 2, i.e. an LLM stage forward half as long as a median
+    encode (tight enough that some encode work spills); greedy, refined and exact owners."""
+    import paper_2607_03229_amd as mp
+    import workload as W
+    costs = []
+    for seed in range(16):
+        d = W.make_workload(wl.name, seed)
+        c = enc.cost(d.cu_seqlens, d.grid_thw, wl.trainable, flops_per_s, PEAK_HBM_GBPS * 1e9)
+        costs.append(c["fwd_seconds"])
+    costs = np.array(costs)
+    step = float(np.median(costs))
+    warm = 0.5 * step * np.arange(8, dtype=np.float64)
+    out = {"n_microbatches": len(costs), "n_ranks": 8,
+           "warmup": "w_r = r * median encode / 2 (1F1B fill)",
+           "rate_tflops": round(flops_per_s / 1e12, 1),
+           "encode_ms_min_median_max": [round(1e3 * float(v), 3)
+                                        for v in (costs.min(), step, costs.max())]}
+    for name, method in (("greedy", mp.OWNER_GREEDY), ("refined", mp.OWNER_REFINED),
+                         ("exact", mp.OWNER_EXACT)):
+        t0 = time.perf_counter()
+        try:
+            _, _, worst = mp.owner_map(costs, warm, method)
+        except mp.MpipeError:   # the exact search's node budget
+            worst = None
+        out[f"{name}_us"] = round(1e6 * (time.perf_counter() - t0), 1)
+        out[f"{name}_max_spill_ms"] = None if worst is None else round(1e3 * worst, 3)
+    out["spill_if_all_on_rank0_ms"] = round(1e3 * float(costs.sum()), 3)
+    return out
+
+
 def _cpu_model() -> str:
     try:
         for line in open("/proc/cpuinfo"):
@@ -381,6 +415,7 @@ def main():
         "roofline": roofline,
         "kernels": kernels,
     }
+    result["owner_map"] = owner_scenario(enc, wl, flops / (ms_step * 1e-3))
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on its bounded sample")
         result["cpu_baseline"] = cpu_baseline()

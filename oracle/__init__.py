@@ -280,3 +280,29 @@ def merge_gather(d_emb: np.ndarray, idx: np.ndarray) -> np.ndarray:
     if rc:
         raise ValueError("index out of range or repeated")
     return out
+
+
+# --------------------------------------------------------------------------
+# ByMicrobatch owner (cost model, Sec. 4.3) -- plain Python by the definition
+# --------------------------------------------------------------------------
+
+def owner_spill(owner, cost, warmup):
+    """spill_r = max(0, E_r - w_r) with E_r the summed cost of the micro-batches rank r
+    owns (added in index order); returns (per-rank spill list, the step's max_r spill_r)."""
+    E = [0.0] * len(warmup)
+    for m, r in enumerate(owner):
+        E[int(r)] += float(cost[m])
+    spill = [max(0.0, E[r] - float(warmup[r])) for r in range(len(warmup))]
+    return spill, max(spill, default=0.0)
+
+
+def owner_bruteforce(cost, warmup):
+    """The ByMicrobatch owner by its definition: among all n_ranks ** n_mb assignments,
+    one that minimises max_r spill_r (tiny inputs only).  Returns (owner, max spill)."""
+    import itertools
+    best = None
+    for owner in itertools.product(range(len(warmup)), repeat=len(cost)):
+        s = owner_spill(owner, cost, warmup)[1]
+        if best is None or s < best[1]:
+            best = (list(owner), s)
+    return best

@@ -11,4 +11,5 @@ from ._binding import (  # noqa: F401
     op_gemm, op_layernorm_fwd, op_layernorm_bwd, op_rope, op_attention_fwd,
     op_attention_bwd, op_scratch_bytes,
     F32, BF16, OK, NOOP_FROZEN,
+    owner_map, OWNER_GREEDY, OWNER_EXACT, OWNER_REFINED,
 )

@@ -81,6 +81,8 @@ def load():
         "mpipe_op_attention_fwd": (st, [i32, P, i64, i32, i32, P, i32, P, P, P, sz, P]),
         "mpipe_op_attention_bwd": (st, [i32, P, P, P, P, i64, i32, i32, P, i32, P, P, sz, P]),
         "mpipe_op_scratch_bytes": (sz, [i64, i32, i32, i32]),
+        "mpipe_encoder_cost": (st, [P, P, i32, P, i32, i32, C.c_double, C.c_double, P]),
+        "mpipe_owner_map": (st, [P, i32, P, i32, i32, P, P, P]),
     }
     for name, (res, args) in sig.items():
         f = getattr(L, name)
@@ -193,6 +195,19 @@ class Encoder:
             int(trainable), _ptr(tape), tb, _ptr(d_merged), _ptr(d_weights), _ptr(d_patches),
             _ptr(workspace), wb, _stream(stream)), allow=(OK, NOOP_FROZEN))
 
+    # -- cost model --
+    def cost(self, cu_seqlens, grid_thw, trainable, flops_per_second: float,
+             bytes_per_second: float) -> Dict[str, float]:
+        """W, D and the roofline seconds of this micro-batch's forward and backward slabs."""
+        cu, cup = _host_i32(cu_seqlens)
+        g, gp = _host_i32(np.asarray(grid_thw).reshape(-1, 3))
+        out = (C.c_double * 6)()
+        _check(self.L.mpipe_encoder_cost(self._h, cup, max(len(cu) - 1, 0), gp, g.shape[0],
+                                         int(trainable), float(flops_per_second),
+                                         float(bytes_per_second), out))
+        keys = ("fwd_flops", "fwd_bytes", "fwd_seconds", "bwd_flops", "bwd_bytes", "bwd_seconds")
+        return dict(zip(keys, list(out)))
+
     def set_side_stream(self, enable: bool):
         """Backward weight-gradient work on the handle's internal stream (default) or not."""
         _check(self.L.mpipe_encoder_set_side_stream(self._h, int(enable)))
@@ -228,6 +243,23 @@ def _dt(t) -> int:
     if t.dtype == torch.float32:
         return F32
     raise MpipeError(-1, f"unsupported dtype {t.dtype}")
+
+
+OWNER_GREEDY, OWNER_EXACT, OWNER_REFINED = 0, 1, 2
+
+
+def owner_map(cost, warmup, method: int = OWNER_GREEDY):
+    """ByMicrobatch owner: (owner [n_mb] int32, spill [n_ranks], max spill)."""
+    c = np.ascontiguousarray(cost, dtype=np.float64)
+    w = np.ascontiguousarray(warmup, dtype=np.float64)
+    owner = np.zeros(c.shape[0], np.int32)
+    spill = np.zeros(w.shape[0], np.float64)
+    worst = C.c_double()
+    _check(load().mpipe_owner_map(c.ctypes.data_as(C.c_void_p), c.shape[0],
+                                  w.ctypes.data_as(C.c_void_p), w.shape[0], int(method),
+                                  owner.ctypes.data_as(C.c_void_p),
+                                  spill.ctypes.data_as(C.c_void_p), C.byref(worst)))
+    return owner, spill, worst.value
 
 
 def merge_scatter(merged, placeholder_idx, embeds, stream=None) -> None:

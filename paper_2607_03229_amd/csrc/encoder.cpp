@@ -2,6 +2,7 @@
 // encoder forward / backward on the caller's stream.  See include/mpipe.h.
 #include "../../include/mpipe.h"
 #include "../../include/mpipe_ops.h"
+#include "../../include/mpipe_sched.h"
 
 #include <hip/hip_runtime.h>
 
@@ -710,6 +711,26 @@ mpipe_status mpipe_encoder_sizes(const mpipe_encoder* e, const int32_t* cu, int3
   if (tape_bytes) *tape_bytes = P.tape_bytes;
   if (n_merged) *n_merged = P.Tm;
   if (n_patches) *n_patches = P.N;
+  return MPIPE_OK;
+}
+
+mpipe_status mpipe_encoder_cost(const mpipe_encoder* e, const int32_t* cu, int32_t n_seg,
+                                const int32_t* thw, int32_t n_items, int32_t trainable,
+                                double flops_per_s, double bytes_per_s, mpipe_slab_cost* out) {
+  MP_RET(check_handle(e));
+  if (!out || !(flops_per_s > 0) || !(bytes_per_s > 0))
+    return fail(MPIPE_ERR_INVALID_ARG, "need an output and rates > 0");
+  Plan P;
+  std::string err;
+  const int rc = build_plan(e->cfg, cu, n_seg, thw, n_items, trainable, P, err);
+  if (rc) return fail((mpipe_status)rc, err);
+  const SlabCost sc = encoder_slab_cost(e->cfg, P);
+  out->fwd_flops = sc.fwd_flops;
+  out->fwd_bytes = sc.fwd_bytes;
+  out->fwd_seconds = std::max(sc.fwd_flops / flops_per_s, sc.fwd_bytes / bytes_per_s);
+  out->bwd_flops = sc.bwd_flops;
+  out->bwd_bytes = sc.bwd_bytes;
+  out->bwd_seconds = std::max(sc.bwd_flops / flops_per_s, sc.bwd_bytes / bytes_per_s);
   return MPIPE_OK;
 }
 

@@ -100,6 +100,13 @@ struct Plan {
   size_t tape_bytes = 0;
 };
 
+// W (FLOPs) and D (algorithmic HBM bytes) of one micro-batch's forward and backward
+// slabs in the plan's trainability mode (owner.cpp).
+struct SlabCost {
+  double fwd_flops = 0, fwd_bytes = 0, bwd_flops = 0, bwd_bytes = 0;
+};
+SlabCost encoder_slab_cost(const Cfg& c, const Plan& P);
+
 // (cos, sin) table of the rotary angles p * theta^(-4k/d) for p < positions, k < d/4.
 std::vector<float> rope_table(const Cfg& c, int positions);
 
