@@ -27,7 +27,10 @@ namespace {
 constexpr int NTHR = 256;
 // 16-row sub-tiles per wave (NS) of the bf16 kernels; a 128-row work tile takes 8 / NS
 // waves.  NS = 4 reuses each LDS fragment over four MFMAs (half the LDS traffic of NS = 2)
-// at one wave per SIMD; NS = 2 runs two blocks of four waves per CU.
+// at one wave per SIMD; NS = 2 runs several blocks of four waves per CU: three for the
+// forward and dQ kernels (two-stage tile rings, 48 KB of LDS and at most 168 registers per
+// wave; measured 7.5 % and 1 % faster than two blocks with three-stage rings), two for
+// dK/dV (three-stage ring, over 200 registers).
 constexpr int FWD_NS = 2, DQ_NS = 2, DKDV_NS = 2;
 
 template <int D> struct AD {
@@ -200,17 +203,18 @@ __device__ __forceinline__ bf16x8 frag_trt(const uint4* tile, int k0a, int k0b, 
 }
 
 // ---- forward ----------------------------------------------------------------------
-// 3-stage pipeline over 64-key tiles: tile t+2 is in flight while tile t is used.
+// 2-stage pipeline over 64-key tiles: tile t+1 is in flight while tile t is used, and
+// the other two blocks on the CU cover what one tile of lookahead leaves exposed.
 // The softmax offset m of a query (log2 domain) moves only when the tile's maximum
 // exceeds it by more than kRescaleLog2: weights exp2(s - m) then stay below 2^8, exact in
 // fp32 and as representable in bf16 as any weight <= 1, and the output rescale (a
 // multiply per accumulator) runs on a few tiles instead of most.  Row sums of the bf16
 // weights come from the PV MFMAs themselves, with a ones operand in place of V.
 template <int D, int NS>
-__global__ __launch_bounds__(64 * (8 / NS), NS == 2 ? 2 : 1) void attn_fwd_kernel(AttnArgs p) {
+__global__ __launch_bounds__(64 * (8 / NS), NS == 2 ? 3 : 1) void attn_fwd_kernel(AttnArgs p) {
   constexpr int NW = 8 / NS, RW = 16 * NS;   // waves per block, rows per wave
   constexpr int NDT = AD<D>::NDT, SL = TG<D, NW>::SLOTS, NI = TG<D, NW>::NI;
-  __shared__ uint4 k0s[SL], k1s[SL], k2s[SL], v0s[SL], v1s[SL], v2s[SL];
+  __shared__ uint4 k0s[SL], k1s[SL], v0s[SL], v1s[SL];
   const int work = blockIdx.x / p.heads, head = blockIdx.x % p.heads;
   const int4 wk = p.work[work];
   const int q0 = wk.x, s0 = wk.y, s1 = wk.z;
@@ -258,8 +262,7 @@ __global__ __launch_bounds__(64 * (8 / NS), NS == 2 ? 2 : 1) void attn_fwd_kerne
   };
   auto body = [&](int t, const uint4* kt_s, const uint4* vt_s, uint4* kn, uint4* vn)
       __attribute__((always_inline)) {
-    if (t + 1 < nt) wait_vm<2 * NI>();
-    else wait_vm<0>();
+    wait_vm<0>();
     lds_barrier();
     const int k0 = s0 + 64 * t;
     f32x4 s[4][NS];
@@ -270,7 +273,7 @@ __global__ __launch_bounds__(64 * (8 / NS), NS == 2 ? 2 : 1) void attn_fwd_kerne
         s[kq][qs] = dot_d<D>(kt_s, 16 * kq + r, qf[qs], g, f32x4{0.f, 0.f, 0.f, 0.f});
     // the next DMAs go out after the score MFMAs, not ahead of their fragment reads
     // (measured 3% faster on the Qwen2-VL segment mix)
-    issue(t + 2, kn, vn);
+    issue(t + 1, kn, vn);
     if (k0 + 64 > s1) {   // ragged last tile: keys past the segment never win or weigh
 #pragma unroll
       for (int kq = 0; kq < 4; ++kq)
@@ -327,11 +330,9 @@ __global__ __launch_bounds__(64 * (8 / NS), NS == 2 ? 2 : 1) void attn_fwd_kerne
         osum[qs] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pb[qs][kk], osum[qs], 0, 0, 0);
   };
   issue(0, k0s, v0s);
-  issue(1, k1s, v1s);
-  for (int t = 0; t < nt; t += 3) {
-    body(t, k0s, v0s, k2s, v2s);
+  for (int t = 0; t < nt; t += 2) {
+    body(t, k0s, v0s, k1s, v1s);
     if (t + 1 < nt) body(t + 1, k1s, v1s, k0s, v0s);
-    if (t + 2 < nt) body(t + 2, k2s, v2s, k1s, v1s);
   }
   bf16* O = reinterpret_cast<bf16*>(p.out) + head * D;
 #pragma unroll
@@ -487,10 +488,10 @@ __global__ __launch_bounds__(64 * (8 / NS), NS == 2 ? 2 : 1) void attn_bwd_dkdv_
 
 // ---- backward: dQ (and delta) --------------------------------------------------------
 template <int D, int NS>
-__global__ __launch_bounds__(64 * (8 / NS), NS == 2 ? 2 : 1) void attn_bwd_dq_kernel(AttnArgs p) {
+__global__ __launch_bounds__(64 * (8 / NS), NS == 2 ? 3 : 1) void attn_bwd_dq_kernel(AttnArgs p) {
   constexpr int NW = 8 / NS, RW = 16 * NS;   // waves per block, rows per wave
   constexpr int NDT = AD<D>::NDT, SL = TG<D, NW>::SLOTS, NI = TG<D, NW>::NI;
-  __shared__ uint4 k0s[SL], k1s[SL], k2s[SL], v0s[SL], v1s[SL], v2s[SL];
+  __shared__ uint4 k0s[SL], k1s[SL], v0s[SL], v1s[SL];
   const int work = blockIdx.x / p.heads, head = blockIdx.x % p.heads;
   const int4 wk = p.work[work];
   const int q0 = wk.x, s0 = wk.y, s1 = wk.z;
@@ -549,10 +550,9 @@ __global__ __launch_bounds__(64 * (8 / NS), NS == 2 ? 2 : 1) void attn_bwd_dq_ke
   };
   auto body = [&](int t, const uint4* k_s, const uint4* v_s, uint4* kn, uint4* vn)
       __attribute__((always_inline)) {
-    if (t + 1 < nt) wait_vm<2 * NI>();
-    else wait_vm<0>();
+    wait_vm<0>();
     lds_barrier();
-    issue(t + 2, kn, vn);
+    issue(t + 1, kn, vn);
     const int kb = s0 + 64 * t;
     f32x4 ds[4][NS];
 #pragma unroll
@@ -592,11 +592,9 @@ __global__ __launch_bounds__(64 * (8 / NS), NS == 2 ? 2 : 1) void attn_bwd_dq_ke
     }
   };
   issue(0, k0s, v0s);
-  issue(1, k1s, v1s);
-  for (int t = 0; t < nt; t += 3) {
-    body(t, k0s, v0s, k2s, v2s);
+  for (int t = 0; t < nt; t += 2) {
+    body(t, k0s, v0s, k1s, v1s);
     if (t + 1 < nt) body(t + 1, k1s, v1s, k0s, v0s);
-    if (t + 2 < nt) body(t + 2, k2s, v2s, k1s, v1s);
   }
   bf16* dQ = reinterpret_cast<bf16*>(p.dq) + head * D;
 #pragma unroll
