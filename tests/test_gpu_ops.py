@@ -35,7 +35,8 @@ GEMM_SHAPES = {
     NN: [(300, 200, 256), (129, 264, 72), (77, 8, 520), (600, 264, 136), (777, 1032, 1280),
          (530, 280, 40)],
     TN: [(200, 264, 333), (8, 16, 1), (136, 128, 1000), (520, 264, 1000), (1280, 600, 77),
-         (512, 256, 5), (600, 392, 63), (600, 392, 250), (520, 264, 291)],
+         (512, 256, 5), (600, 392, 63), (600, 392, 250), (520, 264, 291),
+         (1280, 1176, 700)],
 }
 
 
