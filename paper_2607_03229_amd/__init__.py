@@ -12,4 +12,9 @@ from ._binding import (  # noqa: F401
     op_attention_bwd, op_scratch_bytes,
     F32, BF16, OK, NOOP_FROZEN,
     owner_map, OWNER_GREEDY, OWNER_EXACT, OWNER_REFINED,
+    schedule_valid, Derived, EVENT_FIELDS,
+    SK_1F1B, SK_GPIPE, SK_TRANSPOSE, LAYOUT_SHARDED, LAYOUT_REPLICATED,
+    COMM_NONE, COMM_GATHER, COMM_SCATTER, COMM_SEND, COMM_RECVGRAD, GROUP_REPLICA, GROUP_DATA,
+    EV_FWD, EV_BWD, EV_COLL, EV_DPREDUCE, EV_LOSS, EV_STEP_BARRIER,
+    EDGE_ACTIVATION, EDGE_GRADIENT, EDGE_TURNAROUND, EDGE_ACCUMULATE, EDGE_SEQUENCE,
 )

@@ -1,4 +1,4 @@
-"""ctypes binding of libmpipe (include/mpipe.h, include/mpipe_ops.h).
+"""ctypes binding of libmpipe (include/mpipe.h, mpipe_ops.h, mpipe_sched.h, mpipe_derive.h).
 
 Argument marshalling only: torch tensors provide device memory and the current
 HIP stream; every step of the encoder runs in the library's kernels."""
@@ -83,6 +83,17 @@ def load():
         "mpipe_op_scratch_bytes": (sz, [i64, i32, i32, i32]),
         "mpipe_encoder_cost": (st, [P, P, i32, P, i32, i32, C.c_double, C.c_double, P]),
         "mpipe_owner_map": (st, [P, i32, P, i32, i32, P, P, P]),
+        "mpipe_schedule_valid": (st, [P, i32, i32, P]),
+        "mpipe_derive": (st, [P, i32, i32, P, P, i32, i32, P, P]),
+        "mpipe_derived_destroy": (None, [P]),
+        "mpipe_derived_shape": (st, [P, P, P, P, P, P]),
+        "mpipe_derived_placement": (st, [P, i32, P, P, P, P]),
+        "mpipe_derived_owner": (st, [P, P]),
+        "mpipe_derived_lists": (st, [P, P, P, P, P, P]),
+        "mpipe_derived_nodes": (i32, [P, i32, P, i32]),
+        "mpipe_event_costs": (st, [P, P, P, P, P, C.c_double, C.c_double, C.c_double, P]),
+        "mpipe_makespan": (st, [P, P, P, P, P, P]),
+        "mpipe_memory_peak": (st, [P, P, P]),
     }
     for name, (res, args) in sig.items():
         f = getattr(L, name)
@@ -260,6 +271,131 @@ def owner_map(cost, warmup, method: int = OWNER_GREEDY):
                                   owner.ctypes.data_as(C.c_void_p),
                                   spill.ctypes.data_as(C.c_void_p), C.byref(worst)))
     return owner, spill, worst.value
+
+
+# --------------------------------------------------------------------------
+# Schedule algebra (host only)
+# --------------------------------------------------------------------------
+
+SK_1F1B, SK_GPIPE, SK_TRANSPOSE = 0, 1, 2
+LAYOUT_SHARDED, LAYOUT_REPLICATED = 0, 1
+COMM_NONE, COMM_GATHER, COMM_SCATTER, COMM_SEND, COMM_RECVGRAD = -1, 0, 1, 2, 3
+GROUP_REPLICA, GROUP_DATA = 0, 1
+EV_FWD, EV_BWD, EV_COLL, EV_DPREDUCE, EV_LOSS, EV_STEP_BARRIER = 0, 1, 2, 3, 4, 5
+EDGE_ACTIVATION, EDGE_GRADIENT, EDGE_TURNAROUND, EDGE_ACCUMULATE, EDGE_SEQUENCE = 0, 1, 2, 3, 4
+EVENT_FIELDS = ("kind", "region", "rank", "mb", "stage", "comm", "seam", "group")
+
+
+def _vp(a: np.ndarray) -> C.c_void_p:
+    return a.ctypes.data_as(C.c_void_p)
+
+
+def schedule_valid(cut, n_layers: int, schedule) -> Tuple[bool, str]:
+    """(valid, reason) for a (cut, schedule) pair."""
+    c, cp = _host_i32(cut)
+    s, sp = _host_i32(schedule)
+    st = load().mpipe_schedule_valid(cp if c.size else None, s.size, int(n_layers), sp)
+    return st == OK, ("" if st == OK else last_error())
+
+
+class Derived:
+    """derive(cut, schedule, model) read out into numpy arrays.
+
+    layout, runs_bwd: [k]; slab_lo, slab_hi: [k, P]; owner: [M];
+    seams: [k-1, 3] (left, fwd comm, bwd comm); reduces: [n, 2] (region, group);
+    events: [n_events, 8] int32 with columns EVENT_FIELDS; edges: [n_edges, 3]
+    (from, to, kind); nodes: list of P int32 arrays."""
+
+    def __init__(self, cut, n_layers: int, schedule, trainable, n_ranks: int, n_mb: int,
+                 owner=None):
+        self.L = load()
+        c, cp = _host_i32(cut)
+        s, sp = _host_i32(schedule)
+        t, tp = _host_i32(trainable)
+        if t.size != s.size:
+            raise MpipeError(-1, "one trainable bit per region")
+        o, op = (None, None) if owner is None else _host_i32(owner)
+        if o is not None and o.size != n_mb:
+            raise MpipeError(-1, "one owner per micro-batch")
+        h = C.c_void_p()
+        _check(self.L.mpipe_derive(cp if c.size else None, s.size, int(n_layers), sp, tp,
+                                   int(n_ranks), int(n_mb), op, C.byref(h)))
+        self._h = h
+        self.k, self.P, self.M = s.size, int(n_ranks), int(n_mb)
+        ho, ne, nd, ns, nr = (C.c_int32() for _ in range(5))
+        _check(self.L.mpipe_derived_shape(h, C.byref(ho), C.byref(ne), C.byref(nd),
+                                          C.byref(ns), C.byref(nr)))
+        self.has_order = bool(ho.value)
+        self.layout = np.zeros(self.k, np.int32)
+        self.runs_bwd = np.zeros(self.k, np.int32)
+        self.slab_lo = np.zeros((self.k, self.P), np.int32)
+        self.slab_hi = np.zeros((self.k, self.P), np.int32)
+        for j in range(self.k):
+            lay, rb = C.c_int32(), C.c_int32()
+            _check(self.L.mpipe_derived_placement(h, j, C.byref(lay), C.byref(rb),
+                                                  _vp(self.slab_lo[j]), _vp(self.slab_hi[j])))
+            self.layout[j], self.runs_bwd[j] = lay.value, rb.value
+        self.owner = np.zeros(self.M, np.int32)
+        _check(self.L.mpipe_derived_owner(h, _vp(self.owner)))
+        self.events = np.zeros((ne.value, 8), np.int32)
+        self.edges = np.zeros((nd.value, 3), np.int32)
+        self.seams = np.zeros((ns.value, 3), np.int32)
+        red_r = np.zeros(nr.value, np.int32)
+        red_g = np.zeros(nr.value, np.int32)
+        _check(self.L.mpipe_derived_lists(h, _vp(self.events), _vp(self.edges), _vp(self.seams),
+                                          _vp(red_r), _vp(red_g)))
+        self.reduces = np.stack([red_r, red_g], axis=1) if nr.value else np.zeros((0, 2), np.int32)
+        self.nodes = []
+        for r in range(self.P):
+            n = self.L.mpipe_derived_nodes(h, r, None, 0)
+            if n < 0:
+                raise MpipeError(-1, last_error())
+            v = np.zeros(n, np.int32)
+            self.L.mpipe_derived_nodes(h, r, _vp(v), n)
+            self.nodes.append(v)
+
+    def __del__(self):
+        h = getattr(self, "_h", None)
+        if h is not None and h.value:
+            self.L.mpipe_derived_destroy(h)
+            self._h = None
+
+    def event_costs(self, fwd_cost, bwd_cost, seam_bytes, reduce_bytes, alpha: float,
+                    beta: float, loss_cost: float) -> np.ndarray:
+        """Cost of every event (Sec. 4.3); fwd_cost/bwd_cost [k, M] seconds of a whole
+        region, seam_bytes [k-1, M], reduce_bytes [k]."""
+        f = np.ascontiguousarray(fwd_cost, dtype=np.float64).reshape(-1)
+        b = np.ascontiguousarray(bwd_cost, dtype=np.float64).reshape(-1)
+        sb = np.ascontiguousarray(seam_bytes, dtype=np.float64).reshape(-1)
+        rb = np.ascontiguousarray(reduce_bytes, dtype=np.float64).reshape(-1)
+        if f.size != self.k * self.M or b.size != self.k * self.M or rb.size != self.k \
+                or sb.size != (self.k - 1) * self.M:
+            raise MpipeError(-1, "cost arrays do not match (k, M)")
+        out = np.zeros(self.events.shape[0], np.float64)
+        _check(self.L.mpipe_event_costs(self._h, _vp(f), _vp(b), _vp(sb) if sb.size else None,
+                                        _vp(rb), float(alpha), float(beta), float(loss_cost),
+                                        _vp(out)))
+        return out
+
+    def makespan(self, cost):
+        """(T, bubble [P], start [n_events], finish [n_events])."""
+        c = np.ascontiguousarray(cost, dtype=np.float64)
+        if c.size != self.events.shape[0]:
+            raise MpipeError(-1, "one cost per event")
+        T = C.c_double()
+        bub = np.zeros(self.P, np.float64)
+        st = np.zeros(c.size, np.float64)
+        fin = np.zeros(c.size, np.float64)
+        _check(self.L.mpipe_makespan(self._h, _vp(c), C.byref(T), _vp(bub), _vp(st), _vp(fin)))
+        return T.value, bub, st, fin
+
+    def memory_peak(self, act_bytes) -> np.ndarray:
+        a = np.ascontiguousarray(act_bytes, dtype=np.float64)
+        if a.size != self.events.shape[0]:
+            raise MpipeError(-1, "one byte count per event")
+        out = np.zeros(self.P, np.float64)
+        _check(self.L.mpipe_memory_peak(self._h, _vp(a), _vp(out)))
+        return out
 
 
 def merge_scatter(merged, placeholder_idx, embeds, stream=None) -> None:

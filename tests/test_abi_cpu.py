@@ -17,7 +17,7 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
 def _declared_functions():
     names = set()
-    for h in ("mpipe.h", "mpipe_ops.h", "mpipe_sched.h"):
+    for h in ("mpipe.h", "mpipe_ops.h", "mpipe_sched.h", "mpipe_derive.h"):
         src = open(os.path.join(ROOT, "include", h)).read()
         src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
         names |= set(re.findall(r"\b(mpipe_[a-z0-9_]+)\s*\(", src))
