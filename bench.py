@@ -76,12 +76,15 @@ EPI_NAMES = ["store", "gelu", "resid", "gelubwd", "f32"]
 
 
 def source_digest() -> str:
-    """Digest of the kernel sources: stored traffic is reported only while it matches."""
+    """Digest of the kernel sources and the host code that launches them: stored traffic is
+    reported only while it matches.  The host-only scheduling sources (owner map, schedule
+    algebra) launch nothing and are left out."""
     import hashlib
     h = hashlib.sha256()
     src = os.path.join(ROOT, "paper_2607_03229_amd", "csrc")
+    host_only = {"owner.cpp", "derive.cpp"}
     for f in sorted(os.listdir(src)):
-        if f.endswith((".hip", ".cpp", ".h")):
+        if f.endswith((".hip", ".cpp", ".h")) and f not in host_only:
             h.update(f.encode())
             with open(os.path.join(src, f), "rb") as fh:
                 h.update(fh.read())
