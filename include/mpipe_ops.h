@@ -44,13 +44,15 @@ mpipe_status mpipe_op_layernorm_fwd(int32_t dtype, const float* X, int64_t rows,
                                     float* rstd, void* hip_stream);
 
 /* LayerNorm backward: dX = dres + LN'(dY) (fp32), dXt = the same in dtype
- * (nullable), grad_g / grad_b += column sums (fp32, nullable).  scratch: at
- * least mpipe_op_scratch_bytes(rows, 1, n, 0) bytes. */
+ * (nullable), grad_g / grad_b += column sums of dY*xhat and dY, colsum_dx +=
+ * column sums of dX (the bias gradient of the product whose output gradient dX
+ * is), all fp32 [n] and nullable.  scratch: at least
+ * mpipe_op_scratch_bytes(rows, 1, n, 0) bytes. */
 mpipe_status mpipe_op_layernorm_bwd(int32_t dtype, const float* dY, const float* X,
                                     const float* mean, const float* rstd, const void* g,
                                     int64_t rows, int32_t n, const float* dres, float* dX,
-                                    void* dXt, float* grad_g, float* grad_b, void* scratch,
-                                    size_t scratch_bytes, void* hip_stream);
+                                    void* dXt, float* grad_g, float* grad_b, float* colsum_dx,
+                                    void* scratch, size_t scratch_bytes, void* hip_stream);
 
 /* 2D rotary position, in place on the q and k blocks of qkv [rows][3*heads*d]
  * (inverse != 0 rotates back: the backward).  Positions come from grid_thw

@@ -76,7 +76,7 @@ def load():
         "mpipe_op_gemm": (st, [i32, i32, i32, i32, i32, i32, P, i64, P, i64, P, i64, P, P, i64,
                                P, i64, i32, i32, i64, P]),
         "mpipe_op_layernorm_fwd": (st, [i32, P, i64, i32, P, P, C.c_float, P, P, P, P]),
-        "mpipe_op_layernorm_bwd": (st, [i32, P, P, P, P, P, i64, i32, P, P, P, P, P, P, sz, P]),
+        "mpipe_op_layernorm_bwd": (st, [i32, P, P, P, P, P, i64, i32, P, P, P, P, P, P, P, sz, P]),
         "mpipe_op_rope": (st, [i32, P, i64, i32, i32, P, i32, C.c_float, i32, P, sz, P]),
         "mpipe_op_attention_fwd": (st, [i32, P, i64, i32, i32, P, i32, P, P, P, sz, P]),
         "mpipe_op_attention_bwd": (st, [i32, P, P, P, P, i64, i32, i32, P, i32, P, P, sz, P]),
@@ -444,10 +444,10 @@ def op_layernorm_fwd(dtype, X, rows, n, g, b, eps, Y, mean=None, rstd=None, stre
 
 
 def op_layernorm_bwd(dtype, dY, X, mean, rstd, g, rows, n, dres, dX, dXt, grad_g, grad_b,
-                     scratch, stream=None):
+                     scratch, stream=None, colsum_dx=None):
     _check(load().mpipe_op_layernorm_bwd(dtype, _ptr(dY), _ptr(X), _ptr(mean), _ptr(rstd), _ptr(g),
                                          rows, n, _ptr(dres), _ptr(dX), _ptr(dXt), _ptr(grad_g),
-                                         _ptr(grad_b), _ptr(scratch),
+                                         _ptr(grad_b), _ptr(colsum_dx), _ptr(scratch),
                                          scratch.numel() * scratch.element_size(),
                                          _stream(stream)))
 

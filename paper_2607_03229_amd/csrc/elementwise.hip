@@ -120,7 +120,9 @@ __global__ __launch_bounds__(256) void ln_fwd_kernel(const float* X, int64_t ldx
 // (and optionally as T for the next GEMM).  Each block owns a contiguous chunk of
 // rows (its four waves take every fourth row); the block's sums of dy*xhat and dy
 // are combined in LDS in a fixed order and written to part_g / part_b
-// [gridDim.x][n] for a deterministic reduction.
+// [gridDim.x][n] for a deterministic reduction.  With part_c the block also sums the
+// dx rows it writes (the bias gradient of the product that produced this residual-stream
+// gradient), so no separate pass over dx is needed.
 constexpr int LN_BWD_MAX_BLOCKS = 1024;
 static_assert(LN_BWD_MAX_BLOCKS <= kPartialRowsMax, "partials must fit the workspace");
 
@@ -144,14 +146,14 @@ __global__ __launch_bounds__(256) void ln_bwd_kernel(const float* dY, int64_t ld
                                                      const float* rstd, const T* gam, int64_t rows,
                                                      int n, int64_t rows_per_block,
                                                      const float* dres, float* dX, T* dXt,
-                                                     float* part_g, float* part_b) {
+                                                     float* part_g, float* part_b, float* part_c) {
   __shared__ float4 red[4 * MC * 64];
   const int wave = threadIdx.x >> 6, l = threadIdx.x & 63;
   const int nc = n / 4;
-  float4 ag[MC], ab[MC], gm[MC];
+  float4 ag[MC], ab[MC], ac[MC], gm[MC];
 #pragma unroll
   for (int i = 0; i < MC; ++i) {
-    ag[i] = ab[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+    ag[i] = ab[i] = ac[i] = make_float4(0.f, 0.f, 0.f, 0.f);
     const int c = l + 64 * i;
     if (c < nc) gm[i] = V4<T>::load(gam + 4 * c);
   }
@@ -200,6 +202,7 @@ __global__ __launch_bounds__(256) void ln_bwd_kernel(const float* dY, int64_t ld
         o.w = rs * (dy[i].w * gm[i].w - s1 - x[i].w * s2) + dr[i].w;
         V4<float>::store(dX + row * ldx + 4 * c, o);
         if (dXt) V4<T>::store(dXt + row * ldx + 4 * c, o);
+        ac[i].x += o.x; ac[i].y += o.y; ac[i].z += o.z; ac[i].w += o.w;
       }
     }
   }
@@ -213,6 +216,12 @@ __global__ __launch_bounds__(256) void ln_bwd_kernel(const float* dY, int64_t ld
   for (int i = 0; i < MC; ++i) red[(wave * MC + i) * 64 + l] = ab[i];
   __syncthreads();
   combine_waves<MC>(red, nc, part_b + (int64_t)blockIdx.x * n);
+  if (!part_c || !dX) return;   // uniform over the grid
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < MC; ++i) red[(wave * MC + i) * 64 + l] = ac[i];
+  __syncthreads();
+  combine_waves<MC>(red, nc, part_c + (int64_t)blockIdx.x * n);
 }
 
 // ---- column sums: part[b][c] = sum of X[r][c] over row chunk b ----------------------
@@ -283,35 +292,72 @@ __global__ __launch_bounds__(256) void colsum_vec_kernel(const T* X, int64_t ld,
   }
 }
 
-// out[c] += sum_b part[b][c], b < nb.  One block of 16 waves per 64 columns: wave w
-// sums partial rows w, w + 16, ... with four loads in flight, and the 16 wave sums are
-// combined in a fixed order (the result depends only on nb, never on timing).
-constexpr int RED_WAVES = 16;
-__global__ __launch_bounds__(64 * RED_WAVES) void reduce_partials_kernel(const float* part,
-                                                                       int64_t nb, int n,
-                                                                       float* out) {
-  __shared__ float red[RED_WAVES][64];
+// out[c] += sum_b part[b][c], b < nb, for up to two (part, out) sets (blockIdx.z), in two
+// fixed-order stages so that the result depends only on nb, never on timing.
+// Stage 1: block (x, g) sums the partial rows of chunk g, [g * chunk, (g + 1) * chunk), for
+// columns 64x..64x+63 (wave w takes rows w, w + 4, ..., four loads in flight; the four wave
+// sums are added in order) and writes the chunk sum over the chunk's first row: only this
+// block reads or writes that part of the buffer.  Stage 2 adds the chunk sums in chunk order.
+struct PartialSet {
+  float* part[3];
+  float* out[3];
+};
+constexpr int RED_CHUNKS = 16;   // at most this many chunks per set
+
+int64_t reduce_chunk_rows(int64_t nb) {
+  const int64_t c = (nb + RED_CHUNKS - 1) / RED_CHUNKS;
+  return c < 16 ? 16 : c;
+}
+
+__global__ __launch_bounds__(256) void reduce_partials_stage1(PartialSet ps, int64_t nb, int n,
+                                                              int64_t chunk) {
+  __shared__ float red[4][64];
+  float* part = ps.part[blockIdx.z];
   const int w = threadIdx.x >> 6, l = threadIdx.x & 63;
   const int c = blockIdx.x * 64 + l;
+  const int64_t r0 = (int64_t)blockIdx.y * chunk;
+  const int64_t r1 = min(nb, r0 + chunk);
   float s0 = 0.f, s1 = 0.f, s2 = 0.f, s3 = 0.f;
   if (c < n) {
-    int64_t b = w;
-    for (; b + 3 * RED_WAVES < nb; b += 4 * RED_WAVES) {
+    int64_t b = r0 + w;
+    for (; b + 12 < r1; b += 16) {
       s0 += part[b * n + c];
-      s1 += part[(b + RED_WAVES) * n + c];
-      s2 += part[(b + 2 * RED_WAVES) * n + c];
-      s3 += part[(b + 3 * RED_WAVES) * n + c];
+      s1 += part[(b + 4) * n + c];
+      s2 += part[(b + 8) * n + c];
+      s3 += part[(b + 12) * n + c];
     }
-    for (; b < nb; b += RED_WAVES) s0 += part[b * n + c];
+    for (; b < r1; b += 4) s0 += part[b * n + c];
   }
   red[w][l] = (s0 + s1) + (s2 + s3);
   __syncthreads();
-  if (w == 0 && c < n) {
-    float t = 0.f;
-#pragma unroll
-    for (int k = 0; k < RED_WAVES; ++k) t += red[k][l];
-    out[c] += t;
-  }
+  if (w == 0 && c < n) part[r0 * n + c] = (red[0][l] + red[1][l]) + (red[2][l] + red[3][l]);
+}
+
+__global__ __launch_bounds__(64) void reduce_partials_stage2(PartialSet ps, int64_t nb, int n,
+                                                             int64_t chunk) {
+  const float* part = ps.part[blockIdx.z];
+  const int c = blockIdx.x * 64 + threadIdx.x;
+  if (c >= n) return;
+  float t = 0.f;
+  for (int64_t r = 0; r < nb; r += chunk) t += part[r * n + c];
+  ps.out[blockIdx.z][c] += t;
+}
+
+// Launch both stages for the non-null sets among (p0, o0), (p1, o1), (p2, o2).
+void reduce_partials(float* p0, float* o0, float* p1, float* o1, float* p2, float* o2,
+                     int64_t nb, int n, hipStream_t s) {
+  PartialSet ps{};
+  int z = 0;
+  if (o0) ps.part[z] = p0, ps.out[z] = o0, ++z;
+  if (o1) ps.part[z] = p1, ps.out[z] = o1, ++z;
+  if (o2) ps.part[z] = p2, ps.out[z] = o2, ++z;
+  if (!z || nb <= 0 || n <= 0) return;
+  const int64_t chunk = reduce_chunk_rows(nb);
+  const unsigned cx = (unsigned)((n + 63) / 64), g = (unsigned)((nb + chunk - 1) / chunk);
+  hipLaunchKernelGGL(reduce_partials_stage1, dim3(cx, g, (unsigned)z), dim3(256), 0, s, ps, nb, n,
+                     chunk);
+  hipLaunchKernelGGL(reduce_partials_stage2, dim3(cx, 1, (unsigned)z), dim3(64), 0, s, ps, nb, n,
+                     chunk);
 }
 
 // out[m][n] += sum_s part[s][m][n], four columns per thread (N % 4 == 0, ldo % 4 == 0,
@@ -581,21 +627,24 @@ int64_t layernorm_bwd_partial_rows(int64_t rows) {
   return b < LN_BWD_MAX_BLOCKS ? b : LN_BWD_MAX_BLOCKS;
 }
 
-hipError_t layernorm_bwd(int dtype, const float* dY, int64_t ldd, const float* X, int64_t ldx,
-                         const float* mean, const float* rstd, const void* g, int64_t rows, int n,
-                         const float* dres, float* dX, void* dXt, float* part_g, float* part_b,
-                         float* grad_g, float* grad_b, hipStream_t s) {
+hipError_t layernorm_bwd_partials(int dtype, const float* dY, int64_t ldd, const float* X,
+                                  int64_t ldx, const float* mean, const float* rstd, const void* g,
+                                  int64_t rows, int n, const float* dres, float* dX, void* dXt,
+                                  float* part_g, float* part_b, float* part_c, int64_t* blocks,
+                                  hipStream_t s) {
+  *blocks = 0;
   if (rows == 0) return hipSuccess;
   // one round of resident blocks (never more than the partial rows the caller sized)
   const int mc = (n / 4 + 63) / 64;
   int64_t nblk = 0;
+  float* pc = dX ? part_c : nullptr;
   auto go = [&](auto MCc) {
     constexpr int MC = decltype(MCc)::value;
     auto launch = [&](auto kern, auto gptr, auto dxt) {
       nblk = std::min(layernorm_bwd_partial_rows(rows), resident_blocks<MC>(kern, 256));
       const int64_t rpb = (rows + nblk - 1) / nblk;
       hipLaunchKernelGGL(kern, dim3((unsigned)nblk), dim3(256), 0, s, dY, ldd, X, ldx, mean, rstd,
-                         gptr, rows, n, rpb, dres, dX, dxt, part_g, part_b);
+                         gptr, rows, n, rpb, dres, dX, dxt, part_g, part_b, pc);
     };
     if (dtype == DT_BF16)
       launch(ln_bwd_kernel<bf16, MC>, (const bf16*)g, (bf16*)dXt);
@@ -603,14 +652,28 @@ hipError_t layernorm_bwd(int dtype, const float* dY, int64_t ldd, const float* X
       launch(ln_bwd_kernel<float, MC>, (const float*)g, (float*)dXt);
   };
   if (!dispatch_mc(mc, go)) return hipErrorInvalidValue;
-  const dim3 rg((unsigned)((n + 63) / 64));
-  if (grad_g)
-    hipLaunchKernelGGL(reduce_partials_kernel, rg, dim3(64 * RED_WAVES), 0, s, part_g, nblk, n,
-                       grad_g);
-  if (grad_b)
-    hipLaunchKernelGGL(reduce_partials_kernel, rg, dim3(64 * RED_WAVES), 0, s, part_b, nblk, n,
-                       grad_b);
+  *blocks = nblk;
   return hipGetLastError();
+}
+
+hipError_t layernorm_bwd_reduce(float* part_g, float* grad_g, float* part_b, float* grad_b,
+                                float* part_c, float* grad_c, int64_t blocks, int n,
+                                hipStream_t s) {
+  reduce_partials(part_g, grad_g, part_b, grad_b, part_c, grad_c, blocks, n, s);
+  return hipGetLastError();
+}
+
+hipError_t layernorm_bwd(int dtype, const float* dY, int64_t ldd, const float* X, int64_t ldx,
+                         const float* mean, const float* rstd, const void* g, int64_t rows, int n,
+                         const float* dres, float* dX, void* dXt, float* part_g, float* part_b,
+                         float* part_c, float* grad_g, float* grad_b, float* grad_c,
+                         hipStream_t s) {
+  if (!dX || !grad_c) part_c = grad_c = nullptr;
+  int64_t nb = 0;
+  hipError_t r = layernorm_bwd_partials(dtype, dY, ldd, X, ldx, mean, rstd, g, rows, n, dres, dX,
+                                        dXt, part_g, part_b, part_c, &nb, s);
+  if (r != hipSuccess) return r;
+  return layernorm_bwd_reduce(part_g, grad_g, part_b, grad_b, part_c, grad_c, nb, n, s);
 }
 
 int64_t colsum_partial_rows(int64_t rows) {
@@ -641,8 +704,7 @@ hipError_t colsum_accumulate(int dtype_in, const void* X, int64_t ld, int64_t ro
       hipLaunchKernelGGL(colsum_partial_kernel<float>, grid, dim3(256), 0, s, (const float*)X, ld,
                          rows, n, rpc, part);
   }
-  hipLaunchKernelGGL(reduce_partials_kernel, dim3((unsigned)((n + 63) / 64)), dim3(64 * RED_WAVES),
-                     0, s, part, nb, n, out);
+  reduce_partials(part, out, nullptr, nullptr, nullptr, nullptr, nb, n, s);
   return hipGetLastError();
 }
 

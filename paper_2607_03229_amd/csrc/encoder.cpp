@@ -53,11 +53,11 @@ struct mpipe_encoder {
   std::vector<Rec> recs;
   std::vector<hipEvent_t> pool;
   // Weight-gradient side stream of the backward (default priority) and its sync events:
-  // 0 fork (caller -> side), 1..4 buffer-free signals (side -> caller), 5 join.
+  // 0 fork (caller -> side), 1..6 buffer-free signals (side -> caller), 7 join.
   bool side_on = true;
   hipStream_t side = nullptr;
   int side_dev = -1;
-  hipEvent_t sync[6] = {};
+  hipEvent_t sync[8] = {};
 
   hipEvent_t event() {
     if (!pool.empty()) {
@@ -197,7 +197,7 @@ mpipe_status colsum(Ctx& x, int dtype_in, const void* X, int64_t ld, int64_t row
 struct SideSync {
   Ctx& x;
   bool on;
-  bool recorded[6] = {};
+  bool recorded[8] = {};
   hipError_t fork() {
     if (!on) return hipSuccess;
     hipError_t r = hipEventRecord(x.e->sync[0], x.s);
@@ -214,11 +214,11 @@ struct SideSync {
   }
   hipError_t join() {
     if (!on) return hipSuccess;
-    hipError_t r = hipEventRecord(x.e->sync[5], x.s2);
-    return r != hipSuccess ? r : hipStreamWaitEvent(x.s, x.e->sync[5], 0);
+    hipError_t r = hipEventRecord(x.e->sync[7], x.s2);
+    return r != hipSuccess ? r : hipStreamWaitEvent(x.s, x.e->sync[7], 0);
   }
 };
-enum { FREE_DU = 1, FREE_DH = 2, FREE_DHM = 3, FREE_DQKV = 4 };
+enum { FREE_DU = 1, FREE_DH = 2, FREE_DHM = 3, FREE_DQKV = 4, FREE_LNP0 = 5, FREE_LNP1 = 6 };
 
 // Creates the side stream and its events on the current device (once per device).
 hipError_t ensure_side(mpipe_encoder* e) {
@@ -484,8 +484,11 @@ mpipe_status backward(Ctx& x, const void* patches, const char* tape, const void*
   char* dO = x.ws + P.ws_do;
   float* delta = reinterpret_cast<float*>(x.ws + P.ws_delta);
   char* dqkv = x.ws + P.ws_dqkv;
+  // LayerNorm-backward partials: two buffers of three sets (gain, shift, and the column sums
+  // of the residual-stream gradient it writes, which is the next bias gradient), each
+  // kPartialRowsMax x h floats
   float* part = reinterpret_cast<float*>(x.ws + P.ws_part);
-  const int64_t part_half = kPartialRowsMax * std::max({3 * h, m, 4 * h, H, (int64_t)c.kpe});
+  const int64_t ln_set = kPartialRowsMax * h;
 
   // Only the merger trainable: it is the trainable source (Lemma 1 applied to the
   // encoder's parts), so its backward ends with its own LayerNorm's affine gradients.
@@ -501,6 +504,32 @@ mpipe_status backward(Ctx& x, const void* patches, const char* tape, const void*
   // stream (x.s2), which forks off after each gradient buffer is produced; the caller's
   // stream waits for a buffer's side readers only before it overwrites that buffer.
   SideSync ss{x, x.s2 != x.s};
+  // LayerNorm backward of dx32 on the caller's stream; its partial sums are reduced into
+  // the gain, shift and bias gradients on the side stream (nothing in the backward reads
+  // them).  The partial buffers alternate, so a call waits only for the reduction of the
+  // call two back before overwriting its buffer.
+  int ln_calls = 0;
+  auto ln_bwd = [&](const float* X_, const char* mean_, const char* rstd_, const void* g_,
+                    const float* dres_, float* dX_, void* dXt_, float* gg, float* gb,
+                    float* gc) -> mpipe_status {
+    const int k = ln_calls++ & 1;
+    float* pg = part + 3 * k * ln_set;
+    float* pb = pg + ln_set;
+    float* pc = (dX_ && gc) ? pb + ln_set : nullptr;
+    MP_CHECK(ss.acquire(FREE_LNP0 + k));
+    int64_t nb = 0;
+    MP_CHECK(run(x.e, x.s, "layernorm_bwd", 0, [&] {
+      return layernorm_bwd_partials(x.dt, dx32, h, X_, h, reinterpret_cast<const float*>(mean_),
+                                    reinterpret_cast<const float*>(rstd_), g_, N, (int)h, dres_,
+                                    dX_, dXt_, pg, pb, pc, &nb, x.s);
+    }));
+    MP_CHECK(ss.fork());
+    MP_CHECK(run(x.e, x.s2, "ln_reduce", 0, [&] {
+      return layernorm_bwd_reduce(pg, gg, pb, gb, pc, pc ? gc : nullptr, nb, (int)h, x.s2);
+    }));
+    MP_CHECK(ss.release(FREE_LNP0 + k));
+    return MPIPE_OK;
+  };
   MP_CHECK(ss.fork());
   // merger
   MP_RET(dw_gemm(x, dM, H, base + MS.gm, 4 * h, H, 4 * h, Tm, x.grad(dw, merger_param(c, M_FC2W)), 4 * h));
@@ -519,15 +548,11 @@ mpipe_status backward(Ctx& x, const void* patches, const char* tape, const void*
     GemmArgs a = ga(du, 4 * h, x.W(merger_param(c, M_FC1W)), 4 * h, Tm, 4 * h, 4 * h, dx32, 4 * h);
     MP_RET(gemm_call(x, GEMM_NN, EPI_F32, a));
   }
-  MP_CHECK(run(x.e, x.s, "layernorm_bwd", 0, [&] {
-    return layernorm_bwd(x.dt, dx32, h, reinterpret_cast<const float*>(base + MS.hfin), h,
-                         reinterpret_cast<const float*>(base + MS.meanz),
-                         reinterpret_cast<const float*>(base + MS.rstdz),
-                         x.W(merger_param(c, M_LNG)), N, (int)h, nullptr,
-                         merger_only ? nullptr : dh, merger_only ? nullptr : dht, part,
-                         part + part_half, x.grad(dw, merger_param(c, M_LNG)),
-                         x.grad(dw, merger_param(c, M_LNB)), x.s);
-  }));
+  MP_RET(ln_bwd(reinterpret_cast<const float*>(base + MS.hfin), base + MS.meanz, base + MS.rstdz,
+                x.W(merger_param(c, M_LNG)), nullptr, merger_only ? nullptr : dh,
+                merger_only ? nullptr : dht, x.grad(dw, merger_param(c, M_LNG)),
+                x.grad(dw, merger_param(c, M_LNB)),
+                merger_only ? nullptr : x.grad(dw, blk_param(c, c.layers - 1, B_FC2B))));
   if (merger_only) return MPIPE_OK;
 
   for (int l = c.layers - 1; l >= 0; --l) {
@@ -537,7 +562,6 @@ mpipe_status backward(Ctx& x, const void* patches, const char* tape, const void*
     // MLP: H_out = H_mid + GELU(B W1^T + b1) W2^T + b2
     MP_CHECK(ss.fork());   // dh, dht
     MP_RET(dw_gemm(x, dht, h, base + S.g, m, h, m, N, x.grad(dw, blk_param(c, l, B_FC2W)), m));
-    MP_RET(colsum(x, DT_F32, dh, h, N, (int)h, x.grad(dw, blk_param(c, l, B_FC2B))));
     MP_CHECK(ss.release(FREE_DH));
     MP_CHECK(ss.acquire(FREE_DU));
     {
@@ -555,17 +579,12 @@ mpipe_status backward(Ctx& x, const void* patches, const char* tape, const void*
       MP_RET(gemm_call(x, GEMM_NN, EPI_F32, a));
     }
     MP_CHECK(ss.acquire(FREE_DHM));
-    MP_CHECK(run(x.e, x.s, "layernorm_bwd", 0, [&] {
-      return layernorm_bwd(x.dt, dx32, h, hmid, h, reinterpret_cast<const float*>(base + S.mean2),
-                           reinterpret_cast<const float*>(base + S.rstd2),
-                           x.W(blk_param(c, l, B_LN2G)), N, (int)h, dh, dhm, dhmt, part,
-                           part + part_half, x.grad(dw, blk_param(c, l, B_LN2G)),
-                           x.grad(dw, blk_param(c, l, B_LN2B)), x.s);
-    }));
+    MP_RET(ln_bwd(hmid, base + S.mean2, base + S.rstd2, x.W(blk_param(c, l, B_LN2G)), dh, dhm,
+                  dhmt, x.grad(dw, blk_param(c, l, B_LN2G)), x.grad(dw, blk_param(c, l, B_LN2B)),
+                  x.grad(dw, blk_param(c, l, B_PROJB))));
     // attention: H_mid = H_in + O Wo^T + bo
     MP_CHECK(ss.fork());   // dhm, dhmt
     MP_RET(dw_gemm(x, dhmt, h, base + S.o, h, h, h, N, x.grad(dw, blk_param(c, l, B_PROJW)), h));
-    MP_RET(colsum(x, DT_F32, dhm, h, N, (int)h, x.grad(dw, blk_param(c, l, B_PROJB))));
     MP_CHECK(ss.release(FREE_DHM));
     {
       GemmArgs a = ga(dhmt, h, x.W(blk_param(c, l, B_PROJW)), h, N, h, h, dO, h);
@@ -603,18 +622,13 @@ mpipe_status backward(Ctx& x, const void* patches, const char* tape, const void*
       MP_RET(gemm_call(x, GEMM_NN, EPI_F32, a));
     }
     MP_CHECK(ss.acquire(FREE_DH));
-    MP_CHECK(run(x.e, x.s, "layernorm_bwd", 0, [&] {
-      return layernorm_bwd(x.dt, dx32, h, hin, h, reinterpret_cast<const float*>(base + S.mean1),
-                           reinterpret_cast<const float*>(base + S.rstd1),
-                           x.W(blk_param(c, l, B_LN1G)), N, (int)h, dhm, dh, dht, part,
-                           part + part_half, x.grad(dw, blk_param(c, l, B_LN1G)),
-                           x.grad(dw, blk_param(c, l, B_LN1B)), x.s);
-    }));
+    MP_RET(ln_bwd(hin, base + S.mean1, base + S.rstd1, x.W(blk_param(c, l, B_LN1G)), dhm, dh, dht,
+                  x.grad(dw, blk_param(c, l, B_LN1G)), x.grad(dw, blk_param(c, l, B_LN1B)),
+                  x.grad(dw, l > 0 ? blk_param(c, l - 1, B_FC2B) : P_PE_B)));
   }
   // patch embedding (the trainable source: nothing goes upstream unless asked)
   MP_CHECK(ss.fork());   // dh, dht
   MP_RET(dw_gemm(x, dht, h, Xp, ldx, h, c.kpe, N, x.grad(dw, P_PE_W), c.kpe));
-  MP_RET(colsum(x, DT_F32, dh, h, N, (int)h, x.grad(dw, P_PE_B)));
   if (d_patches) {
     GemmArgs a = ga(dht, h, Wpe, ldx, N, c.kpe, h, d_patches, c.kpe);
     MP_RET(gemm_call(x, GEMM_NN, EPI_STORE, a));

@@ -72,11 +72,25 @@ hipError_t layernorm_fwd(int dtype, const float* X, int64_t ldx, int64_t rows, i
                          float* mean, float* rstd, hipStream_t s);
 int64_t layernorm_bwd_partial_rows(int64_t rows);
 // dX, dres and dXt use the row stride ldx of X.  dX == nullptr computes only the affine
-// gradients (dXt and dres are then ignored).
+// gradients (dXt and dres are then ignored).  grad_g, grad_b and grad_c (nullable) are
+// accumulated (+=) with the column sums of dy*xhat, dy and the written dX (grad_c needs dX);
+// part_g, part_b and part_c each hold layernorm_bwd_partial_rows(rows) x n floats.
 hipError_t layernorm_bwd(int dtype, const float* dY, int64_t ldd, const float* X, int64_t ldx,
                          const float* mean, const float* rstd, const void* g, int64_t rows, int n,
                          const float* dres, float* dX, void* dXt, float* part_g, float* part_b,
-                         float* grad_g, float* grad_b, hipStream_t s);
+                         float* part_c, float* grad_g, float* grad_b, float* grad_c,
+                         hipStream_t s);
+// The two halves of layernorm_bwd, for callers that reduce on another stream: the kernel
+// (part_c written when both it and dX are non-null; *blocks = the partial rows written)
+// and the deterministic reduction of those partial rows into the (nullable) targets.
+hipError_t layernorm_bwd_partials(int dtype, const float* dY, int64_t ldd, const float* X,
+                                  int64_t ldx, const float* mean, const float* rstd, const void* g,
+                                  int64_t rows, int n, const float* dres, float* dX, void* dXt,
+                                  float* part_g, float* part_b, float* part_c, int64_t* blocks,
+                                  hipStream_t s);
+hipError_t layernorm_bwd_reduce(float* part_g, float* grad_g, float* part_b, float* grad_b,
+                                float* part_c, float* grad_c, int64_t blocks, int n,
+                                hipStream_t s);
 int64_t colsum_partial_rows(int64_t rows);
 hipError_t colsum_accumulate(int dtype_in, const void* X, int64_t ld, int64_t rows, int n,
                              float* part, float* out, hipStream_t s);

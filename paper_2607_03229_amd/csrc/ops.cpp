@@ -66,7 +66,7 @@ size_t mpipe_op_scratch_bytes(int64_t N, int32_t heads, int32_t n, int32_t n_seg
   const size_t work = al(((size_t)(N + ATTN_TILE - 1) / ATTN_TILE + (size_t)n_seg + 1) * 16);
   const size_t delta = al((size_t)heads * N * 4);
   const size_t pos = al((size_t)N * 4) + al((size_t)65536 * 8);
-  const size_t part = al((size_t)layernorm_bwd_partial_rows(N) * std::max(n, 1) * 4) * 2;
+  const size_t part = al((size_t)layernorm_bwd_partial_rows(N) * std::max(n, 1) * 4) * 3;
   return std::max(work + delta, pos) + part + 4096;
 }
 
@@ -105,15 +105,16 @@ mpipe_status mpipe_op_layernorm_fwd(int32_t dtype, const float* X, int64_t rows,
 mpipe_status mpipe_op_layernorm_bwd(int32_t dtype, const float* dY, const float* X,
                                     const float* mean, const float* rstd, const void* g,
                                     int64_t rows, int32_t n, const float* dres, float* dX,
-                                    void* dXt, float* grad_g, float* grad_b, void* scratch,
-                                    size_t scratch_bytes, void* stream) {
+                                    void* dXt, float* grad_g, float* grad_b, float* colsum_dx,
+                                    void* scratch, size_t scratch_bytes, void* stream) {
   if (n % 4 || n > 2048 || n <= 0) return set_error(MPIPE_ERR_UNSUPPORTED, "n must be a multiple of 4, <= 2048");
-  const size_t half = al((size_t)layernorm_bwd_partial_rows(rows) * n * 4);
-  if (scratch_bytes < 2 * half) return set_error(MPIPE_ERR_WORKSPACE, "scratch too small");
+  const size_t third = al((size_t)layernorm_bwd_partial_rows(rows) * n * 4);
+  if (scratch_bytes < 3 * third) return set_error(MPIPE_ERR_WORKSPACE, "scratch too small");
   float* pg = reinterpret_cast<float*>(scratch);
-  float* pb = reinterpret_cast<float*>(reinterpret_cast<char*>(scratch) + half);
-  OP_CHECK(layernorm_bwd(dtype, dY, n, X, n, mean, rstd, g, rows, n, dres, dX, dXt, pg, pb, grad_g,
-                         grad_b, reinterpret_cast<hipStream_t>(stream)));
+  float* pb = reinterpret_cast<float*>(reinterpret_cast<char*>(scratch) + third);
+  float* pc = reinterpret_cast<float*>(reinterpret_cast<char*>(scratch) + 2 * third);
+  OP_CHECK(layernorm_bwd(dtype, dY, n, X, n, mean, rstd, g, rows, n, dres, dX, dXt, pg, pb, pc,
+                         grad_g, grad_b, colsum_dx, reinterpret_cast<hipStream_t>(stream)));
   return MPIPE_OK;
 }
 

@@ -299,9 +299,10 @@ int build_plan(const Cfg& c, const int32_t* cu, int n_seg, const int32_t* thw, i
     p.ws_delta = ws.take((size_t)N * nh * 4);
     p.ws_dqkv = ws.take((size_t)N * 3 * h * E);
     const int64_t widest = std::max({3 * h, m, 4 * h, H, (int64_t)c.kpe});
-    // LayerNorm-affine partials (two halves, caller's stream) and bias column-sum
-    // partials (own region: the backward runs column sums on its side stream)
-    p.ws_part = ws.take((size_t)kPartialRowsMax * widest * 4 * 2);
+    // LayerNorm-backward partials (two buffers of three sets: gain, shift and the column
+    // sums of the residual-stream gradient, h columns each) and bias column-sum partials
+    // (own region: the backward runs the remaining column sums on its side stream)
+    p.ws_part = ws.take((size_t)kPartialRowsMax * 6 * h * 4);
     p.ws_cpart = ws.take((size_t)kPartialRowsMax * widest * 4);
     // largest split-K partial over the weight-gradient GEMMs
     size_t dw = 0;

@@ -156,13 +156,21 @@ def test_layernorm_fwd_bwd(dtype, n):
     dres = rng.standard_normal((rows, n)).astype(np.float32)
     dX, dXt = zeros((rows, n), "f32"), zeros((rows, n), dtype)
     gg, gb = to_dev(np.ones(n), "f32"), to_dev(np.zeros(n), "f32")
+    gc = to_dev(np.full(n, 2.0), "f32")
     scratch = torch.empty(mp.op_scratch_bytes(rows, 1, n, 0), dtype=torch.uint8, device=dev)
     mp.op_layernorm_bwd(_dt(dtype), to_dev(dY, "f32"), dX_, mean, rstd, to_dev(g, dtype), rows, n,
-                        to_dev(dres, "f32"), dX, dXt, gg, gb, scratch)
+                        to_dev(dres, "f32"), dX, dXt, gg, gb, scratch, colsum_dx=gc)
     rdx, rdg, rdb = oracle.layernorm_bwd(dY, X, g, rmu, rrs)
     assert max_rel(host(dX), rdx + dres) < 1e-4
     assert max_rel(host(dXt), rdx + dres) < TOL[dtype]
     assert max_rel(host(gg), 1 + rdg) < 1e-4 and max_rel(host(gb), rdb) < 1e-4
+    # the fused column sums of dX, accumulated onto 2 (the bias-gradient Accumulate)
+    assert max_rel(host(gc), 2.0 + (rdx + dres).sum(axis=0)) < 1e-4
+    # without colsum_dx, and without dX (affine gradients only), nothing else changes
+    gg2, gb2 = to_dev(np.zeros(n), "f32"), to_dev(np.zeros(n), "f32")
+    mp.op_layernorm_bwd(_dt(dtype), to_dev(dY, "f32"), dX_, mean, rstd, to_dev(g, dtype), rows, n,
+                        None, None, None, gg2, gb2, scratch)
+    assert max_rel(host(gg2), rdg) < 1e-4 and max_rel(host(gb2), rdb) < 1e-4
 
 
 @pytest.mark.parametrize("dtype,heads,d", [("bf16", 16, 80), ("bf16", 4, 64), ("f32", 4, 32)])
