@@ -656,6 +656,11 @@ hipError_t layernorm_bwd_partials(int dtype, const float* dY, int64_t ldd, const
   return hipGetLastError();
 }
 
+hipError_t partials_reduce(float* part, float* out, int64_t rows, int n, hipStream_t s) {
+  reduce_partials(part, out, nullptr, nullptr, nullptr, nullptr, rows, n, s);
+  return hipGetLastError();
+}
+
 hipError_t layernorm_bwd_reduce(float* part_g, float* grad_g, float* part_b, float* grad_b,
                                 float* part_c, float* grad_c, int64_t blocks, int n,
                                 hipStream_t s) {

@@ -182,6 +182,14 @@ mpipe_status dw_gemm(Ctx& x, const void* A, int64_t lda, const void* B, int64_t 
   return MPIPE_OK;
 }
 
+// out += the column sums that the fc1 input-gradient GEMM wrote per 64-row band
+mpipe_status band_reduce(Ctx& x, int64_t rows, int n, float* out) {
+  float* part = reinterpret_cast<float*>(x.ws + x.P.ws_gpart);
+  MP_CHECK(run(x.e, x.s2, "colsum", 0,
+               [&] { return partials_reduce(part, out, (rows + 63) / 64, n, x.s2); }));
+  return MPIPE_OK;
+}
+
 mpipe_status colsum(Ctx& x, int dtype_in, const void* X, int64_t ld, int64_t rows, int n,
                     float* out) {
   float* part = reinterpret_cast<float*>(x.ws + x.P.ws_cpart);
@@ -534,15 +542,22 @@ mpipe_status backward(Ctx& x, const void* patches, const char* tape, const void*
   // merger
   MP_RET(dw_gemm(x, dM, H, base + MS.gm, 4 * h, H, 4 * h, Tm, x.grad(dw, merger_param(c, M_FC2W)), 4 * h));
   MP_RET(colsum(x, x.dt, dM, H, Tm, (int)H, x.grad(dw, merger_param(c, M_FC2B))));
+  // the GELU-backward GEMM also writes the column sums of du (the fc1 bias gradient) when
+  // it runs on the kernel that can; otherwise the side stream sums du
+  bool fused = false;
+  float* gpart = reinterpret_cast<float*>(x.ws + P.ws_gpart);
   {
     GemmArgs a = ga(dM, H, x.W(merger_param(c, M_FC2W)), 4 * h, Tm, 4 * h, H, du, 4 * h);
     a.aux = base + MS.um;
     a.ld_aux = 4 * h;
+    fused = gemm_fused_colsum(x.dt, GEMM_NN, EPI_GELU_BWD, a);
+    if (fused) a.colsum = gpart;
     MP_RET(gemm_call(x, GEMM_NN, EPI_GELU_BWD, a));
   }
   MP_CHECK(ss.fork());
   MP_RET(dw_gemm(x, du, 4 * h, base + MS.z, 4 * h, 4 * h, 4 * h, Tm, x.grad(dw, merger_param(c, M_FC1W)), 4 * h));
-  MP_RET(colsum(x, x.dt, du, 4 * h, Tm, (int)(4 * h), x.grad(dw, merger_param(c, M_FC1B))));
+  MP_RET(fused ? band_reduce(x, Tm, (int)(4 * h), x.grad(dw, merger_param(c, M_FC1B)))
+               : colsum(x, x.dt, du, 4 * h, Tm, (int)(4 * h), x.grad(dw, merger_param(c, M_FC1B))));
   MP_CHECK(ss.release(FREE_DU));
   {
     GemmArgs a = ga(du, 4 * h, x.W(merger_param(c, M_FC1W)), 4 * h, Tm, 4 * h, 4 * h, dx32, 4 * h);
@@ -568,11 +583,14 @@ mpipe_status backward(Ctx& x, const void* patches, const char* tape, const void*
       GemmArgs a = ga(dht, h, x.W(blk_param(c, l, B_FC2W)), m, N, m, h, du, m);
       a.aux = base + S.u;
       a.ld_aux = m;
+      fused = gemm_fused_colsum(x.dt, GEMM_NN, EPI_GELU_BWD, a);
+      if (fused) a.colsum = gpart;
       MP_RET(gemm_call(x, GEMM_NN, EPI_GELU_BWD, a));
     }
-    MP_CHECK(ss.fork());   // du
+    MP_CHECK(ss.fork());   // du and its band sums
     MP_RET(dw_gemm(x, du, m, base + S.b, h, m, h, N, x.grad(dw, blk_param(c, l, B_FC1W)), h));
-    MP_RET(colsum(x, x.dt, du, m, N, (int)m, x.grad(dw, blk_param(c, l, B_FC1B))));
+    MP_RET(fused ? band_reduce(x, N, (int)m, x.grad(dw, blk_param(c, l, B_FC1B)))
+                 : colsum(x, x.dt, du, m, N, (int)m, x.grad(dw, blk_param(c, l, B_FC1B))));
     MP_CHECK(ss.release(FREE_DU));
     {
       GemmArgs a = ga(du, m, x.W(blk_param(c, l, B_FC1W)), h, N, h, m, dx32, h);

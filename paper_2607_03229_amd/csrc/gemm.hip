@@ -335,20 +335,30 @@ hipError_t dispatch_epi(const GemmArgs& a, int epi, hipStream_t s) {
 // Host entry: layout = NT (fwd), NN (dX) or TN (dW); requirements checked by the caller:
 // K-contiguous operands need K % VEC == 0 and ld % VEC == 0; K-major operands need
 // their column count and ld to be multiples of VEC; all pointers 16-byte aligned.
+namespace {
+// The big kernels (bf16, M >= 512, N >= 256) have 16-byte vector epilogues only: every
+// output/aux row stride must keep 16-byte alignment, else the general kernel takes the
+// problem.
+bool takes_big(int dtype, int epi, const GemmArgs& a) {
+  if (!(dtype == DT_BF16 && a.M >= 512 && a.N >= 256 && a.N % 8 == 0)) return false;
+  auto al16 = [](const void* q) { return (reinterpret_cast<uintptr_t>(q) & 15) == 0; };
+  const bool f32out = epi == EPI_RESID || epi == EPI_F32;
+  const int64_t vq = f32out ? 4 : 8;
+  return al16(a.C) && a.ldc % vq == 0 && (a.bias == nullptr || al16(a.bias)) &&
+         (a.aux == nullptr || (al16(a.aux) && a.ld_aux % (epi == EPI_RESID ? 4 : 8) == 0)) &&
+         (a.C2 == nullptr || (al16(a.C2) && a.ldc2 % 8 == 0)) &&
+         (epi != EPI_F32 || a.split_stride % 4 == 0);
+}
+}  // namespace
+
+bool gemm_fused_colsum(int dtype, int layout, int epi, const GemmArgs& a) {
+  return layout == GEMM_NN && epi == EPI_GELU_BWD && a.kps <= 0 && takes_big(dtype, epi, a);
+}
+
 hipError_t gemm(int dtype, int layout, int epi, const GemmArgs& a, hipStream_t s) {
   if (a.M <= 0 || a.N <= 0) return hipSuccess;
-  if (dtype == DT_BF16 && a.M >= 512 && a.N >= 256 && a.N % 8 == 0) {
-    // the 256x256 kernel's epilogue is 16-byte vectors only: every output/aux row stride
-    // must keep 16-byte alignment, else the general kernel takes the problem
-    auto al16 = [](const void* q) { return (reinterpret_cast<uintptr_t>(q) & 15) == 0; };
-    const bool f32out = epi == EPI_RESID || epi == EPI_F32;
-    const int64_t vq = f32out ? 4 : 8;
-    const bool vec = al16(a.C) && a.ldc % vq == 0 && (a.bias == nullptr || al16(a.bias)) &&
-                     (a.aux == nullptr || (al16(a.aux) && a.ld_aux % (epi == EPI_RESID ? 4 : 8) == 0)) &&
-                     (a.C2 == nullptr || (al16(a.C2) && a.ldc2 % 8 == 0)) &&
-                     (epi != EPI_F32 || a.split_stride % 4 == 0);
-    if (vec) return gemm_big(layout, epi, a, s);
-  }
+  if (a.colsum && !gemm_fused_colsum(dtype, layout, epi, a)) return hipErrorInvalidValue;
+  if (takes_big(dtype, epi, a)) return gemm_big(layout, epi, a, s);
   if (dtype == DT_BF16) {
     switch (layout) {
       case GEMM_NT: return dispatch_epi<bf16, false, false>(a, epi, s);

@@ -149,7 +149,8 @@ __device__ __forceinline__ void aux_fetch(const GemmArgs& p, int split, int m, i
 
 template <int EPI>
 __device__ __forceinline__ void epi8_vec(const GemmArgs& p, int split, int m, int n, float* v,
-                                         const float* bias8, const AuxV& ax) {
+                                         const float* bias8, const AuxV& ax,
+                                         float* sum8 = nullptr) {
 #pragma unroll
   for (int e = 0; e < 8; ++e) v[e] += bias8[e];
   if constexpr (EPI == EPI_STORE || EPI == EPI_GELU || EPI == EPI_GELU_BWD) {
@@ -176,6 +177,10 @@ __device__ __forceinline__ void epi8_vec(const GemmArgs& p, int split, int m, in
       const bf16* g8 = reinterpret_cast<const bf16*>(&ax.v[0]);
 #pragma unroll
       for (int e = 0; e < 8; ++e) o[e] = (bf16)(v[e] * (float)g8[e]);
+      if (sum8) {   // column sums of what is stored (the next bias gradient)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) sum8[e] += (float)o[e];
+      }
     }
     *reinterpret_cast<uint4*>(reinterpret_cast<bf16*>(p.C) + (int64_t)m * p.ldc + n) =
         *reinterpret_cast<const uint4*>(o);
@@ -830,6 +835,11 @@ __global__ __launch_bounds__(NTHR, 2) void gemm_nn_kernel(GemmArgs p) {
     for (int e = 0; e < 8; ++e) bias8[e] = (float)b8[e];
   }
   auto row_of = [&](int pi, int u) { return m0 + wm * 64 + 16 * pi + (l >> 4) + 4 * u; };
+  // GELU-backward column sums over this wave's 64-row band (p.colsum is grid-uniform)
+  const bool kSum = EPI == EPI_GELU_BWD && p.colsum != nullptr;
+  float cs[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) cs[e] = 0.f;
   constexpr bool kAux = EPI == EPI_GELU_BWD || EPI == EPI_RESID || EPI == EPI_F32;
   AuxV ax[2][4];
   auto fetch = [&](int pi, AuxV (&dst)[4]) __attribute__((always_inline)) {
@@ -866,7 +876,7 @@ __global__ __launch_bounds__(NTHR, 2) void gemm_nn_kernel(GemmArgs p) {
         const float4 x1 = *reinterpret_cast<const float4*>(stage + rr * SP + 8 * cg + 4);
         v[0] = x0.x; v[1] = x0.y; v[2] = x0.z; v[3] = x0.w;
         v[4] = x1.x; v[5] = x1.y; v[6] = x1.z; v[7] = x1.w;
-        epi8_vec<EPI>(p, split, m, n, v, bias8, a);
+        epi8_vec<EPI>(p, split, m, n, v, bias8, a, kSum ? cs : nullptr);
       };
       if constexpr (kAux) {
 #pragma unroll
@@ -875,6 +885,21 @@ __global__ __launch_bounds__(NTHR, 2) void gemm_nn_kernel(GemmArgs p) {
 #pragma unroll 1
         for (int u = 0; u < 4; ++u) out_row(u, ax[0][0]);
       }
+    }
+  }
+  if (kSum) {
+    // the four lanes of a column group hold rows l >> 4 = 0..3 of each staged quad:
+    // add them in a fixed order, then one lane writes the band's eight sums
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      cs[e] += __shfl_xor(cs[e], 16);
+      cs[e] += __shfl_xor(cs[e], 32);
+    }
+    const int band0 = m0 + wm * 64;
+    if ((l >> 4) == 0 && vec && band0 < p.M) {
+      float* dst = p.colsum + (int64_t)(band0 / 64) * p.N + n;
+      *reinterpret_cast<float4*>(dst) = make_float4(cs[0], cs[1], cs[2], cs[3]);
+      *reinterpret_cast<float4*>(dst + 4) = make_float4(cs[4], cs[5], cs[6], cs[7]);
     }
   }
 }

@@ -33,8 +33,15 @@ struct GemmArgs {
   void* C2 = nullptr;
   int64_t ldc2 = 0;
   int beta = 0;
+  // EPI_GELU_BWD on the 128x256 NN kernel only (gemm_fused_colsum says when): column sums
+  // of the stored output over each band of 64 rows, colsum[m / 64][n], fp32, row stride N
+  float* colsum = nullptr;
 };
 hipError_t gemm(int dtype, int layout, int epi, const GemmArgs& a, hipStream_t s);
+// Whether gemm() runs this problem on the NN kernel that can write GemmArgs::colsum.
+bool gemm_fused_colsum(int dtype, int layout, int epi, const GemmArgs& a);
+// out[c] += sum of part[r][c] over r < rows, in a fixed order (two stages).
+hipError_t partials_reduce(float* part, float* out, int64_t rows, int n, hipStream_t s);
 // 256x256-tile bf16 kernel (M >= 512, N >= 256), same contract as gemm()
 hipError_t gemm_big(int layout, int epi, const GemmArgs& a, hipStream_t s);
 

@@ -89,9 +89,17 @@ std::vector<float> rope_table(const Cfg& c, int positions) {
   return t;
 }
 
+// At most four K splits: each split adds an fp32 partial of the whole output, written
+// and read back by the reduction (ten splits of the qkv weight gradient moved 400 MB),
+// and the weight-gradient GEMMs share the chip with the caller's stream anyway.
+// Measured against a cap of 16 at the Qwen2-VL shape: 292.7 -> 290.4 ms/step with the
+// side stream, 304.3 -> 293.5 ms/step without it.
+constexpr int64_t kMaxSplitK = 4;
+
 GemmSplit choose_split(int64_t M, int64_t N, int64_t K) {
   // Weight-gradient GEMMs have few output tiles and a long K (tokens): split K so
-  // the grid fills whole rounds of 256 CUs (each split keeps >= 1024 rows of K).
+  // the grid fills whole rounds of 256 CUs as far as the cap allows (each split keeps
+  // >= 1024 rows of K).
   // Tile size follows the kernel the GEMM dispatches to (256 when M >= 512, N >= 256).
   const bool big = M >= 512 && N >= 256;
   const int64_t t = big ? 256 : 128;
@@ -99,7 +107,7 @@ GemmSplit choose_split(int64_t M, int64_t N, int64_t K) {
   const int64_t per_round = big ? 256 : 512;
   int64_t best = 1;
   double best_eff = 0.0;
-  for (int64_t s = 1; s <= 16; ++s) {
+  for (int64_t s = 1; s <= kMaxSplitK; ++s) {
     if (s > 1 && K / s < 1024) break;
     const int64_t blocks = tiles * s;
     const int64_t rounds = (blocks + per_round - 1) / per_round;
@@ -304,6 +312,8 @@ int build_plan(const Cfg& c, const int32_t* cu, int n_seg, const int32_t* thw, i
     // (own region: the backward runs the remaining column sums on its side stream)
     p.ws_part = ws.take((size_t)kPartialRowsMax * 6 * h * 4);
     p.ws_cpart = ws.take((size_t)kPartialRowsMax * widest * 4);
+    // GELU-backward column sums per 64-row band, written by the input-gradient GEMM of fc1
+    p.ws_gpart = ws.take((size_t)((std::max(N, Tm) + 63) / 64) * std::max(m, 4 * h) * 4);
     // largest split-K partial over the weight-gradient GEMMs
     size_t dw = 0;
     auto need = [&](int64_t M_, int64_t N_, int64_t K_) {
