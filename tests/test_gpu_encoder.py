@@ -235,6 +235,58 @@ def test_full_size_forward_sampled(name):
         assert np.isfinite(host(out["dw"])).all()
 
 
+def test_full_size_backward_sampled_and_relocated():
+    """The benchmark's trained micro-batch at full size, launched as the benchmark launches
+    it (side stream on), with the patch gradient requested:
+    (a) the smallest item's merged rows and patch gradient against the oracle run on that
+        item alone (items are independent: block-diagonal attention, row-wise elsewhere);
+    (b) encoding three owner groups separately gives the same merged rows bit for bit and
+        weight gradients that sum to the full run's, up to fp32 summation order
+        (relocation, Sec. 4.2)."""
+    wl = W.make_workload("c4_qwen2vl_trained", 0)
+    cfg = wl.cfg
+    w, X, dM = wl.weights(), wl.patches(), wl.d_merged()
+    cu, grid = np.asarray(wl.cu_seqlens), np.asarray(wl.grid_thw)
+    announce(f"full-size fwd+bwd c4_qwen2vl_trained N={wl.n_patches} items={wl.n_items}")
+    full = GpuRun(cfg, w, X, cu, grid).run(True, d_merged=dM, want_dx=True)
+    assert full["status"] == 0
+    merged, dx, dw_full = host(full["merged"]), host(full["dx"]), host(full["dw"])
+    del full
+    assert np.isfinite(dw_full).all() and np.isfinite(dx).all()
+    mo = np.concatenate([[0], np.cumsum(wl.merged_per_item)])
+    # (a) one item alone on the oracle
+    i = _smallest_items(wl, 1)[0]
+    sl, ms = slice(int(cu[i]), int(cu[i + 1])), slice(int(mo[i]), int(mo[i + 1]))
+    n = sl.stop - sl.start
+    announce(f"oracle: item {i} alone ({n} patches, 32 blocks)")
+    rc, rM, _, rdx = oracle.encoder(cfg, w, X[sl], [0, n], grid[i:i + 1], True,
+                                    d_merged=dM[ms], want_d_patches=True)
+    assert rc == 0
+    em, ex = max_rel(merged[ms], rM), max_rel(dx[sl], rdx)
+    print(f"item {i} ({n} patches): merged max-rel {em:.2e}, d_patches max-rel {ex:.2e}")
+    assert em < TOL["bf16"] and ex < TOL["bf16"]
+    # (b) three owner groups
+    dw_sum = np.zeros(dw_full.shape)
+    for k in range(3):
+        grp = list(range(k, wl.n_items, 3))
+        announce(f"owner group {k}: items {grp}")
+        Xg = np.concatenate([X[cu[j]:cu[j + 1]] for j in grp])
+        gg = grid[grp]
+        cug = np.concatenate([[0], np.cumsum(gg[:, 0] * gg[:, 1] * gg[:, 2])]).astype(np.int32)
+        dMg = np.concatenate([dM[mo[j]:mo[j + 1]] for j in grp])
+        r = GpuRun(cfg, w, Xg, cug, gg).run(True, d_merged=dMg)
+        mg = host(r["merged"])
+        mgo = np.concatenate([[0], np.cumsum([wl.merged_per_item[j] for j in grp])])
+        for t, j in enumerate(grp):
+            assert np.array_equal(mg[mgo[t]:mgo[t + 1]], merged[mo[j]:mo[j + 1]]), j
+        dw_sum += host(r["dw"])
+        del r
+    errs = _per_tensor_errors(cfg, dw_sum, dw_full)
+    worst = max(errs, key=errs.get)
+    print(f"relocated weight gradients: worst {worst} {errs[worst]:.2e}")
+    assert errs[worst] < 1e-4
+
+
 def test_full_depth_gradients_one_item():
     """Qwen2-VL-ViT shape at full depth (32 layers): weight and patch gradients
     of one 256-patch image against the oracle."""
