@@ -210,7 +210,8 @@ def _smallest_items(wl, k):
     return sorted(np.argsort(n, kind="stable")[:k].tolist())
 
 
-@pytest.mark.parametrize("name", ["c2_vitl_frozen", "c4_qwen2vl_trained"])
+@pytest.mark.parametrize("name", ["c2_vitl_frozen", "c3_vitl_trained", "c4_qwen2vl_trained",
+                                  "c5_mixed_f05_trained"])
 def test_full_size_forward_sampled(name):
     """Full micro-batch on the GPU; the oracle recomputes the smallest item alone
     (valid by the block-diagonal independence of items)."""
