@@ -201,6 +201,42 @@ def test_rope(dtype, heads, d):
 ATTN_LENS = [1, 5, 64, 127, 128, 129, 300, 16, 1000, 705]
 
 
+def test_attention_longest_segments():
+    """The longest segments the workloads hold: a 1344 x 1344 image (9,216 patches) and a
+    ragged 8,229-row segment, d = 80, forward and backward against the oracle.  Many key
+    tiles per query test the lazily moved softmax offset and the long accumulations."""
+    import paper_2607_03229_amd as mp
+    torch, dev = torch_dev()
+    lens = [9216, 8229]
+    heads, d = 2, 80
+    h = heads * d
+    rng = np.random.default_rng(77)
+    cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    N = int(cu[-1])
+    announce(f"attention longest segments {lens} heads={heads} d={d}")
+    qkv = rnd(rng, (N, 3 * h), "bf16", 1.5)
+    q, k, v = qkv[:, :h], qkv[:, h:2 * h], qkv[:, 2 * h:]
+    tq = to_dev(qkv, "bf16")
+    o, lse = zeros((N, h), "bf16"), zeros((heads, N), "f32")
+    scratch = torch.empty(mp.op_scratch_bytes(N, heads, h, len(lens)), dtype=torch.uint8,
+                          device=dev)
+    mp.op_attention_fwd(_dt("bf16"), tq, N, heads, d, cu, o, lse, scratch)
+    dO = rnd(rng, (N, h), "bf16")
+    dqkv = zeros((N, 3 * h), "bf16")
+    mp.op_attention_bwd(_dt("bf16"), tq, o, to_dev(dO, "bf16"), lse, N, heads, d, cu, dqkv,
+                        scratch)
+    got_o, got_lse, got = host(o), host(lse), host(dqkv)
+    ro, rlse = oracle.attention(q, k, v, cu, heads, d)
+    assert max_rel(got_o, ro) < 2e-2
+    assert max_rel(got_lse, rlse.T) < 1e-3
+    rdq, rdk, rdv = oracle.attention_bwd(q, k, v, ro, dO, rlse, cu, heads, d)
+    for name, sl, ref in (("dq", slice(0, h), rdq), ("dk", slice(h, 2 * h), rdk),
+                          ("dv", slice(2 * h, 3 * h), rdv)):
+        err = max_rel(got[:, sl], ref)
+        print(f"longest segments {name}: max-rel {err:.2e}")
+        assert err < 3e-2, (name, err)
+
+
 @pytest.mark.parametrize("dtype,heads,d", [("bf16", 2, 80), ("bf16", 2, 64), ("bf16", 3, 32),
                                            ("f32", 2, 32)])
 def test_attention_fwd_bwd(dtype, heads, d):
