@@ -24,7 +24,6 @@
 namespace mpipe {
 namespace {
 
-constexpr int NTHR = 256;
 // 16-row sub-tiles per wave (NS) of the bf16 kernels; a 128-row work tile takes 8 / NS
 // waves.  NS = 4 reuses each LDS fragment over four MFMAs (half the LDS traffic of NS = 2)
 // at one wave per SIMD; NS = 2 runs several blocks of four waves per CU: three for the
@@ -213,7 +212,7 @@ __device__ __forceinline__ bf16x8 frag_trt(const uint4* tile, int k0a, int k0b, 
 template <int D, int NS>
 __global__ __launch_bounds__(64 * (8 / NS), NS == 2 ? 3 : 1) void attn_fwd_kernel(AttnArgs p) {
   constexpr int NW = 8 / NS, RW = 16 * NS;   // waves per block, rows per wave
-  constexpr int NDT = AD<D>::NDT, SL = TG<D, NW>::SLOTS, NI = TG<D, NW>::NI;
+  constexpr int NDT = AD<D>::NDT, SL = TG<D, NW>::SLOTS;
   __shared__ uint4 k0s[SL], k1s[SL], v0s[SL], v1s[SL];
   const int work = blockIdx.x / p.heads, head = blockIdx.x % p.heads;
   const int4 wk = p.work[work];
@@ -499,7 +498,7 @@ __global__ __launch_bounds__(64 * (8 / NS), NS == 2 ? 2 : 1) void attn_bwd_dkdv_
 template <int D, int NS>
 __global__ __launch_bounds__(64 * (8 / NS), NS == 2 ? 3 : 1) void attn_bwd_dq_kernel(AttnArgs p) {
   constexpr int NW = 8 / NS, RW = 16 * NS;   // waves per block, rows per wave
-  constexpr int NDT = AD<D>::NDT, SL = TG<D, NW>::SLOTS, NI = TG<D, NW>::NI;
+  constexpr int NDT = AD<D>::NDT, SL = TG<D, NW>::SLOTS;
   __shared__ uint4 k0s[SL], k1s[SL], v0s[SL], v1s[SL];
   const int work = blockIdx.x / p.heads, head = blockIdx.x % p.heads;
   const int4 wk = p.work[work];

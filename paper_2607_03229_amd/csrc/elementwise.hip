@@ -588,6 +588,7 @@ int64_t resident_blocks(K kernel, int threads) {
 // calls f(integral_constant<int, MC>) for the float4-per-lane count of a LayerNorm row
 template <class F>
 bool dispatch_mc(int mc, F&& f) {
+  static_assert(MAXC == 8, "one case per chunk count up to MAXC");
   switch (mc) {
     case 1: f(std::integral_constant<int, 1>{}); return true;
     case 2: f(std::integral_constant<int, 2>{}); return true;

@@ -78,10 +78,15 @@ template <class F>
 hipError_t run(mpipe_encoder* e, hipStream_t s, const char* cls, double flops, F&& f) {
   if (!e || !e->prof) return f();
   hipEvent_t a = e->event(), b = e->event();
-  if (a) hipEventRecord(a, s);
+  const bool ra = a && hipEventRecord(a, s) == hipSuccess;
   hipError_t r = f();
-  if (b) hipEventRecord(b, s);
-  if (a && b) e->recs.push_back({cls, a, b, flops, e->side != nullptr && s == e->side});
+  const bool rb = b && hipEventRecord(b, s) == hipSuccess;
+  if (ra && rb) {
+    e->recs.push_back({cls, a, b, flops, e->side != nullptr && s == e->side});
+  } else {   // an event that could not be recorded times nothing: give both back
+    if (a) e->pool.push_back(a);
+    if (b) e->pool.push_back(b);
+  }
   return r;
 }
 
@@ -234,11 +239,11 @@ hipError_t ensure_side(mpipe_encoder* e) {
   hipError_t r = hipGetDevice(&dev);
   if (r != hipSuccess) return r;
   if (e->side && e->side_dev == dev) return hipSuccess;
-  if (e->side) {
-    hipStreamSynchronize(e->side);
-    hipStreamDestroy(e->side);
+  if (e->side) {   // the handle moved to another device: rebuild its side stream there
+    (void)hipStreamSynchronize(e->side);
+    (void)hipStreamDestroy(e->side);
     for (auto& ev : e->sync) {
-      if (ev) hipEventDestroy(ev);
+      if (ev) (void)hipEventDestroy(ev);
       ev = nullptr;
     }
     e->side = nullptr;
@@ -680,20 +685,21 @@ mpipe_status mpipe_encoder_create(const mpipe_encoder_cfg* cfg, mpipe_encoder** 
 
 void mpipe_encoder_destroy(mpipe_encoder* e) {
   if (!e) return;
-  if (e->staging_pending && e->staging_ev) hipEventSynchronize(e->staging_ev);
-  if (e->staging) hipHostFree(e->staging);
-  if (e->staging_ev) hipEventDestroy(e->staging_ev);
+  // teardown has no caller to report to: each release is attempted regardless
+  if (e->staging_pending && e->staging_ev) (void)hipEventSynchronize(e->staging_ev);
+  if (e->staging) (void)hipHostFree(e->staging);
+  if (e->staging_ev) (void)hipEventDestroy(e->staging_ev);
   for (auto& r : e->recs) {
-    hipEventDestroy(r.a);
-    hipEventDestroy(r.b);
+    (void)hipEventDestroy(r.a);
+    (void)hipEventDestroy(r.b);
   }
-  for (auto ev : e->pool) hipEventDestroy(ev);
+  for (auto ev : e->pool) (void)hipEventDestroy(ev);
   if (e->side) {
-    hipStreamSynchronize(e->side);
-    hipStreamDestroy(e->side);
+    (void)hipStreamSynchronize(e->side);
+    (void)hipStreamDestroy(e->side);
   }
   for (auto ev : e->sync)
-    if (ev) hipEventDestroy(ev);
+    if (ev) (void)hipEventDestroy(ev);
   delete e;
 }
 
@@ -885,7 +891,7 @@ int32_t mpipe_profile_read(mpipe_encoder* e, void* stream, int32_t cap, char* na
   std::map<std::string, std::tuple<int64_t, double, double>> agg;
   for (auto& r : e->recs) {
     float t = 0.f;
-    hipEventElapsedTime(&t, r.a, r.b);
+    if (hipEventElapsedTime(&t, r.a, r.b) != hipSuccess) t = 0.f;   // counted, timed as 0
     auto& v = agg[r.side ? r.cls + "@side" : r.cls];
     std::get<0>(v) += 1;
     std::get<1>(v) += t;

@@ -255,7 +255,7 @@ mpipe_status mpipe_owner_map(const double* cost, int32_t n_mb, const double* war
     greedy(cost, n_mb, warmup, n_ranks, owner);
     if (method != MPIPE_OWNER_GREEDY) refine(cost, n_mb, warmup, n_ranks, owner);
     if (method == MPIPE_OWNER_EXACT) {
-      Exact x{cost, warmup, n_mb, n_ranks};
+      Exact x{cost, warmup, n_mb, n_ranks, {}, {}, {}, {}, {}};
       x.ord.resize(n_mb);
       std::iota(x.ord.begin(), x.ord.end(), 0);
       std::stable_sort(x.ord.begin(), x.ord.end(), [&](int a, int b) { return cost[a] > cost[b]; });
