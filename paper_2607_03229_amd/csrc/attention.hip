@@ -34,7 +34,11 @@ constexpr int FWD_NS = 2, DQ_NS = 2, DKDV_NS = 2;
 
 template <int D> struct AD {
   static constexpr int NC = D / 8;                          // 16-byte chunks per row
-  static constexpr int PC = (NC % 2 == 0) ? NC + 1 : NC;    // odd pitch: conflict-free reads
+  // d = 80: rows of 10 chunks with chunk c of row R stored at c ^ ((R >> 3) & 1), which
+  // keeps both the 16-row row-fragment reads and the 8-row transposing reads on distinct
+  // banks; other widths: an odd pitch (conflict-free row-fragment reads)
+  static constexpr bool SWZ = (D == 80);
+  static constexpr int PC = SWZ ? NC : (NC % 2 == 0) ? NC + 1 : NC;
   static constexpr int NF = D / 32;                         // full 32-wide K steps over d
   static constexpr bool REM = (D % 32) != 0;                // a last, partial 32-wide step
   static constexpr int NS32 = (D + 31) / 32;                // 32-wide K steps, padded
@@ -43,17 +47,26 @@ template <int D> struct AD {
 
 // ---- LDS tile helpers ------------------------------------------------------------
 
-// A/B fragment of a 16x16x32 MFMA from a row tile: row `row`, d in [32f + 8g, +8)
+// Stored position of chunk c of tile row `row` (see AD::SWZ).  The same XOR maps a stored
+// position back to its chunk.
 template <int D>
-__device__ __forceinline__ bf16x8 frag_row(const uint4* rowt, int row, int f, int g) {
-  uint4 v = rowt[row * AD<D>::PC + 4 * f + g];
+__device__ __forceinline__ int tile_chunk(int row, int c) {
+  return AD<D>::SWZ ? (c ^ ((row >> 3) & 1)) : c;
+}
+// A/B fragment of a 16x16x32 MFMA from a row tile: row rbase + r (rbase a multiple of 16,
+// r < 16), d in [32f + 8g, +8).  The swizzle bit of such a row is bit 3 of r, so only
+// the lane's own base moves and every fragment keeps a constant offset from it.
+template <int D>
+__device__ __forceinline__ bf16x8 frag_row(const uint4* rowt, int rbase, int r, int f, int g) {
+  const int sb = AD<D>::SWZ ? (r >> 3) & 1 : 0;
+  uint4 v = rowt[(rbase + r) * AD<D>::PC + 4 * f + (g ^ sb)];
   return *reinterpret_cast<bf16x8*>(&v);
 }
 // Register fragments of one row (query/key) straight from global memory, as 32-wide K
 // steps over d.  For d = 80 the third step is padded: lane groups 0-1 hold d 64..79 and
-// groups 2-3 hold zeros, so the matching LDS operand may read any finite data there (its
-// tile's pad chunk and the next row's first chunk), and every product over d is one chain
-// of 16x16x32 MFMAs.
+// groups 2-3 hold zeros, so the matching LDS operand may read any finite data there (the
+// first chunks of the next row, or the tile's filled pad slots past row 63), and every
+// product over d is one chain of 16x16x32 MFMAs.
 template <int D> struct RowFrag {
   bf16x8 f[AD<D>::NS32];
 };
@@ -74,13 +87,14 @@ __device__ __forceinline__ void load_rowfrag(RowFrag<D>& R, const bf16* X, int64
   }
 }
 
-// acc += A(row tile, rows arow..) x B(register fragment) over d
+// acc += A(row tile, rows rbase + 0..15) x B(register fragment) over d
 template <int D>
-__device__ __forceinline__ f32x4 dot_d(const uint4* rowt, int arow, const RowFrag<D>& B, int g,
-                                       f32x4 acc) {
+__device__ __forceinline__ f32x4 dot_d(const uint4* rowt, int rbase, int r, const RowFrag<D>& B,
+                                       int g, f32x4 acc) {
 #pragma unroll
   for (int f = 0; f < AD<D>::NS32; ++f)
-    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(frag_row<D>(rowt, arow, f, g), B.f[f], acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(frag_row<D>(rowt, rbase, r, f, g), B.f[f], acc,
+                                                  0, 0, 0);
   return acc;
 }
 
@@ -96,8 +110,8 @@ __device__ __forceinline__ bf16x8 pack8(const f32x4& a, const f32x4& b) {
 }
 
 // ---- asynchronous tile pipeline ------------------------------------------------------
-// A tile is 64 rows x D of one head, stored row-major in LDS with an odd pitch of PC
-// 16-byte chunks (conflict-free row-fragment reads).  It is filled by 16-byte
+// A tile is 64 rows x D of one head, stored row-major in LDS with a pitch of PC 16-byte
+// chunks (tile_chunk gives a chunk's stored position).  It is filled by 16-byte
 // global->LDS DMA (global_load_lds): lane l of a wave instruction writes LDS slot
 // base + l, so each lane picks the source of its slot; pad slots duplicate chunk 0
 // and rows past the segment read a clamped (valid) row.  Transposed operands come
@@ -122,7 +136,7 @@ __device__ __forceinline__ void dma_tile(uint4* tile, const bf16* X, int64_t ld,
   for (int i = 0; i < TG<D, NW>::NI; ++i) {
     const int inst = i * NW + w;
     const int slot = inst * 64 + lane;
-    int row = slot / PC, ch = slot % PC;
+    int row = slot / PC, ch = tile_chunk<D>(row, slot % PC);
     ch = ch < NC ? ch : 0;
     row = row < 64 ? row : 63;   // slots past the 64 rows repeat the last row
     int grow = r0 + row;
@@ -143,7 +157,7 @@ __device__ __forceinline__ void tile_src_init(TileSrc<D, NW>& S, int64_t ld) {
 #pragma unroll
   for (int i = 0; i < TG<D, NW>::NI; ++i) {
     const int slot = (i * NW + w) * 64 + lane;
-    int row = slot / PC, ch = slot % PC;
+    int row = slot / PC, ch = tile_chunk<D>(row, slot % PC);
     ch = ch < NC ? ch : 0;
     row = row < 64 ? row : 63;
     S.off[i] = (int64_t)row * ld + 8 * ch;
@@ -179,17 +193,19 @@ __device__ __forceinline__ void lds_barrier() {
   __builtin_amdgcn_s_waitcnt(15 | (7 << 4) | (0 << 8) | (3 << 14));   // lgkmcnt(0)
   asm volatile("s_barrier" ::: "memory");
 }
-// Transposed fragment of a raw [row][d] tile: for the 16-lane group of this lane,
-// rows {k0a..k0a+3} then {k0b..k0b+3} at column c0 + (lane & 15).
+// Transposed fragment of a raw [row][d] tile: for the 16-lane group g of this lane, rows
+// {kb + 4g ..+3} then {kb + 16 + 4g ..+3} at column c0 + (lane & 15).
 template <int D>
-__device__ __forceinline__ bf16x8 frag_trt(const uint4* tile, int k0a, int k0b, int c0, int r) {
+__device__ __forceinline__ bf16x8 frag_trt(const uint4* tile, int kb, int c0, int g, int r) {
+  // rows kb + 4g + r/4 (first read) and 16 further (second read), kb a multiple of 8: the
+  // swizzle bit of those rows is bit 1 of g.  Lane r reads 8 bytes at column c0 + 4 (r mod 4).
   constexpr int PC = AD<D>::PC;
   const char* base = reinterpret_cast<const char*>(tile);
-  const int off = (r >> 2) * PC * 16 + (c0 + 4 * (r & 3)) * 2;
-  const s16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-      (lds_s16x4*)(base + k0a * PC * 16 + off));
-  const s16x4 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-      (lds_s16x4*)(base + k0b * PC * 16 + off));
+  const int sb = AD<D>::SWZ ? (g >> 1) & 1 : 0;
+  const int lane_off = ((4 * g + (r >> 2)) * PC + (((r & 3) >> 1) ^ sb)) * 16 + (r & 1) * 8;
+  const int off = (kb * PC + c0 / 8) * 16 + lane_off;
+  const s16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(base + off));
+  const s16x4 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(base + off + 16 * PC * 16));
   bf16x8 v;
   const bf16* pa = reinterpret_cast<const bf16*>(&a);
   const bf16* pb = reinterpret_cast<const bf16*>(&b);
@@ -273,7 +289,7 @@ __global__ __launch_bounds__(64 * (8 / NS), NS == 2 ? 3 : 1) void attn_fwd_kerne
     for (int kq = 0; kq < 4; ++kq)
 #pragma unroll
       for (int qs = 0; qs < NS; ++qs)
-        s[kq][qs] = dot_d<D>(kt_s, 16 * kq + r, qf[qs], g, f32x4{0.f, 0.f, 0.f, 0.f});
+        s[kq][qs] = dot_d<D>(kt_s, 16 * kq, r, qf[qs], g, f32x4{0.f, 0.f, 0.f, 0.f});
     // the next DMAs go out after the score MFMAs, not ahead of their fragment reads
     // (measured 3% faster on the Qwen2-VL segment mix)
     issue(t + 1, kn, vn);
@@ -323,7 +339,7 @@ __global__ __launch_bounds__(64 * (8 / NS), NS == 2 ? 3 : 1) void attn_fwd_kerne
     for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
       for (int kk = 0; kk < 2; ++kk) {
-        const bf16x8 a = frag_trt<D>(vt_s, 32 * kk + 4 * g, 32 * kk + 16 + 4 * g, 16 * dt, r);
+        const bf16x8 a = frag_trt<D>(vt_s, 32 * kk, 16 * dt, g, r);
 #pragma unroll
         for (int qs = 0; qs < NS; ++qs)
           o[qs][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb[qs][kk], o[qs][dt], 0, 0, 0);
@@ -426,7 +442,7 @@ __global__ __launch_bounds__(64 * (8 / NS), NS == 2 ? 2 : 1) void attn_bwd_dkdv_
       f32x4 P[2][NS], dS[2][NS];   // [query half][ks]
 #pragma unroll
       for (int h2 = 0; h2 < 2; ++h2) {
-        const int qrow = 16 * (2 * kk + h2) + r;
+        const int qb16 = 16 * (2 * kk + h2);
         const int q4 = 16 * (2 * kk + h2) + 4 * g;   // this lane's four queries
         const float4 lq = *reinterpret_cast<const float4*>(lse_s + q4);
         const float4 eq = *reinterpret_cast<const float4*>(del_s + q4);
@@ -434,8 +450,8 @@ __global__ __launch_bounds__(64 * (8 / NS), NS == 2 ? 2 : 1) void attn_bwd_dkdv_
         const float de[4] = {eq.x, eq.y, eq.z, eq.w};
 #pragma unroll
         for (int ks = 0; ks < NS; ++ks) {
-          f32x4 s = dot_d<D>(q_s, qrow, kf[ks], g, f32x4{0.f, 0.f, 0.f, 0.f});
-          f32x4 dp = dot_d<D>(do_s, qrow, vf[ks], g, f32x4{0.f, 0.f, 0.f, 0.f});
+          f32x4 s = dot_d<D>(q_s, qb16, r, kf[ks], g, f32x4{0.f, 0.f, 0.f, 0.f});
+          f32x4 dp = dot_d<D>(do_s, qb16, r, vf[ks], g, f32x4{0.f, 0.f, 0.f, 0.f});
 #pragma unroll
           for (int v = 0; v < 4; ++v) {
             const float pp = fast_exp2(fmaf(s[v], sl2, nl[v]));
@@ -462,8 +478,8 @@ __global__ __launch_bounds__(64 * (8 / NS), NS == 2 ? 2 : 1) void attn_bwd_dkdv_
         const bf16x8 ads = pack8(dS[0][ks], dS[1][ks]);
 #pragma unroll
         for (int dt = 0; dt < NDT; ++dt) {
-          const bf16x8 bdo = frag_trt<D>(do_s, 32 * kk + 4 * g, 32 * kk + 16 + 4 * g, 16 * dt, r);
-          const bf16x8 bq = frag_trt<D>(q_s, 32 * kk + 4 * g, 32 * kk + 16 + 4 * g, 16 * dt, r);
+          const bf16x8 bdo = frag_trt<D>(do_s, 32 * kk, 16 * dt, g, r);
+          const bf16x8 bq = frag_trt<D>(q_s, 32 * kk, 16 * dt, g, r);
           dv[ks][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ap, bdo, dv[ks][dt], 0, 0, 0);
           dk[ks][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ads, bq, dk[ks][dt], 0, 0, 0);
         }
@@ -567,8 +583,8 @@ __global__ __launch_bounds__(64 * (8 / NS), NS == 2 ? 3 : 1) void attn_bwd_dq_ke
     for (int kq = 0; kq < 4; ++kq)
 #pragma unroll
       for (int qs = 0; qs < NS; ++qs) {
-        f32x4 sv = dot_d<D>(k_s, 16 * kq + r, qf[qs], g, f32x4{0.f, 0.f, 0.f, 0.f});
-        f32x4 dp = dot_d<D>(v_s, 16 * kq + r, dof[qs], g, f32x4{0.f, 0.f, 0.f, 0.f});
+        f32x4 sv = dot_d<D>(k_s, 16 * kq, r, qf[qs], g, f32x4{0.f, 0.f, 0.f, 0.f});
+        f32x4 dp = dot_d<D>(v_s, 16 * kq, r, dof[qs], g, f32x4{0.f, 0.f, 0.f, 0.f});
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
           const float pp = fast_exp2(fmaf(sv[v], sl2, -lse2[qs]));
@@ -593,7 +609,7 @@ __global__ __launch_bounds__(64 * (8 / NS), NS == 2 ? 3 : 1) void attn_bwd_dq_ke
       for (int qs = 0; qs < NS; ++qs) b[qs] = pack8(ds[2 * kk][qs], ds[2 * kk + 1][qs]);
 #pragma unroll
       for (int dt = 0; dt < NDT; ++dt) {
-        const bf16x8 a = frag_trt<D>(k_s, 32 * kk + 4 * g, 32 * kk + 16 + 4 * g, 16 * dt, r);
+        const bf16x8 a = frag_trt<D>(k_s, 32 * kk, 16 * dt, g, r);
 #pragma unroll
         for (int qs = 0; qs < NS; ++qs)
           dq[qs][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b[qs], dq[qs][dt], 0, 0, 0);
