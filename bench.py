@@ -185,6 +185,66 @@ def copy_calibration():
     print(json.dumps({"copy_read_bytes": CAL_READ, "copy_write_bytes": CAL_WRITE}), flush=True)
 
 
+def gemm_vs_library(workload: str, seed: int):
+    """The encoder step's GEMM shapes, each run alone: the library's kernels against
+    torch.mm (hipBLASLt on ROCm) on the same bf16 operands, HIP-event timed.  The
+    weight gradients run the step's four-way K split (fp32 partials, the reduction
+    not timed) against hipBLASLt's single bf16-output product."""
+    import torch
+    import paper_2607_03229_amd as mp
+    import workload as W
+    dev = torch.device("cuda:0")
+    wl = W.make_workload(workload, seed)
+    T, h, f = int(wl.cu_seqlens[-1]), wl.cfg.hidden, wl.cfg.mlp
+
+    def tm(fn, reps=10):
+        fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps
+
+    g = torch.Generator(device=dev).manual_seed(seed)
+
+    def rnd(*shape):
+        return (torch.randn(*shape, device=dev, generator=g) * 0.5).to(torch.bfloat16)
+
+    def line(name, M, N, K, ours, lib):
+        fl = 2.0 * M * N * K
+        print(json.dumps({"gemm": name, "M": M, "N": N, "K": K,
+                          "ours_ms": round(ours, 3), "ours_tflops": round(fl / ours / 1e9, 1),
+                          "hipblaslt_ms": round(lib, 3), "hipblaslt_tflops": round(fl / lib / 1e9, 1)}),
+              flush=True)
+
+    # forward and input-gradient products: C[M][N] = A[M][K] B[K][N], bf16 out
+    for name, M, N, K in [("qkv_fwd", T, 3 * h, h), ("proj_fwd", T, h, h), ("fc1_fwd", T, f, h),
+                          ("fc2_fwd", T, h, f), ("qkv_dgrad", T, h, 3 * h)]:
+        A, B = rnd(M, K), rnd(K, N)
+        C = torch.empty(M, N, dtype=torch.bfloat16, device=dev)
+        bias = torch.zeros(N, dtype=torch.bfloat16, device=dev)
+        ours = tm(lambda: mp.op_gemm(mp.BF16, 1, 0, M, N, K, A, K, B, N, C, N, bias=bias))
+        lib = tm(lambda: torch.mm(A, B, out=C))
+        line(name, M, N, K, ours, lib)
+        del A, B, C
+    # weight gradients: C[M][N] = sum over tokens of A[k][M] B[k][N]
+    for name, M, N in [("qkv_wgrad", h, 3 * h), ("proj_wgrad", h, h), ("fc1_wgrad", h, f),
+                       ("fc2_wgrad", f, h)]:
+        A, B = rnd(T, M), rnd(T, N)
+        kps = (T // 4 + 63) // 64 * 64
+        C = torch.empty(4, M, N, dtype=torch.float32, device=dev)
+        ours = tm(lambda: mp.op_gemm(mp.BF16, 2, 4, M, N, T, A, M, B, N, C, N, k_per_split=kps,
+                                     split_stride=M * N))
+        Cb = torch.empty(M, N, dtype=torch.bfloat16, device=dev)
+        At = A.t()
+        lib = tm(lambda: torch.mm(At, B, out=Cb))
+        line(name, M, N, T, ours, lib)
+        del A, B, C, Cb
+
+
 def cpu_baseline(sample_layers: int = 8):
     """Time the CPU oracle on a bounded sample of the same workload shape: one
     224x224 image (256 patches, the smallest the size draw produces) through the
@@ -277,6 +337,8 @@ def main():
     ap.add_argument("--summarize-pmc", nargs=4, metavar=("FETCH_CAL", "WRITE_CAL", "FETCH", "WRITE"),
                     help="rocprofv3 PMC databases -> profiles/hbm_traffic.json")
     ap.add_argument("--pmc-commands", default="", help="commands recorded with --summarize-pmc")
+    ap.add_argument("--gemm-vs-library", action="store_true",
+                    help="only time the step's GEMM shapes alone, against torch.mm (hipBLASLt)")
     args = ap.parse_args()
     if args.summarize_pmc:
         summarize_pmc(*args.summarize_pmc, args.pmc_commands)
@@ -288,6 +350,9 @@ def main():
 
     if args.copy_calibration:
         copy_calibration()
+        return
+    if args.gemm_vs_library:
+        gemm_vs_library(args.workload, args.seed)
         return
     import torch
     import paper_2607_03229_amd as mp
