@@ -148,28 +148,26 @@ __global__ __launch_bounds__(256) void ln_bwd_kernel(const float* dY, int64_t ld
                                                      const float* dres, float* dX, T* dXt,
                                                      float* part_g, float* part_b, float* part_c) {
   __shared__ float4 red[4 * MC * 64];
+  __shared__ float4 gms[MC * 64];   // the gain, read from LDS per row (registers go to loads)
   const int wave = threadIdx.x >> 6, l = threadIdx.x & 63;
   const int nc = n / 4;
-  float4 ag[MC], ab[MC], ac[MC], gm[MC];
+  float4 ag[MC], ab[MC], ac[MC];
 #pragma unroll
-  for (int i = 0; i < MC; ++i) {
-    ag[i] = ab[i] = ac[i] = make_float4(0.f, 0.f, 0.f, 0.f);
-    const int c = l + 64 * i;
-    if (c < nc) gm[i] = V4<T>::load(gam + 4 * c);
-  }
+  for (int i = 0; i < MC; ++i) ag[i] = ab[i] = ac[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int c = threadIdx.x; c < nc; c += 256) gms[c] = V4<T>::load(gam + 4 * c);
+  __syncthreads();
   const int64_t r0 = (int64_t)blockIdx.x * rows_per_block;
   const int64_t r1 = min(rows, r0 + rows_per_block);
   for (int64_t row = r0 + wave; row < r1; row += 4) {
     const float mu = mean[row], rs = rstd[row];
     // every operand of the row is requested before any is used
-    float4 x[MC], dy[MC], dr[MC];
+    float4 x[MC], dy[MC];
 #pragma unroll
     for (int i = 0; i < MC; ++i) {
       const int c = l + 64 * i;
       if (c < nc) {
         x[i] = V4<float>::load(X + row * ldx + 4 * c);
         dy[i] = V4<float>::load(dY + row * ldd + 4 * c);
-        dr[i] = dres ? V4<float>::load(dres + row * ldx + 4 * c) : make_float4(0.f, 0.f, 0.f, 0.f);
       }
     }
     float s1 = 0.f, s2 = 0.f;
@@ -179,8 +177,9 @@ __global__ __launch_bounds__(256) void ln_bwd_kernel(const float* dY, int64_t ld
       if (c < nc) {
         x[i] = make_float4((x[i].x - mu) * rs, (x[i].y - mu) * rs, (x[i].z - mu) * rs,
                            (x[i].w - mu) * rs);   // now xhat
-        const float4 gd = make_float4(dy[i].x * gm[i].x, dy[i].y * gm[i].y, dy[i].z * gm[i].z,
-                                      dy[i].w * gm[i].w);
+        const float4 gm = gms[c];
+        const float4 gd = make_float4(dy[i].x * gm.x, dy[i].y * gm.y, dy[i].z * gm.z,
+                                      dy[i].w * gm.w);
         s1 += gd.x + gd.y + gd.z + gd.w;
         s2 += gd.x * x[i].x + gd.y * x[i].y + gd.z * x[i].z + gd.w * x[i].w;
         ag[i].x += dy[i].x * x[i].x; ag[i].y += dy[i].y * x[i].y;
@@ -195,11 +194,14 @@ __global__ __launch_bounds__(256) void ln_bwd_kernel(const float* dY, int64_t ld
     for (int i = 0; i < MC; ++i) {
       const int c = l + 64 * i;
       if (c < nc) {
+        const float4 gm = gms[c];
+        const float4 dr =
+            dres ? V4<float>::load(dres + row * ldx + 4 * c) : make_float4(0.f, 0.f, 0.f, 0.f);
         float4 o;
-        o.x = rs * (dy[i].x * gm[i].x - s1 - x[i].x * s2) + dr[i].x;
-        o.y = rs * (dy[i].y * gm[i].y - s1 - x[i].y * s2) + dr[i].y;
-        o.z = rs * (dy[i].z * gm[i].z - s1 - x[i].z * s2) + dr[i].z;
-        o.w = rs * (dy[i].w * gm[i].w - s1 - x[i].w * s2) + dr[i].w;
+        o.x = rs * (dy[i].x * gm.x - s1 - x[i].x * s2) + dr.x;
+        o.y = rs * (dy[i].y * gm.y - s1 - x[i].y * s2) + dr.y;
+        o.z = rs * (dy[i].z * gm.z - s1 - x[i].z * s2) + dr.z;
+        o.w = rs * (dy[i].w * gm.w - s1 - x[i].w * s2) + dr.w;
         V4<float>::store(dX + row * ldx + 4 * c, o);
         if (dXt) V4<T>::store(dXt + row * ldx + 4 * c, o);
         ac[i].x += o.x; ac[i].y += o.y; ac[i].z += o.z; ac[i].w += o.w;
