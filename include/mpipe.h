@@ -38,7 +38,8 @@
  *             (tau, hb, wb, dh, dw), patch position y = 2hb + dh, x = 2wb + dw,
  *             so every 2x2 merge window is four consecutive rows; a patch
  *             vector is flattened as (channel, frame, py, px).
- *   grid_thw  host int32 [n_items][3] = (t, gh, gw) in patches; gh, gw even.
+ *   grid_thw  host int32 [n_items][3] = (t, gh, gw) in patches; gh, gw even
+ *             and at most 32768 (a row's (y, x) is packed in 15 bits each).
  *   cu_seqlens host int32 [n_seg + 1], attention segments over the packed rows:
  *             0 = cu[0] < cu[1] < ... < cu[n_seg] = N; each segment lies inside
  *             one item and starts/ends on a temporal-slice boundary of it (one

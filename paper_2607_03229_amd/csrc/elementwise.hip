@@ -475,7 +475,7 @@ __global__ void rope_kernel(T* qk, int64_t ld, int64_t rows, int heads, int d, i
   const int which = rem / (heads * groups);
   rem %= heads * groups;
   const int hd = rem / groups, j0 = 4 * (rem % groups);
-  const int32_t pp = pos[r];
+  const uint32_t pp = (uint32_t)pos[r];
   T* v = qk + r * ld + (which ? kcol : 0) + hd * d;
   const float4 a = V4<T>::load(v + j0), b = V4<T>::load(v + j0 + half);
   const float x1[4] = {a.x, a.y, a.z, a.w}, x2[4] = {b.x, b.y, b.z, b.w};
@@ -483,7 +483,7 @@ __global__ void rope_kernel(T* qk, int64_t ld, int64_t rows, int heads, int d, i
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
     const int j = j0 + e;
-    const int coord = (j < quarter) ? (pp >> 16) : (pp & 0xFFFF);
+    const int coord = (int)((j < quarter) ? (pp >> 16) : (pp & 0xFFFFu));
     const float2 cs = tab[coord * quarter + (j < quarter ? j : j - quarter)];
     const float sn = inverse ? -cs.y : cs.y;
     o1[e] = x1[e] * cs.x - x2[e] * sn;
@@ -507,7 +507,7 @@ __global__ void rope8_kernel(T* qk, int64_t ld, int64_t rows, int heads, int d, 
   const int which = rem / (heads * groups);
   rem -= which * heads * groups;
   const int hd = rem / groups, j0 = 8 * (rem - hd * groups);
-  const int32_t pp = pos[r];
+  const uint32_t pp = (uint32_t)pos[r];
   T* v = qk + r * ld + (which ? kcol : 0) + hd * d;
   float4 a0, a1, b0, b1;
   V8<T>::load(v + j0, a0, a1);
@@ -518,7 +518,7 @@ __global__ void rope8_kernel(T* qk, int64_t ld, int64_t rows, int heads, int d, 
 #pragma unroll
   for (int e = 0; e < 8; ++e) {
     const int j = j0 + e;
-    const int coord = (j < quarter) ? (pp >> 16) : (pp & 0xFFFF);
+    const int coord = (int)((j < quarter) ? (pp >> 16) : (pp & 0xFFFFu));
     const float2 cs = tab[coord * quarter + (j < quarter ? j : j - quarter)];
     const float sn = inverse ? -cs.y : cs.y;
     o1[e] = x1[e] * cs.x - x2[e] * sn;

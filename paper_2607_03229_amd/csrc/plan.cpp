@@ -165,8 +165,10 @@ int build_plan(const Cfg& c, const int32_t* cu, int n_seg, const int32_t* thw, i
       err = "grid height and width must be even for the 2x2 merge (item " + std::to_string(i) + ")";
       return -2;
     }
-    if (gh > 65534 || gw > 65534) {
-      err = "grid too large";
+    // a row's position is packed as y << 16 | x into 32 bits: both sides stay below 2^15
+    if (gh > kMaxGridSide || gw > kMaxGridSide) {
+      err = "grid height and width must be at most " + std::to_string(kMaxGridSide) +
+            " patches (item " + std::to_string(i) + ")";
       return -2;
     }
     start[i] = N;

@@ -59,6 +59,10 @@ struct MergerSet {
   size_t um, gm;                 // [Tm][4h] pre-activation / GELU output
 };
 
+// Largest grid side (in patches) an item may have: positions are packed as y << 16 | x,
+// so each coordinate must fit in 15 bits.
+constexpr int kMaxGridSide = 32768;
+
 // Upper bound of the partial-sum rows of the deterministic column reductions (LayerNorm
 // backward blocks, column-sum chunks); the workspace holds this many rows per reduction.
 constexpr int64_t kPartialRowsMax = 1024;
@@ -80,7 +84,7 @@ struct Plan {
   bool trainable = false;          // mode == MODE_TRAINED: every layer records a tape
   int64_t sum_len2 = 0;          // sum over segments of len^2 (attention FLOPs)
   // host metadata, uploaded into the workspace head
-  std::vector<int32_t> pos;        // N: y << 16 | x
+  std::vector<int32_t> pos;        // N: y << 16 | x (y, x < kMaxGridSide)
   std::vector<int32_t> q_work;     // 4 ints per query tile (start, seg start, seg end, 0)
   std::vector<int32_t> k_work;     // 4 ints per key tile
   std::vector<float> rope_tab;     // (cos, sin) of p * theta^(-4k/d), [positions][d/4]

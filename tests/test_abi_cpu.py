@@ -84,6 +84,17 @@ def test_sizes_and_metadata_validation(L):
     assert enc.sizes(np.arange(0, 4 * 48 + 1, 48), gv, True)["n_patches"] == 192
     with pytest.raises(B.MpipeError):
         enc.sizes(np.array([0, 30, 192]), gv, True)
+    # grid sides: positions are packed y << 16 | x, so a side may be at most 32768 patches
+    # (a larger coordinate would reach the sign bit of the packed int32)
+    for side, ok in ((32768, True), (32770, False), (65534, False)):
+        for gg in (np.array([[1, side, 2]], np.int32), np.array([[1, 2, side]], np.int32)):
+            n = int(gg[0].prod())
+            if ok:
+                assert enc.sizes(np.array([0, n]), gg, False)["n_patches"] == n
+            else:
+                with pytest.raises(B.MpipeError) as e:
+                    enc.sizes(np.array([0, n]), gg, False)
+                assert e.value.status == -2
     # empty micro-batch (text only) is a valid no-op
     e0 = enc.sizes(np.array([0]), np.zeros((0, 3), np.int32), True)
     assert e0["n_patches"] == 0 and e0["n_merged"] == 0
