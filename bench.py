@@ -73,6 +73,11 @@ CAL_ROWS, CAL_COLS = 32768, 3584          # bf16 rows copied by the calibration 
 CAL_READ = CAL_ROWS * CAL_COLS * 2 + 8 * CAL_ROWS
 CAL_WRITE = CAL_ROWS * CAL_COLS * 2
 EPI_NAMES = ["store", "gelu", "resid", "gelubwd", "f32"]
+# What `traffic` counts: the TCC (L2) FETCH_SIZE + WRITE_SIZE counters, i.e. bytes moved
+# between the L2 and the data fabric.  Reads served by the 256 MB Infinity Cache are
+# included, so this bounds HBM traffic from above; it is per launch, like `achieved`.
+TRAFFIC_NOTE = ("L2<->fabric bytes per launch (TCC FETCH_SIZE + WRITE_SIZE, scaled by a "
+                "known-size copy; includes Infinity-Cache hits, so an upper bound on HBM bytes)")
 
 
 def source_digest() -> str:
@@ -245,37 +250,69 @@ def gemm_vs_library(workload: str, seed: int):
         del A, B, C, Cb
 
 
-def cpu_baseline(sample_layers: int = 8):
-    """Time the CPU oracle on a bounded sample of the same workload shape: one
-    224x224 image (256 patches, the smallest the size draw produces) through the
-    Qwen2-VL-ViT-shaped encoder truncated to `sample_layers` of its blocks (patch
-    embedding and merger included), forward and backward.  The measured time is
-    scaled to the full-depth encoder by the ratio of model FLOPs (every block
-    costs the same), and the sample is stated alongside."""
+def _prefix_sample(min_patches: int = 4096):
+    """The benchmark draw's own items (C4 workload, seed 0), in order, until at least
+    `min_patches` patches: the deterministic prefix the CPU baseline is timed on."""
+    import workload as W
+    wl = W.make_workload("c4_qwen2vl_trained", 0)
+    n = wl.grid_thw[:, 0] * wl.grid_thw[:, 1] * wl.grid_thw[:, 2]
+    k = int(np.searchsorted(np.cumsum(n), min_patches) + 1)
+    return wl.grid_thw[:k]
+
+
+def _time_oracle(layers: int, grid) -> tuple:
+    """Seconds of one oracle forward + backward (fp32, trained) of the Qwen2-VL-ViT shape
+    with `layers` blocks on the items `grid`, and the patch count."""
     import dataclasses
 
     import oracle
     import workload as W
-    full = W.CONFIGS["c4_qwen2vl_trained"].cfg
-    cfg = dataclasses.replace(full, layers=sample_layers)
-    W.custom_spec("cpu_baseline_sample", cfg)
-    wl = W.make_workload("cpu_baseline_sample", 0, grid_thw=np.array([[1, 16, 16]]))
+    cfg = dataclasses.replace(W.CONFIGS["c4_qwen2vl_trained"].cfg, layers=layers)
+    W.custom_spec(f"cpu_baseline_{layers}", cfg, emb_seqs=8, emb_seq_len=8192)
+    wl = W.make_workload(f"cpu_baseline_{layers}", 0, grid_thw=np.array(grid))
     w, X = wl.weights(), wl.patches()
-    dM = np.random.default_rng(0).standard_normal((wl.n_merged, cfg.llm_hidden))
+    dM = W.round_bf16(np.random.default_rng(0).standard_normal(
+        (wl.n_merged, cfg.llm_hidden)).astype(np.float32))
     t0 = time.perf_counter()
-    oracle.encoder(cfg, w, X, wl.cu_seqlens, wl.grid_thw, True, d_merged=dM)
-    dt = time.perf_counter() - t0
-    n = wl.n_patches
-    f_sample = model_flops(cfg, n, n * n, True)
-    f_full = model_flops(full, n, n * n, True)
-    t_full = dt * f_full / f_sample
-    return {"value": round(n / t_full, 4), "unit": "patch-tokens/s",
-            "cores": oracle.num_threads(), "kind": "oracle",
-            "sample": (f"one 224x224 image (256 patches), Qwen2-VL-ViT shape truncated to "
-                       f"{sample_layers} of 32 blocks, fp64 forward+backward incl. patch "
-                       f"embedding and merger: {dt:.1f} s measured, scaled by model FLOPs "
-                       f"({f_full / f_sample:.2f}x) to the full 32-block encoder"),
-            "cpu": _cpu_model()}
+    oracle.encoder(cfg, w, X, wl.cu_seqlens, wl.grid_thw, True, d_merged=dM, precision="f32")
+    return time.perf_counter() - t0, wl.n_patches
+
+
+def cpu_baseline(full_depth: bool = False):
+    """Time the CPU oracle (fp32, forward + backward, every part trainable) on the
+    deterministic prefix of the benchmark's own draw: its first items until >= 4,096
+    patches (5,336 patches, items 0-2, for seed 0).
+
+    Default (bounded, about a minute of CPU on 16 cores): the prefix is timed twice, with
+    0 blocks (patch embedding + merger) and with 1 block of the encoder; every block is
+    the same computation on the same rows, so the 32-block time is t0 + 32 (t1 - t0), both
+    terms measured on this draw.  full_depth=True times the prefix through all 32 blocks
+    in one run instead (about 15 minutes on 16 cores)."""
+    import oracle
+    grid = _prefix_sample()
+    host = _host_info()
+    host["omp_threads"] = oracle.num_threads()
+    if full_depth:
+        t, n = _time_oracle(32, grid)
+        return {"value": round(n / t, 3), "unit": "patch-tokens/s", "cores": host["omp_threads"],
+                "kind": "oracle",
+                "sample": (f"prefix of the benchmark draw (c4_qwen2vl_trained seed 0, items "
+                           f"0-{len(grid) - 1}, {n} patches), fp32 forward+backward, all 32 "
+                           f"blocks, patch embedding and merger: {t:.1f} s measured"),
+                **host}
+    t0, n = _time_oracle(0, grid)
+    log(f"cpu oracle: prefix of {n} patches, 0 blocks: {t0:.1f} s")
+    t1, _ = _time_oracle(1, grid)
+    log(f"cpu oracle: prefix of {n} patches, 1 block: {t1:.1f} s")
+    t_full = t0 + 32 * (t1 - t0)
+    return {"value": round(n / t_full, 3), "unit": "patch-tokens/s",
+            "cores": host["omp_threads"], "kind": "oracle",
+            "sample": (f"prefix of the benchmark draw (c4_qwen2vl_trained seed 0, items "
+                       f"0-{len(grid) - 1}, {n} patches), fp32 forward+backward incl. patch "
+                       f"embedding and merger, timed at 0 blocks ({t0:.1f} s) and 1 block "
+                       f"({t1:.1f} s); 32 blocks = t0 + 32 (t1 - t0) = {t_full:.0f} s"),
+            "measured_s": {"blocks0": round(t0, 2), "blocks1": round(t1, 2)},
+            **host}
 
 
 def owner_scenario(enc, wl, flops_per_s: float) -> dict:
@@ -312,14 +349,22 @@ def owner_scenario(enc, wl, flops_per_s: float) -> dict:
     return out
 
 
-def _cpu_model() -> str:
+def _host_info() -> dict:
+    """CPU model, sockets and the cores this process may run on."""
+    model, sockets = "unknown", set()
     try:
         for line in open("/proc/cpuinfo"):
-            if line.startswith("model name"):
-                return line.split(":", 1)[1].strip()
+            if line.startswith("model name") and model == "unknown":
+                model = line.split(":", 1)[1].strip()
+            elif line.startswith("physical id"):
+                sockets.add(line.split(":", 1)[1].strip())
     except OSError:
         pass
-    return "unknown"
+    try:
+        nproc = len(os.sched_getaffinity(0))
+    except AttributeError:
+        nproc = os.cpu_count() or 0
+    return {"cpu": model, "sockets": max(len(sockets), 1), "nproc": nproc}
 
 
 def main():
@@ -330,6 +375,11 @@ def main():
     ap.add_argument("--workload", default="c4_qwen2vl_trained")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-baseline-full", action="store_true",
+                    help="time the oracle's sample through all 32 blocks in one run "
+                         "(about 15 minutes on 16 cores) instead of at 0 and 1 blocks")
+    ap.add_argument("--cpu-baseline-only", action="store_true",
+                    help="only time the CPU oracle sample and print its JSON object")
     ap.add_argument("--no-profile", action="store_true",
                     help="skip the per-kernel event timing (roofline figures)")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -348,6 +398,9 @@ def main():
               "(see DESIGN.md for how the transpose schedule shards it).", file=sys.stderr)
         sys.exit(2)
 
+    if args.cpu_baseline_only:
+        print(json.dumps(cpu_baseline(full_depth=args.cpu_baseline_full)), flush=True)
+        return
     if args.copy_calibration:
         copy_calibration()
         return
@@ -395,10 +448,9 @@ def main():
         torch.cuda.synchronize()
         log(f"warmup step {i + 1}/{args.warmup} done")
     profile = not args.no_profile
-    if profile:
-        enc.profile(True)
-    # per-step HIP events on the stream (median / min); the whole-job figure is the host
-    # clock over all K steps, bracketed by device synchronisation
+    # Headline: K steps with no per-kernel instrumentation.  Per-step HIP events on the
+    # stream give the median / min; the whole-job figure is the host clock over all K
+    # steps, bracketed by device synchronisation.
     evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -410,8 +462,21 @@ def main():
     elapsed = time.perf_counter() - t0
     per_step = sorted(evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps))
     log(f"timed {args.steps} steps: {elapsed * 1e3 / args.steps:.1f} ms/step")
-    kern = enc.profile_read(stream) if profile else {}
-    enc.profile(False)
+    # Per-kernel figures from a separate pass: every launch bracketed by a HIP event pair
+    # on the stream it is launched on (the caller's, or the backward's side stream)
+    kern = {}
+    prof_steps = min(args.steps, 5)
+    if profile:
+        enc.profile(True)
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        for _ in range(prof_steps):
+            step()
+        torch.cuda.synchronize()
+        log(f"per-kernel pass: {prof_steps} steps, "
+            f"{(time.perf_counter() - t1) * 1e3 / prof_steps:.1f} ms/step with events")
+        kern = enc.profile_read(stream)
+        enc.profile(False)
 
     # scatter bandwidth, timed on its own
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -433,7 +498,7 @@ def main():
     achieved = flops / (ms_step * 1e-3) / 1e12
     peak = PEAK_BF16_TFLOPS if cfg.dtype == "bf16" else PEAK_F32_TFLOPS
 
-    roofline = None
+    roofline = roofline_top = None
     kernels = {}
     if kern:
         # kernel classes on the caller's stream form the critical path; the weight-gradient
@@ -444,17 +509,26 @@ def main():
                             "ms_avg": round(ms / max(n, 1), 4),
                             "tflops": round(fl / (ms * 1e-3) / 1e12, 1) if ms > 0 and fl > 0 else None,
                             "stream": "side" if side else "caller"}
-        main = [k for k in kernels if kernels[k]["stream"] == "caller" and kern[k][2] > 0]
-        dom = max(main or [k[:-5] if k.endswith("@side") else k for k in kern if kern[k][2] > 0],
-                  key=lambda k: kernels[k]["ms_total"])
-        key = dom if dom in kern else dom + "@side"
-        n, ms, fl = kern[key]
-        ach = fl / n / (ms / n * 1e-3) / 1e12
-        roofline = {"kernel": dom, "bound": "mfma", "achieved": round(ach, 1), "peak": peak,
+        def roof(cls):
+            key = cls if cls in kern else cls + "@side"
+            n, ms, fl = kern[key]
+            ach = fl / n / (ms / n * 1e-3) / 1e12
+            return {"kernel": cls, "bound": "mfma", "achieved": round(ach, 1), "peak": peak,
                     "unit": "TFLOP/s", "frac": round(ach / peak, 4),
-                    "traffic": stored_traffic(dom),
+                    "traffic": stored_traffic(cls),
+                    "traffic_counter": TRAFFIC_NOTE,
                     "launches": n, "avg_ms": round(ms / n, 4),
-                    "flop_per_launch": fl / n, "stream": kernels[dom]["stream"]}
+                    "flop_per_launch": fl / n, "stream": kernels[cls]["stream"],
+                    "timed_over_steps": prof_steps}
+
+        # the roofline kernel: the largest MFMA class on the caller's (critical) stream;
+        # beside it, the largest class of the whole trace when that is another one
+        mfma = [k for k in kernels if (kern.get(k) or kern.get(k + "@side"))[2] > 0]
+        main = [k for k in mfma if kernels[k]["stream"] == "caller"]
+        dom = max(main or mfma, key=lambda k: kernels[k]["ms_total"])
+        roofline = roof(dom)
+        top = max(mfma, key=lambda k: kernels[k]["ms_total"])
+        roofline_top = roof(top) if top != dom else None
 
     result = {
         "metric": METRIC,
@@ -481,12 +555,13 @@ def main():
         "scatter_GBps": round(scatter_gbps, 1),
         "scatter_pct_of_hbm": round(100 * scatter_gbps / PEAK_HBM_GBPS, 1),
         "roofline": roofline,
+        "roofline_largest_class": roofline_top if kern else None,
         "kernels": kernels,
     }
     result["owner_map"] = owner_scenario(enc, wl, flops / (ms_step * 1e-3))
     if not args.no_cpu_baseline:
-        log("timing the CPU oracle on its bounded sample")
-        result["cpu_baseline"] = cpu_baseline()
+        log("timing the CPU oracle on its sample (the benchmark draw's first items)")
+        result["cpu_baseline"] = cpu_baseline(full_depth=args.cpu_baseline_full)
     print(json.dumps(result), flush=True)
 
 

@@ -143,6 +143,18 @@ mpipe_status mpipe_encoder_sizes(const mpipe_encoder* enc, const int32_t* cu_seq
                                  int32_t trainable, size_t* workspace_bytes, size_t* tape_bytes,
                                  int64_t* n_merged, int64_t* n_patches);
 
+/* The byte ranges of the workspace (which = 0) or the tape (which = 1) that the
+ * forward and backward of this micro-batch and mode may write, in layout order
+ * (host query, validates the metadata like mpipe_encoder_sizes).  Every range is
+ * followed by at least 256 bytes that no call writes: a caller may fill the
+ * buffers with a canary pattern and check, after a step, that everything outside
+ * the ranges kept it.  Writes up to `cap` ranges into offsets / bytes (both
+ * nullable when cap == 0) and the total count into *n_regions. */
+mpipe_status mpipe_encoder_regions(const mpipe_encoder* enc, const int32_t* cu_seqlens,
+                                   int32_t n_seg, const int32_t* grid_thw, int32_t n_items,
+                                   int32_t trainable, int32_t which, int64_t* offsets,
+                                   int64_t* bytes, int32_t cap, int32_t* n_regions);
+
 /* Fwd(enc, m).  weights, patches: device, cfg dtype.  merged: device
  * [n_merged][llm_hidden], cfg dtype, overwritten.  trainable (mpipe_train_mode)
  * != MPIPE_FROZEN records the activations that mode's backward needs into `tape`

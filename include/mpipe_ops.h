@@ -37,6 +37,22 @@ mpipe_status mpipe_op_gemm(int32_t dtype, int32_t layout, int32_t epilogue, int3
                            void* C2, int64_t ldc2, int32_t beta, int32_t k_per_split,
                            int64_t split_stride, void* hip_stream);
 
+/* Deterministic split-K reduction of the weight gradient (the Accumulate edge of
+ * Sec. 4.1: gradients are added into what the buffer holds):
+ *   out[m][n] += sum over s = 0 .. splits-1, in that order, of part[s][m][n]
+ * part: fp32 [splits][M][N] dense (the partials epilogue 4 writes with split_stride
+ * M*N); out: fp32 [M][ldo], ldo >= N.  Four columns per thread when N and ldo are
+ * multiples of 4 and both pointers 16-byte aligned, one column per thread otherwise;
+ * both paths add in the same order. */
+mpipe_status mpipe_op_splitk_reduce(const float* part, int32_t splits, int64_t M, int64_t N,
+                                    float* out, int64_t ldo, void* hip_stream);
+
+/* The number of K splits the encoder backward gives the weight-gradient product
+ * dW[M][N] = sum over K tokens (host query, no device work): 1 means one unsplit
+ * launch accumulating into d_weights; s > 1 means s fp32 partials then
+ * mpipe_op_splitk_reduce.  -1 for negative sizes. */
+int32_t mpipe_op_weight_grad_splits(int64_t M, int64_t N, int64_t K);
+
 /* LayerNorm over rows of width n (n % 4 == 0, n <= 2048): X fp32 [rows][n];
  * g, b, Y in dtype; mean, rstd fp32 [rows] (nullable). */
 mpipe_status mpipe_op_layernorm_fwd(int32_t dtype, const float* X, int64_t rows, int32_t n,

@@ -64,6 +64,7 @@ def load():
         "mpipe_param_tensors": (i32, [P]),
         "mpipe_param_info": (st, [P, i32, C.c_char_p, i32, P, P, P]),
         "mpipe_encoder_sizes": (st, [P, P, i32, P, i32, i32, P, P, P, P]),
+        "mpipe_encoder_regions": (st, [P, P, i32, P, i32, i32, i32, P, P, i32, P]),
         "mpipe_encoder_fwd": (st, [P, P, P, P, i32, P, i32, i32, P, P, sz, P, sz, P]),
         "mpipe_encoder_bwd": (st, [P, P, P, P, i32, P, i32, i32, P, sz, P, P, P, P, sz, P]),
         "mpipe_merge_scatter": (st, [P, i64, i32, i32, P, P, i64, P]),
@@ -75,6 +76,8 @@ def load():
         "mpipe_profile_read": (i32, [P, P, i32, P, i32, P, P, P]),
         "mpipe_op_gemm": (st, [i32, i32, i32, i32, i32, i32, P, i64, P, i64, P, i64, P, P, i64,
                                P, i64, i32, i32, i64, P]),
+        "mpipe_op_splitk_reduce": (st, [P, i32, i64, i64, P, i64, P]),
+        "mpipe_op_weight_grad_splits": (i32, [i64, i64, i64]),
         "mpipe_op_layernorm_fwd": (st, [i32, P, i64, i32, P, P, C.c_float, P, P, P, P]),
         "mpipe_op_layernorm_bwd": (st, [i32, P, P, P, P, P, i64, i32, P, P, P, P, P, P, P, sz, P]),
         "mpipe_op_rope": (st, [i32, P, i64, i32, i32, P, i32, C.c_float, i32, P, sz, P]),
@@ -183,6 +186,19 @@ class Encoder:
                                           C.byref(nm), C.byref(npch)))
         return {"workspace": ws.value, "tape": tp.value, "n_merged": nm.value,
                 "n_patches": npch.value}
+
+    def regions(self, cu_seqlens, grid_thw, trainable, which: int) -> np.ndarray:
+        """int64 [n][2] (offset, bytes) of the workspace (which=0) or tape (1) ranges the
+        step may write; at least 256 bytes after each range are never written."""
+        cu, cup = _host_i32(cu_seqlens)
+        g, gp = _host_i32(np.asarray(grid_thw).reshape(-1, 3))
+        n = C.c_int32()
+        args = (self._h, cup, max(len(cu) - 1, 0), gp, g.shape[0], int(trainable), which)
+        _check(self.L.mpipe_encoder_regions(*args, None, None, 0, C.byref(n)))
+        off, nb = np.zeros(n.value, np.int64), np.zeros(n.value, np.int64)
+        _check(self.L.mpipe_encoder_regions(*args, off.ctypes.data_as(C.c_void_p),
+                                            nb.ctypes.data_as(C.c_void_p), n.value, C.byref(n)))
+        return np.stack([off, nb], axis=1)
 
     # -- fwd / bwd --
     def fwd(self, weights, patches, cu_seqlens, grid_thw, trainable: bool, merged, tape,
@@ -436,6 +452,16 @@ def op_gemm(dtype: int, layout: int, epilogue: int, M: int, N: int, K: int, A, l
     _check(load().mpipe_op_gemm(dtype, layout, epilogue, M, N, K, _ptr(A), lda, _ptr(B), ldb,
                                 _ptr(Cout), ldc, _ptr(bias), _ptr(aux), ld_aux, _ptr(C2), ldc2,
                                 beta, k_per_split, split_stride, _stream(stream)))
+
+
+def op_splitk_reduce(part, splits: int, M: int, N: int, out, ldo: int, stream=None) -> None:
+    _check(load().mpipe_op_splitk_reduce(_ptr(part), splits, M, N, _ptr(out), ldo,
+                                         _stream(stream)))
+
+
+def gemm_split(M: int, N: int, K: int) -> int:
+    """K splits of the backward's weight-gradient product dW[M][N] over K tokens."""
+    return int(load().mpipe_op_weight_grad_splits(M, N, K))
 
 
 def op_layernorm_fwd(dtype, X, rows, n, g, b, eps, Y, mean=None, rstd=None, stream=None):

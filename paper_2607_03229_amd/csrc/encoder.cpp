@@ -752,6 +752,27 @@ mpipe_status mpipe_encoder_sizes(const mpipe_encoder* e, const int32_t* cu, int3
   return MPIPE_OK;
 }
 
+mpipe_status mpipe_encoder_regions(const mpipe_encoder* e, const int32_t* cu, int32_t n_seg,
+                                   const int32_t* thw, int32_t n_items, int32_t trainable,
+                                   int32_t which, int64_t* offsets, int64_t* bytes, int32_t cap,
+                                   int32_t* n_regions) {
+  MP_RET(check_handle(e));
+  if (which != 0 && which != 1) return fail(MPIPE_ERR_INVALID_ARG, "which must be 0 or 1");
+  if (!n_regions || cap < 0 || (cap > 0 && (!offsets || !bytes)))
+    return fail(MPIPE_ERR_INVALID_ARG, "null output");
+  Plan P;
+  std::string err;
+  const int rc = build_plan(e->cfg, cu, n_seg, thw, n_items, trainable, P, err);
+  if (rc) return fail((mpipe_status)rc, err);
+  const std::vector<Region>& R = which == 0 ? P.ws_regions : P.tape_regions;
+  *n_regions = (int32_t)R.size();
+  for (int32_t i = 0; i < cap && i < (int32_t)R.size(); ++i) {
+    offsets[i] = (int64_t)R[i].off;
+    bytes[i] = (int64_t)R[i].bytes;
+  }
+  return MPIPE_OK;
+}
+
 mpipe_status mpipe_encoder_cost(const mpipe_encoder* e, const int32_t* cu, int32_t n_seg,
                                 const int32_t* thw, int32_t n_items, int32_t trainable,
                                 double flops_per_s, double bytes_per_s, mpipe_slab_cost* out) {

@@ -93,6 +93,20 @@ mpipe_status mpipe_op_gemm(int32_t dtype, int32_t layout, int32_t epi, int32_t M
   return MPIPE_OK;
 }
 
+mpipe_status mpipe_op_splitk_reduce(const float* part, int32_t splits, int64_t M, int64_t N,
+                                    float* out, int64_t ldo, void* stream) {
+  if (splits < 1 || M < 0 || N < 0 || ldo < N)
+    return set_error(MPIPE_ERR_INVALID_ARG, "need splits >= 1, M, N >= 0 and ldo >= N");
+  if (M * N > 0 && (!part || !out)) return set_error(MPIPE_ERR_INVALID_ARG, "null device buffer");
+  OP_CHECK(splitk_reduce(part, splits, M, N, out, ldo, reinterpret_cast<hipStream_t>(stream)));
+  return MPIPE_OK;
+}
+
+int32_t mpipe_op_weight_grad_splits(int64_t M, int64_t N, int64_t K) {
+  if (M < 0 || N < 0 || K < 0) return -1;
+  return choose_split(M, N, K).splits;
+}
+
 mpipe_status mpipe_op_layernorm_fwd(int32_t dtype, const float* X, int64_t rows, int32_t n,
                                     const void* g, const void* b, float eps, void* Y, float* mean,
                                     float* rstd, void* stream) {

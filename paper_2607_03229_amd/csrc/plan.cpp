@@ -11,11 +11,18 @@ namespace {
 constexpr int kTile = 128;      // attention rows per work item (matches ATTN_TILE)
 constexpr size_t kAlign = 256;
 
+// Regions are 256-byte aligned and each is followed by at least kGuard bytes that no
+// kernel writes, so a caller can fill a buffer with a canary pattern and find any write
+// that strays out of its region (mpipe_encoder_regions lists the regions).
+constexpr size_t kGuard = 256;
+
 struct Arena {
   size_t top = 0;
+  std::vector<Region>* log = nullptr;
   size_t take(size_t bytes) {
     const size_t off = (top + kAlign - 1) / kAlign * kAlign;
-    top = off + bytes;
+    top = off + bytes + kGuard;
+    if (log && bytes) log->push_back({off, bytes});
     return off;
   }
 };
@@ -255,7 +262,10 @@ int build_plan(const Cfg& c, const int32_t* cu, int n_seg, const int32_t* thw, i
   p.ws_kwork = ws.take(sizeof(int32_t) * p.k_work.size());
   p.ws_rope = ws.take(sizeof(float) * p.rope_tab.size());
   (void)q4;
-  p.meta_bytes = ws.top;
+  // uploaded by one copy (the guards between them included): one region
+  p.meta_bytes = p.ws_rope + sizeof(float) * p.rope_tab.size();
+  p.ws_regions.push_back({0, p.meta_bytes});
+  ws.log = &p.ws_regions;
   if (c.kp != c.kpe) {
     p.ws_xp = ws.take((size_t)N * c.kp * E);
     p.ws_wpe = ws.take((size_t)h * c.kp * E);
@@ -336,10 +346,12 @@ int build_plan(const Cfg& c, const int32_t* cu, int n_seg, const int32_t* thw, i
   // ---- tape ----
   if (mode == MODE_MERGER) {   // the merger's inputs only: the blocks run no backward
     Arena tp;
+    tp.log = &p.tape_regions;
     p.tape_mrg = merger_set(tp, tp.take((size_t)N * h * 4), true);
     p.tape_bytes = tp.top;
   } else if (mode == MODE_TRAINED) {
     Arena tp;
+    tp.log = &p.tape_regions;
     p.tape_act.resize(c.layers);
     size_t h_in = tp.take((size_t)N * h * 4);
     for (int l = 0; l < c.layers; ++l) {

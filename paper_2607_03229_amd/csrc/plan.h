@@ -77,6 +77,11 @@ GemmSplit choose_split(int64_t M, int64_t N, int64_t K);
 // merger trainable.
 enum { MODE_FROZEN = 0, MODE_TRAINED = 1, MODE_MERGER = 2 };
 
+// A byte range [off, off + bytes) of the workspace or the tape.
+struct Region {
+  size_t off, bytes;
+};
+
 struct Plan {
   int64_t N = 0, Tm = 0;
   int n_items = 0, n_seg = 0;
@@ -99,10 +104,12 @@ struct Plan {
          ws_delta = 0, ws_dqkv = 0, ws_part = 0, ws_cpart = 0, ws_dwpart = 0,
          ws_gpart = 0;
   size_t ws_bytes = 0;
+  std::vector<Region> ws_regions;   // every range a kernel may write, in layout order
   // tape layout: every layer and the merger (MODE_TRAINED), the merger only (MODE_MERGER)
   std::vector<ActSet> tape_act;
   MergerSet tape_mrg{};
   size_t tape_bytes = 0;
+  std::vector<Region> tape_regions;
 };
 
 // W (FLOPs) and D (algorithmic HBM bytes) of one micro-batch's forward and backward

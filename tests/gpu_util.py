@@ -31,13 +31,24 @@ def zeros(shape, dtype_str: str):
                        device=dev)
 
 
+def nans(shape, dtype_str: str):
+    """An output buffer the library must overwrite: NaN everywhere, so an element that is
+    never written fails max_rel (which is NaN-propagating) instead of passing as 0."""
+    torch, dev = torch_dev()
+    return torch.full(shape, float("nan"),
+                      dtype=torch.bfloat16 if dtype_str == "bf16" else torch.float32, device=dev)
+
+
 def host(t) -> np.ndarray:
     return t.detach().float().cpu().numpy().astype(np.float64)
 
 
 def max_rel(x, r) -> float:
-    """max |x - r| / max |r|, per tensor."""
+    """max |x - r| / max |r|, per tensor; NaN (which fails every bound) when either side
+    holds a NaN."""
     x, r = np.asarray(x, np.float64), np.asarray(r, np.float64)
+    if np.isnan(x).any() or np.isnan(r).any():
+        return float("nan")
     den = np.max(np.abs(r)) if r.size else 0.0
     if den == 0.0:
         return float(np.max(np.abs(x))) if x.size else 0.0

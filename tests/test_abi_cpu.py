@@ -60,6 +60,38 @@ def test_unsupported_configs_rejected(L):
         assert e.value.status == -5
 
 
+@pytest.mark.parametrize("trainable", [0, 1, 2])
+def test_workspace_and_tape_regions(L, trainable):
+    """The writable ranges the planner lays out: inside the buffer, in order, and each
+    followed by at least 256 unwritten guard bytes (the canary check of the GPU test
+    relies on this)."""
+    wl = W.make_workload("c4_qwen2vl_trained", 0)
+    enc = B.Encoder(wl.cfg)
+    s = enc.sizes(wl.cu_seqlens, wl.grid_thw, trainable)
+    for which, total in ((0, s["workspace"]), (1, s["tape"])):
+        r = enc.regions(wl.cu_seqlens, wl.grid_thw, trainable, which)
+        if which == 1 and trainable == 0:
+            assert len(r) == 0 and total == 0
+            continue
+        assert len(r) > 0 and (r[:, 1] > 0).all() and (r[:, 0] % 256 == 0).all()
+        ends = r[:, 0] + r[:, 1]
+        assert (r[1:, 0] >= ends[:-1] + 256).all()
+        assert ends[-1] + 256 <= total
+    enc.close()
+
+
+def test_weight_grad_split_plan(L):
+    """The split plan the backward uses (host query): no split below 2,048 tokens, the
+    benchmark's weight gradients split, at most four ways, rejected sizes answer -1."""
+    import paper_2607_03229_amd as mp
+    assert mp.gemm_split(3840, 1280, 656) == 1
+    assert mp.gemm_split(3840, 1280, 2047) == 1
+    for M, N in ((3840, 1280), (1280, 1280), (5120, 1280), (1280, 5120), (1280, 1176)):
+        s = mp.gemm_split(M, N, 42940)
+        assert 2 <= s <= 4, (M, N, s)
+    assert mp.gemm_split(-1, 8, 8) == -1
+
+
 def test_sizes_and_metadata_validation(L):
     wl = W.make_workload("c4_qwen2vl_trained", 0)
     enc = B.Encoder(wl.cfg)
@@ -167,7 +199,8 @@ def test_merger_only_mode_host_side(L):
     N, h, Tm = wl.n_patches, wl.cfg.hidden, wl.n_merged
     # final residual (fp32), LN output (bf16), LN stats, GELU' and GELU of fc1 (bf16)
     expect = N * h * 4 + N * h * 2 + 2 * N * 4 + 2 * Tm * 4 * h * 2
-    assert expect <= part["tape"] <= expect + 4 * 256
+    # six regions, each padded to 256-byte alignment and followed by a 256-byte guard
+    assert expect <= part["tape"] <= expect + 6 * 512
     assert part["tape"] * 20 < full["tape"]
     assert part["n_merged"] == full["n_merged"]
     for bad in (3, -1):

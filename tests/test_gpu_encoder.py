@@ -8,7 +8,7 @@ import pytest
 
 import oracle
 import workload as W
-from tests.gpu_util import announce, host, max_rel, to_dev, torch_dev, zeros
+from tests.gpu_util import announce, host, max_rel, nans, to_dev, torch_dev, zeros
 
 pytestmark = pytest.mark.gpu
 
@@ -27,23 +27,52 @@ class GpuRun:
         self.X = to_dev(patches, cfg.dtype)
 
     def run(self, trainable, d_merged=None, want_dx=False, dw_init=None):
+        """One forward (and backward when d_merged is given).  The workspace and tape
+        start filled with a canary byte; afterwards every byte outside the ranges the
+        planner lays out (mpipe_encoder_regions) must still hold it."""
         torch = self.torch
         s = self.enc.sizes(self.cu, self.grid, trainable)
-        ws = torch.empty(max(s["workspace"], 1), dtype=torch.uint8, device=self.dev)
-        tape = (torch.empty(max(s["tape"], 1), dtype=torch.uint8, device=self.dev)
+        ws = torch.full((max(s["workspace"], 1),), CANARY, dtype=torch.uint8, device=self.dev)
+        tape = (torch.full((max(s["tape"], 1),), CANARY, dtype=torch.uint8, device=self.dev)
                 if trainable else None)
-        merged = zeros((s["n_merged"], self.cfg.llm_hidden), self.cfg.dtype)
+        merged = nans((s["n_merged"], self.cfg.llm_hidden), self.cfg.dtype)
         self.enc.fwd(self.w, self.X, self.cu, self.grid, trainable, merged, tape, ws)
         out = {"merged": merged}
         if d_merged is not None:
             dw = (to_dev(dw_init, "f32") if dw_init is not None
                   else zeros((self.w.numel(),), "f32"))
-            dx = zeros(tuple(self.X.shape), self.cfg.dtype) if want_dx else None
+            dx = nans(tuple(self.X.shape), self.cfg.dtype) if want_dx else None
             out["status"] = self.enc.bwd(self.w, self.X, self.cu, self.grid, trainable, tape,
                                          to_dev(d_merged, self.cfg.dtype), dw, dx, ws)
             out["dw"], out["dx"] = dw, dx
         torch.cuda.synchronize()
+        for which, buf in ((0, ws), (1, tape)):
+            if buf is not None:
+                bad = _canary_violations(buf, self.enc.regions(self.cu, self.grid, trainable,
+                                                               which))
+                assert not bad, f"{'tape' if which else 'workspace'} written outside its " \
+                                f"regions: {bad[:4]}"
         return out
+
+
+CANARY = 0xA5
+
+
+def _canary_violations(buf, regions):
+    """(start, end) of each gap between the writable regions (and after the last) in
+    which some byte lost the canary value."""
+    import torch
+    gaps, prev = [], 0
+    for off, nb in regions.tolist():
+        if off > prev:
+            gaps.append((prev, off))
+        prev = off + nb
+    if buf.numel() > prev:
+        gaps.append((prev, buf.numel()))
+    if not gaps:
+        return []
+    flags = torch.stack([(buf[a:b] != CANARY).any() for a, b in gaps]).cpu().numpy()
+    return [g for g, f in zip(gaps, flags) if f]
 
 
 def _per_tensor_errors(cfg, got, ref):
@@ -56,12 +85,13 @@ def _per_tensor_errors(cfg, got, ref):
     return errs
 
 
-def _check_full(wl_cfg, w, X, cu, grid, d_merged, tol, label):
+def _check_full(wl_cfg, w, X, cu, grid, d_merged, tol, label, precision="f64"):
     announce(f"encoder fwd+bwd {label} N={len(X)}")
     g = GpuRun(wl_cfg, w, X, cu, grid)
     out = g.run(True, d_merged=d_merged, want_dx=True)
+    announce(f"oracle ({precision}) {label}")
     rc, rM, rdw, rdx = oracle.encoder(wl_cfg, w, X, cu, grid, True, d_merged=d_merged,
-                                      want_d_patches=True)
+                                      want_d_patches=True, precision=precision)
     assert out["status"] == 0 and rc == 0
     em = max_rel(host(out["merged"]), rM)
     assert em < tol, f"merged max-rel {em}"
@@ -71,6 +101,7 @@ def _check_full(wl_cfg, w, X, cu, grid, d_merged, tol, label):
     ex = max_rel(host(out["dx"]), rdx)
     assert ex < tol, f"d_patches max-rel {ex}"
     print(f"{label}: merged {em:.2e}  d_w worst {worst} {errs[worst]:.2e}  d_patches {ex:.2e}")
+    return out
 
 
 @pytest.mark.parametrize("seed", [0, 1])
@@ -214,26 +245,40 @@ def _smallest_items(wl, k):
                                   "c5_mixed_f05_trained"])
 def test_full_size_forward_sampled(name):
     """Full micro-batch on the GPU; the oracle recomputes the smallest item alone
-    (valid by the block-diagonal independence of items)."""
+    (valid by the block-diagonal independence of items).  Trained workloads also run
+    the backward with the patch gradient requested, and the smallest item's patch
+    gradient is compared too (the oracle's run on that item alone, fed the item's rows
+    of the upstream gradient)."""
     wl = W.make_workload(name, 0)
     cfg = wl.cfg
     w, X = wl.weights(), wl.patches()
     announce(f"full-size forward {name} N={wl.n_patches} items={wl.n_items}")
     g = GpuRun(cfg, w, X, wl.cu_seqlens, wl.grid_thw)
-    out = g.run(wl.trainable, d_merged=wl.d_merged() if wl.trainable else None)
+    dM = wl.d_merged() if wl.trainable else None
+    out = g.run(wl.trainable, d_merged=dM, want_dx=bool(wl.trainable))
     got = host(out["merged"])
+    gdx = host(out["dx"]) if wl.trainable else None
     per_m = wl.merged_per_item
     mo = np.concatenate([[0], np.cumsum(per_m)])
     for i in _smallest_items(wl, 1):
         sl = slice(int(wl.cu_seqlens[i]), int(wl.cu_seqlens[i + 1]))
+        ms = slice(int(mo[i]), int(mo[i + 1]))
         n = sl.stop - sl.start
-        _, Mi, _, _ = oracle.encoder(cfg, w, X[sl], [0, n], wl.grid_thw[i:i + 1], False)
-        err = max_rel(got[mo[i]:mo[i + 1]], Mi)
+        announce(f"oracle: {name} item {i} alone ({n} patches)")
+        if wl.trainable:
+            _, Mi, _, dXi = oracle.encoder(cfg, w, X[sl], [0, n], wl.grid_thw[i:i + 1], True,
+                                           d_merged=dM[ms], want_d_patches=True)
+            ex = max_rel(gdx[sl], dXi)
+            print(f"{name} item {i} ({n} patches): d_patches max-rel {ex:.2e}")
+            assert ex < TOL["bf16"]
+        else:
+            _, Mi, _, _ = oracle.encoder(cfg, w, X[sl], [0, n], wl.grid_thw[i:i + 1], False)
+        err = max_rel(got[ms], Mi)
         print(f"{name} item {i} ({n} patches): merged max-rel {err:.2e}")
         assert err < TOL["bf16"]
     assert np.isfinite(got).all()
     if wl.trainable:
-        assert np.isfinite(host(out["dw"])).all()
+        assert np.isfinite(host(out["dw"])).all() and np.isfinite(gdx).all()
 
 
 def test_full_size_backward_sampled_and_relocated():
@@ -288,6 +333,30 @@ def test_full_size_backward_sampled_and_relocated():
     assert errs[worst] < 1e-4
 
 
+def test_full_size_video_micro_batch_items_independent():
+    """The mixed-modality workload at image fraction 0: eight 16-frame 448 x 448 clips
+    (65,536 patches, one 8,192-row attention segment each), trained, full size and depth.
+    Every output is finite, and the first clip encoded alone gives its merged rows and
+    patch gradient bit for bit as inside the micro-batch (items are independent:
+    block-diagonal attention, row-wise elsewhere).  The oracle pins the clip path itself
+    at reduced depth (test_video_clip_16_frames_reduced_depth)."""
+    wl = W.make_workload("c5_mixed_f0_trained", 0)
+    cfg = wl.cfg
+    assert (wl.grid_thw == np.array([8, 32, 32])).all() and wl.n_patches == 65536
+    w, X, dM = wl.weights(), wl.patches(), wl.d_merged()
+    announce(f"full-size video micro-batch N={wl.n_patches}")
+    full = GpuRun(cfg, w, X, wl.cu_seqlens, wl.grid_thw).run(True, d_merged=dM, want_dx=True)
+    merged, dx = host(full["merged"]), host(full["dx"])
+    assert np.isfinite(merged).all() and np.isfinite(dx).all()
+    assert np.isfinite(host(full["dw"])).all()
+    del full
+    announce("first clip alone")
+    one = GpuRun(cfg, w, X[:8192], [0, 8192], wl.grid_thw[:1]).run(True, d_merged=dM[:2048],
+                                                                   want_dx=True)
+    assert np.array_equal(host(one["merged"]), merged[:2048])
+    assert np.array_equal(host(one["dx"]), dx[:8192])
+
+
 def test_full_depth_gradients_one_item():
     """Qwen2-VL-ViT shape at full depth (32 layers): weight and patch gradients
     of one 256-patch image against the oracle."""
@@ -297,6 +366,70 @@ def test_full_depth_gradients_one_item():
     dM = W.round_bf16(rng.standard_normal((wl.n_merged, cfg.llm_hidden)).astype(np.float32))
     _check_full(cfg, wl.weights(), wl.patches(), wl.cu_seqlens, wl.grid_thw, dM, TOL["bf16"],
                 "c4-shape one item")
+
+
+# ---------------------------------------------------------------------------
+# Reduced-depth Qwen2-VL-ViT shape at the sizes where the benchmark's weight-gradient
+# route runs: every weight-gradient GEMM has K (tokens) >= 2048, so the planner splits
+# K, the TN kernel writes fp32 partials and the split-K reduction adds them into
+# d_weights; M >= 512, so the fc1 bias sums come from the GELU-backward GEMM epilogue;
+# the side stream is on (the default), as in the benchmark.
+# ---------------------------------------------------------------------------
+
+def _qwen_reduced(layers=1):
+    cfg = dataclasses.replace(W.CONFIGS["c4_qwen2vl_trained"].cfg, layers=layers)
+    W.custom_spec(f"qwen_{layers}blk", cfg, emb_seqs=8, emb_seq_len=8192)
+    return cfg
+
+
+def _splits_of(cfg, n_tokens, n_merged):
+    """The K splits the library plans for each weight-gradient GEMM (ABI query)."""
+    import paper_2607_03229_amd as mp
+    h, m, H = cfg.hidden, cfg.mlp, cfg.llm_hidden
+    shapes = {"qkv": (3 * h, h, n_tokens), "proj": (h, h, n_tokens), "fc1": (m, h, n_tokens),
+              "fc2": (h, m, n_tokens), "pe": (h, cfg.k_pe, n_tokens),
+              "merger.fc1": (4 * h, 4 * h, n_merged), "merger.fc2": (H, 4 * h, n_merged)}
+    return {k: mp.gemm_split(*v) for k, v in shapes.items()}
+
+
+@pytest.mark.timeout(900)
+def test_split_k_weight_gradients_benchmark_prefix():
+    """The benchmark draw's (C4, seed 0) first items in order until >= 4096 patches, one
+    block of the Qwen2-VL-ViT shape: merged rows, every weight- and bias-gradient tensor
+    and the patch gradient against the oracle (fp32), with the block's weight gradients
+    on the split-K route the benchmark runs (Sec. 4.1, the Accumulate edge)."""
+    cfg = _qwen_reduced(1)
+    full = W.make_workload("c4_qwen2vl_trained", 0)
+    n = full.grid_thw[:, 0] * full.grid_thw[:, 1] * full.grid_thw[:, 2]
+    k = int(np.searchsorted(np.cumsum(n), 4096) + 1)
+    wl = W.make_workload("qwen_1blk", 0, grid_thw=full.grid_thw[:k])
+    assert wl.n_patches >= 4096
+    sp = _splits_of(cfg, wl.n_patches, wl.n_merged)
+    print(f"prefix of {k} items, {wl.n_patches} patches; K splits {sp}")
+    for name in ("qkv", "proj", "fc1", "fc2", "pe"):
+        assert sp[name] > 1, (name, sp[name])
+    rng = np.random.default_rng(11)
+    dM = W.round_bf16(rng.standard_normal((wl.n_merged, cfg.llm_hidden)).astype(np.float32))
+    _check_full(cfg, wl.weights(), wl.patches(), wl.cu_seqlens, wl.grid_thw, dM, TOL["bf16"],
+                "qwen 1 block, benchmark prefix", precision="f32")
+
+
+@pytest.mark.timeout(900)
+def test_video_clip_16_frames_reduced_depth():
+    """One 16-frame 448 x 448 clip (temporal patch 2: t = 8, 32 x 32 patches, a single
+    8,192-row attention segment) through one block of the Qwen2-VL-ViT shape, forward and
+    backward against the oracle (fp32).  Its 2,048 merged rows put the merger's fc2
+    weight gradient on the split-K route too."""
+    cfg = _qwen_reduced(1)
+    wl = W.make_workload("qwen_1blk", 0, grid_thw=np.array([[8, 32, 32]]))
+    assert wl.n_patches == 8192 and wl.n_merged == 2048
+    sp = _splits_of(cfg, wl.n_patches, wl.n_merged)
+    print(f"clip: K splits {sp}")
+    assert sp["merger.fc2"] > 1 and sp["fc1"] > 1
+    rng = np.random.default_rng(12)
+    dM = W.round_bf16(rng.standard_normal((wl.n_merged, cfg.llm_hidden)).astype(np.float32))
+    _check_full(cfg, wl.weights(), wl.patches(), wl.cu_seqlens, wl.grid_thw, dM, TOL["bf16"],
+                "qwen 1 block, 16-frame clip", precision="f32")
 
 
 # ---------------------------------------------------------------------------

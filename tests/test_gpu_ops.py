@@ -5,7 +5,7 @@ import numpy as np
 import pytest
 
 import oracle
-from tests.gpu_util import announce, host, max_rel, rnd, to_dev, torch_dev, zeros
+from tests.gpu_util import announce, host, max_rel, nans, rnd, to_dev, torch_dev, zeros
 
 pytestmark = pytest.mark.gpu
 
@@ -53,7 +53,7 @@ def test_gemm_layouts(dtype, layout):
         A = rnd(rng, (K, M) if layout == TN else (M, K), dtype)
         B = rnd(rng, (N, K) if layout == NT else (K, N), dtype)
         ref = _ref_product(layout, A, B)
-        C = zeros((M, N), "f32")
+        C = nans((M, N), "f32")
         mp.op_gemm(_dt(dtype), layout, E_F32, M, N, K, to_dev(A, dtype), A.shape[1],
                    to_dev(B, dtype), B.shape[1], C, N)
         torch.cuda.synchronize()
@@ -85,12 +85,12 @@ def test_gemm_epilogues(dtype, M, N, K, layout):
     pre = oracle.linear(A, B, bias)
     # store with bias
     announce(f"gemm epilogue store {dtype} layout={layout}")
-    C = zeros((M, N), dtype)
+    C = nans((M, N), dtype)
     mp.op_gemm(_dt(dtype), layout, E_STORE, M, N, K, dA, K, dB, ldb, C, N, bias=db)
     assert max_rel(host(C), pre) < TOL[dtype]
     # GELU, with GELU' of the pre-activation stored for the backward
     announce(f"gemm epilogue gelu {dtype} layout={layout}")
-    C, C2 = zeros((M, N), dtype), zeros((M, N), dtype)
+    C, C2 = nans((M, N), dtype), nans((M, N), dtype)
     mp.op_gemm(_dt(dtype), layout, E_GELU, M, N, K, dA, K, dB, ldb, C, N, bias=db, C2=C2, ldc2=N)
     assert max_rel(host(C2), oracle.gelu_grad(pre)) < TOL[dtype]
     assert max_rel(host(C), oracle.gelu(pre)) < TOL[dtype]
@@ -104,7 +104,7 @@ def test_gemm_epilogues(dtype, M, N, K, layout):
     announce(f"gemm epilogue gelu-bwd {dtype} layout={layout}")
     U = rnd(rng, (M, N), dtype)
     Gd = oracle.gelu_grad(U).astype(np.float32)
-    C = zeros((M, N), dtype)
+    C = nans((M, N), dtype)
     mp.op_gemm(_dt(dtype), layout, E_GELUBWD, M, N, K, dA, K, dB, ldb, C, N, aux=to_dev(Gd, dtype),
                ld_aux=N)
     assert max_rel(host(C), oracle.linear(A, B) * oracle.gelu_grad(U)) < TOL[dtype]
@@ -115,23 +115,45 @@ def test_gemm_epilogues(dtype, M, N, K, layout):
     assert max_rel(host(C), R + oracle.linear(A, B)) < 2e-5
 
 
-@pytest.mark.parametrize("dtype,M,N", [("bf16", 136, 264), ("f32", 136, 264),
-                                       ("bf16", 520, 264)])
-def test_gemm_split_k(dtype, M, N):
+@pytest.mark.parametrize("dtype,M,N,K,kps", [("bf16", 136, 264, 1000, 256),
+                                              ("f32", 136, 264, 1000, 256),
+                                              ("bf16", 520, 264, 1000, 256),
+                                              ("bf16", 1280, 768, 3000, 1024)])
+@pytest.mark.parametrize("ldo_pad", [0, 3])
+def test_gemm_split_k(dtype, M, N, K, kps, ldo_pad):
+    """The weight-gradient route of the backward: the TN GEMM writes one fp32 partial per K
+    split, and the split-K reduction adds the partials, in split order, into a d_weights
+    block that already holds a value (Accumulate).  Checked against the oracle's Linear
+    backward, dW = dY^T X.  ldo_pad = 0 takes the four-column reduction, 3 the
+    one-column one (a row stride that is not a multiple of 4)."""
     import paper_2607_03229_amd as mp
     torch, dev = torch_dev()
-    rng = np.random.default_rng(3)
-    K, kps = 1000, 256
-    announce(f"gemm split-k {dtype} M={M} N={N}")
+    rng = np.random.default_rng(3 + M)
+    announce(f"gemm split-k {dtype} M={M} N={N} K={K} kps={kps} ldo_pad={ldo_pad}")
     A, B = rnd(rng, (K, M), dtype), rnd(rng, (K, N), dtype)
     splits = (K + kps - 1) // kps
-    part = zeros((splits, M, N), "f32")
+    part = nans((splits, M, N), "f32")
     mp.op_gemm(_dt(dtype), TN, E_F32, M, N, K, to_dev(A, dtype), M, to_dev(B, dtype), N, part, N,
                k_per_split=kps, split_stride=M * N)
     got = host(part)
     for s in range(splits):
         sl = slice(s * kps, min(K, (s + 1) * kps))
-        assert max_rel(got[s], A[sl].T.astype(np.float64) @ B[sl]) < 2e-5
+        _, ref_s, _ = oracle.linear_bwd(A[sl], B[sl], np.zeros((M, N)))
+        assert max_rel(got[s], ref_s) < 2e-5, s
+    # reduce into an accumulating target
+    ldo = N + ldo_pad
+    base = rng.standard_normal((M, ldo)).astype(np.float32)
+    out = to_dev(base, "f32")
+    mp.op_splitk_reduce(part, splits, M, N, out, ldo)
+    res = host(out)
+    _, ref, _ = oracle.linear_bwd(A, B, np.zeros((M, N)))
+    assert max_rel(res[:, :N], base[:, :N] + ref) < 2e-5
+    np.testing.assert_array_equal(res[:, N:], base[:, N:])   # the stride's pad untouched
+    # the two reduction paths add in the same order: bitwise the same sums
+    if ldo_pad:
+        out4 = to_dev(base[:, :N], "f32")
+        mp.op_splitk_reduce(part, splits, M, N, out4, N)
+        np.testing.assert_array_equal(host(out4), res[:, :N])
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
@@ -144,8 +166,8 @@ def test_layernorm_fwd_bwd(dtype, n):
     announce(f"layernorm {dtype} n={n}")
     X = (rng.standard_normal((rows, n)) * 3 + 1).astype(np.float32)
     g, b = rnd(rng, (n,), dtype, 0.1, 1.0), rnd(rng, (n,), dtype, 0.1)
-    Y = zeros((rows, n), dtype)
-    mean, rstd = zeros((rows,), "f32"), zeros((rows,), "f32")
+    Y = nans((rows, n), dtype)
+    mean, rstd = nans((rows,), "f32"), nans((rows,), "f32")
     dX_ = to_dev(X, "f32")
     mp.op_layernorm_fwd(_dt(dtype), dX_, rows, n, to_dev(g, dtype), to_dev(b, dtype), 1e-6, Y,
                         mean, rstd)
@@ -154,7 +176,7 @@ def test_layernorm_fwd_bwd(dtype, n):
     assert max_rel(host(mean), rmu) < 1e-5 and max_rel(host(rstd), rrs) < 1e-5
     dY = rng.standard_normal((rows, n)).astype(np.float32)
     dres = rng.standard_normal((rows, n)).astype(np.float32)
-    dX, dXt = zeros((rows, n), "f32"), zeros((rows, n), dtype)
+    dX, dXt = nans((rows, n), "f32"), nans((rows, n), dtype)
     gg, gb = to_dev(np.ones(n), "f32"), to_dev(np.zeros(n), "f32")
     gc = to_dev(np.full(n, 2.0), "f32")
     scratch = torch.empty(mp.op_scratch_bytes(rows, 1, n, 0), dtype=torch.uint8, device=dev)
@@ -217,12 +239,12 @@ def test_attention_longest_segments():
     qkv = rnd(rng, (N, 3 * h), "bf16", 1.5)
     q, k, v = qkv[:, :h], qkv[:, h:2 * h], qkv[:, 2 * h:]
     tq = to_dev(qkv, "bf16")
-    o, lse = zeros((N, h), "bf16"), zeros((heads, N), "f32")
+    o, lse = nans((N, h), "bf16"), nans((heads, N), "f32")
     scratch = torch.empty(mp.op_scratch_bytes(N, heads, h, len(lens)), dtype=torch.uint8,
                           device=dev)
     mp.op_attention_fwd(_dt("bf16"), tq, N, heads, d, cu, o, lse, scratch)
     dO = rnd(rng, (N, h), "bf16")
-    dqkv = zeros((N, 3 * h), "bf16")
+    dqkv = nans((N, 3 * h), "bf16")
     mp.op_attention_bwd(_dt("bf16"), tq, o, to_dev(dO, "bf16"), lse, N, heads, d, cu, dqkv,
                         scratch)
     got_o, got_lse, got = host(o), host(lse), host(dqkv)
@@ -234,7 +256,7 @@ def test_attention_longest_segments():
                           ("dv", slice(2 * h, 3 * h), rdv)):
         err = max_rel(got[:, sl], ref)
         print(f"longest segments {name}: max-rel {err:.2e}")
-        assert err < 3e-2, (name, err)
+        assert err < 2e-2, (name, err)
 
 
 @pytest.mark.parametrize("dtype,heads,d", [("bf16", 2, 80), ("bf16", 2, 64), ("bf16", 3, 32),
@@ -251,7 +273,7 @@ def test_attention_fwd_bwd(dtype, heads, d):
     q, k, v = qkv[:, :h], qkv[:, h:2 * h], qkv[:, 2 * h:]
     ro, rlse = oracle.attention(q, k, v, cu, heads, d)
     tq = to_dev(qkv, dtype)
-    o, lse = zeros((N, h), dtype), zeros((heads, N), "f32")
+    o, lse = nans((N, h), dtype), nans((heads, N), "f32")
     scratch = torch.empty(mp.op_scratch_bytes(N, heads, h, len(ATTN_LENS)), dtype=torch.uint8,
                           device=dev)
     mp.op_attention_fwd(_dt(dtype), tq, N, heads, d, cu, o, lse, scratch)
@@ -261,10 +283,10 @@ def test_attention_fwd_bwd(dtype, heads, d):
     announce(f"attention bwd {dtype} heads={heads} d={d} N={N}")
     dO = rnd(rng, (N, h), dtype)
     rdq, rdk, rdv = oracle.attention_bwd(q, k, v, ro, dO, rlse, cu, heads, d)
-    dqkv = zeros((N, 3 * h), dtype)
+    dqkv = nans((N, 3 * h), dtype)
     mp.op_attention_bwd(_dt(dtype), tq, o, to_dev(dO, dtype), lse, N, heads, d, cu, dqkv, scratch)
     got = host(dqkv)
     for name, sl, ref in (("dq", slice(0, h), rdq), ("dk", slice(h, 2 * h), rdk),
                           ("dv", slice(2 * h, 3 * h), rdv)):
         err = max_rel(got[:, sl], ref)
-        assert err < (3e-2 if dtype == "bf16" else 1e-5), (name, err)
+        assert err < (2e-2 if dtype == "bf16" else 1e-5), (name, err)
