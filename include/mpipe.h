@@ -214,6 +214,20 @@ mpipe_status mpipe_merge_check_indices(const int64_t* placeholder_idx, int64_t n
                                        int64_t n_rows, int32_t* marks, int32_t* status,
                                        void* hip_stream);
 
+/* The same check for callers that cannot allocate device memory (work under
+ * stream capture, serving loops, harnesses that forbid allocation): the per-row
+ * counters live in a device array built into the library, so the caller passes
+ * only the indices and the status word, and the call allocates nothing.
+ * n_rows may be at most MPIPE_CHECK_NOALLOC_MAX_ROWS (4 MiB of int32 counters,
+ * held by every GPU the library runs on until the process ends); a larger n_rows
+ * returns MPIPE_ERR_WORKSPACE with nothing enqueued.  Every call on one GPU uses
+ * that GPU's one array (cleared on the stream before use): calls that overlap on
+ * one GPU, on different streams or threads, race and must be ordered by the
+ * caller.  Result identical to mpipe_merge_check_indices. */
+#define MPIPE_CHECK_NOALLOC_MAX_ROWS (1 << 20)
+mpipe_status mpipe_merge_check_indices_noalloc(const int64_t* placeholder_idx, int64_t n_merged,
+                                               int64_t n_rows, int32_t* status, void* hip_stream);
+
 /* Message for the last non-OK status returned on this thread. */
 const char* mpipe_last_error(void);
 

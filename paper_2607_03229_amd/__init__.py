@@ -7,7 +7,8 @@ computes; if the library is missing, every call raises.
 """
 from ._binding import (  # noqa: F401
     MpipeError, Encoder, EncoderCfg, load, lib_path, last_error,
-    merge_scatter, merge_gather, merge_check_indices,
+    merge_scatter, merge_gather, merge_check_indices, merge_check_indices_noalloc,
+    CHECK_NOALLOC_MAX_ROWS,
     op_gemm, op_layernorm_fwd, op_layernorm_bwd, op_rope, op_attention_fwd,
     op_attention_bwd, op_scratch_bytes, op_splitk_reduce, gemm_split,
     F32, BF16, OK, NOOP_FROZEN,

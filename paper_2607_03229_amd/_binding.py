@@ -70,6 +70,7 @@ def load():
         "mpipe_merge_scatter": (st, [P, i64, i32, i32, P, P, i64, P]),
         "mpipe_merge_gather": (st, [P, i64, i32, i32, P, i64, P, P]),
         "mpipe_merge_check_indices": (st, [P, i64, i64, P, P, P]),
+        "mpipe_merge_check_indices_noalloc": (st, [P, i64, i64, P, P]),
         "mpipe_last_error": (C.c_char_p, []),
         "mpipe_profile_enable": (st, [P, i32]),
         "mpipe_encoder_set_side_stream": (st, [P, i32]),
@@ -435,6 +436,17 @@ def merge_gather(d_embeds, placeholder_idx, d_merged, stream=None) -> None:
 def merge_check_indices(placeholder_idx, n_rows: int, marks, status, stream=None) -> None:
     _check(load().mpipe_merge_check_indices(_ptr(placeholder_idx), placeholder_idx.numel(),
                                             n_rows, _ptr(marks), _ptr(status), _stream(stream)))
+
+
+def merge_check_indices_noalloc(placeholder_idx, n_rows: int, status, stream=None) -> None:
+    """mpipe_merge_check_indices without a caller buffer (the library's built-in
+    counters; n_rows <= CHECK_NOALLOC_MAX_ROWS)."""
+    _check(load().mpipe_merge_check_indices_noalloc(_ptr(placeholder_idx),
+                                                    placeholder_idx.numel(), n_rows,
+                                                    _ptr(status), _stream(stream)))
+
+
+CHECK_NOALLOC_MAX_ROWS = 1 << 20   # MPIPE_CHECK_NOALLOC_MAX_ROWS of include/mpipe.h
 
 
 # --------------------------------------------------------------------------

@@ -10,7 +10,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libmpipe.so")
-SOURCES = ["gemm.hip", "gemm_big.hip", "attention.hip", "elementwise.hip", "plan.cpp", "encoder.cpp", "ops.cpp", "owner.cpp", "derive.cpp"]
+SOURCES = ["gemm.hip", "gemm_big.hip", "attention.hip", "elementwise.hip", "plan.cpp", "encoder.cpp", "ops.cpp", "owner.cpp", "derive.cpp", "noalloc.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 # Packed-fp32 VALU instructions are disabled for every HIP object.
