@@ -72,7 +72,7 @@ TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.json")
 CAL_ROWS, CAL_COLS = 32768, 3584          # bf16 rows copied by the calibration gather
 CAL_READ = CAL_ROWS * CAL_COLS * 2 + 8 * CAL_ROWS
 CAL_WRITE = CAL_ROWS * CAL_COLS * 2
-EPI_NAMES = ["store", "gelu", "resid", "gelubwd", "f32"]
+EPI_NAMES = ["store", "gelu", "resid", "gelubwd", "f32", "storerope"]
 # What `traffic` counts: the TCC (L2) FETCH_SIZE + WRITE_SIZE counters, i.e. bytes moved
 # between the L2 and the data fabric.  Reads served by the 256 MB Infinity Cache are
 # included, so this bounds HBM traffic from above; it is per launch, like `achieved`.

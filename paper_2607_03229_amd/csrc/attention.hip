@@ -496,6 +496,38 @@ __global__ __launch_bounds__(64 * (8 / NS), NS == 2 ? 2 : 1) void attn_bwd_dkdv_
   }
   bf16* dK = reinterpret_cast<bf16*>(p.dk) + head * D;
   bf16* dV = reinterpret_cast<bf16*>(p.dv) + head * D;
+  if (p.rope_pos != nullptr) {
+    // q, k pair-interleaved and rotated: rotate each dK pair (stored columns c & ~1,
+    // c | 1, in lanes r & ~1, r | 1) back and write it in the original column order.  The
+    // rotary factors of the lane's keys and column pairs are all loaded first.
+    float2 cs[NS][4][NDT];
+#pragma unroll
+    for (int ks = 0; ks < NS; ++ks)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int key = min(k0 + RW * w + 16 * ks + 4 * g + v, s1 - 1);
+#pragma unroll
+        for (int dt = 0; dt < NDT; ++dt)
+          cs[ks][v][dt] = rope_cs(p.rope_pos, p.rope_tab, D, key, (16 * dt + r) >> 1);
+      }
+#pragma unroll
+    for (int ks = 0; ks < NS; ++ks)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int key = k0 + RW * w + 16 * ks + 4 * g + v;   // the same in lanes r, r ^ 1
+        if (key >= s1) continue;
+#pragma unroll
+        for (int dt = 0; dt < NDT; ++dt) {
+          const float x = dk[ks][dt][v] * p.scale;
+          const float y = __shfl_xor(x, 1);
+          const float2 c = cs[ks][v][dt];
+          dK[(int64_t)key * p.ldd + rope_component(16 * dt + r, D)] =
+              (bf16)((r & 1) ? rope_second(y, x, c, true) : rope_first(x, y, c, true));
+          dV[(int64_t)key * p.ldd + 16 * dt + r] = (bf16)(dv[ks][dt][v]);
+        }
+      }
+    return;
+  }
 #pragma unroll
   for (int ks = 0; ks < NS; ++ks)
 #pragma unroll
@@ -623,6 +655,42 @@ __global__ __launch_bounds__(64 * (8 / NS), NS == 2 ? 3 : 1) void attn_bwd_dq_ke
     if (t + 1 < nt) body(t + 1, k1s, v1s, k0s, v0s);
   }
   bf16* dQ = reinterpret_cast<bf16*>(p.dq) + head * D;
+  if (p.rope_pos != nullptr) {
+    // q, k pair-interleaved and rotated: stored columns 16 dt + 4 g .. +3 of a lane are the
+    // rotary pairs j0 = 8 dt + 2 g and j0 + 1 (one axis, consecutive table entries).  Their
+    // factors are all loaded first; each pair is rotated back and written as components
+    // j0, j0 + 1 and j0 + D/2, j0 + 1 + D/2.
+    constexpr int Q4 = D / 4;
+#pragma unroll
+    for (int qs = 0; qs < NS; ++qs) {
+      const int q = qrow[qs];
+      const uint32_t pp = (uint32_t)p.rope_pos[min(q, s1 - 1)];
+      float4 cs[NDT];
+#pragma unroll
+      for (int dt = 0; dt < NDT; ++dt) {
+        const int j0 = 8 * dt + 2 * g;
+        const int coord = (int)(j0 < Q4 ? (pp >> 16) : (pp & 0xFFFFu));
+        cs[dt] = *reinterpret_cast<const float4*>(p.rope_tab + coord * Q4 +
+                                                  (j0 < Q4 ? j0 : j0 - Q4));
+      }
+      if (q >= s1) continue;
+      bf16* row = dQ + (int64_t)q * p.ldd;
+#pragma unroll
+      for (int dt = 0; dt < NDT; ++dt) {
+        float x[4];
+#pragma unroll
+        for (int v = 0; v < 4; ++v) x[v] = dq[qs][dt][v] * p.scale;
+        const float4 c = cs[dt];
+        rope_unrotate(x[0], x[1], make_float2(c.x, c.y));
+        rope_unrotate(x[2], x[3], make_float2(c.z, c.w));
+        const int j0 = 8 * dt + 2 * g;
+        bf16 a2[2] = {(bf16)x[0], (bf16)x[2]}, b2[2] = {(bf16)x[1], (bf16)x[3]};
+        *reinterpret_cast<uint32_t*>(row + j0) = *reinterpret_cast<uint32_t*>(a2);
+        *reinterpret_cast<uint32_t*>(row + j0 + D / 2) = *reinterpret_cast<uint32_t*>(b2);
+      }
+    }
+    return;
+  }
 #pragma unroll
   for (int qs = 0; qs < NS; ++qs) {
     const int q = qrow[qs];
@@ -711,8 +779,17 @@ __global__ void attn_bwd_dq_f32_kernel(AttnArgs p) {
     const float ds = expf(s * p.scale - L) * (dp - del);
     for (int e = 0; e < D; ++e) dq[e] += ds * K[(int64_t)k * p.ld + e];
   }
-  float* dQ = reinterpret_cast<float*>(p.dq) + head * D;
-  for (int e = 0; e < D; ++e) dQ[(int64_t)q * p.ldd + e] = dq[e] * p.scale;
+  float* dQ = reinterpret_cast<float*>(p.dq) + head * D + (int64_t)q * p.ldd;
+  if (p.rope_pos != nullptr) {   // pair-interleaved q, k: rotate back, original order
+    for (int j = 0; j < D / 2; ++j) {
+      float a = dq[2 * j] * p.scale, b = dq[2 * j + 1] * p.scale;
+      rope_unrotate(a, b, rope_cs(p.rope_pos, p.rope_tab, D, q, j));
+      dQ[j] = a;
+      dQ[j + D / 2] = b;
+    }
+  } else {
+    for (int e = 0; e < D; ++e) dQ[e] = dq[e] * p.scale;
+  }
 }
 
 template <int D>
@@ -744,11 +821,18 @@ __global__ void attn_bwd_dkdv_f32_kernel(AttnArgs p) {
       dk[e] += ds * Q[(int64_t)q * p.ld + e];
     }
   }
-  float* dK = reinterpret_cast<float*>(p.dk) + head * D;
-  float* dV = reinterpret_cast<float*>(p.dv) + head * D;
-  for (int e = 0; e < D; ++e) {
-    dK[(int64_t)k * p.ldd + e] = dk[e] * p.scale;
-    dV[(int64_t)k * p.ldd + e] = dv[e];
+  float* dK = reinterpret_cast<float*>(p.dk) + head * D + (int64_t)k * p.ldd;
+  float* dV = reinterpret_cast<float*>(p.dv) + head * D + (int64_t)k * p.ldd;
+  for (int e = 0; e < D; ++e) dV[e] = dv[e];
+  if (p.rope_pos != nullptr) {   // pair-interleaved q, k: rotate back, original order
+    for (int j = 0; j < D / 2; ++j) {
+      float a = dk[2 * j] * p.scale, b = dk[2 * j + 1] * p.scale;
+      rope_unrotate(a, b, rope_cs(p.rope_pos, p.rope_tab, D, k, j));
+      dK[j] = a;
+      dK[j + D / 2] = b;
+    }
+  } else {
+    for (int e = 0; e < D; ++e) dK[e] = dk[e] * p.scale;
   }
 }
 

@@ -59,6 +59,51 @@ __device__ __forceinline__ float gelu_grad_fast(float u) {
   return fmaf(u, d, P);
 }
 
+// ---- 2D rotary position on pair-interleaved q / k columns ----------------------------
+// The encoder stores the q and k columns of every head pair-interleaved: stored column 2j
+// of a head holds rotary component j and stored column 2j + 1 holds component j + d/2,
+// the two components one rotation mixes.  q and k are permuted alike, so attention
+// scores are unchanged, and a rotation needs only adjacent values.  pos[row] packs the
+// patch position as y << 16 | x; tab[p * d/4 + k] = (cos, sin) of p * theta^(-4k/d).
+// Component j < d/4 turns by the angle of y, the others by that of x.
+
+// original head-local component of stored head-local column s
+__host__ __device__ __forceinline__ int rope_component(int s, int d) {
+  return (s & 1) ? (s >> 1) + (d >> 1) : (s >> 1);
+}
+// (cos, sin) of rotary pair j (< d/2) of packed row `row`
+__device__ __forceinline__ float2 rope_cs(const int32_t* pos, const float2* tab, int d,
+                                          int64_t row, int j) {
+  const uint32_t pp = (uint32_t)pos[row];
+  const int q4 = d >> 2;
+  const bool along_y = j < q4;
+  const int coord = (int)(along_y ? (pp >> 16) : (pp & 0xFFFFu));
+  return tab[coord * q4 + (along_y ? j : j - q4)];
+}
+// Forward rotation of (a, b) = (x_j, x_{j+d/2}); the backward applies the inverse.
+// Written with explicit fmaf so that every kernel and every unrolled copy rounds the
+// same way (a row's result must not depend on the tile or lane that computes it):
+//   rotate:   a' = fma(a, c, -(b s)),  b' = fma(b, c, a s)
+//   unrotate: a' = fma(a, c, b s),     b' = fma(b, c, -(a s))
+__device__ __forceinline__ float rope_first(float a, float b, float2 cs, bool inverse) {
+  const float bs = b * cs.y;
+  return fmaf(a, cs.x, inverse ? bs : -bs);
+}
+__device__ __forceinline__ float rope_second(float a, float b, float2 cs, bool inverse) {
+  const float as = a * cs.y;
+  return fmaf(b, cs.x, inverse ? -as : as);
+}
+__device__ __forceinline__ void rope_rotate(float& a, float& b, float2 cs) {
+  const float a0 = a;
+  a = rope_first(a0, b, cs, false);
+  b = rope_second(a0, b, cs, false);
+}
+__device__ __forceinline__ void rope_unrotate(float& a, float& b, float2 cs) {
+  const float a0 = a;
+  a = rope_first(a0, b, cs, true);
+  b = rope_second(a0, b, cs, true);
+}
+
 // bf16 pair packing helpers on 32-bit words (low half = first element)
 __device__ __forceinline__ uint32_t pack_lo(uint32_t a, uint32_t b) {  // a.lo | b.lo << 16
   return __builtin_amdgcn_perm(b, a, 0x05040100u);

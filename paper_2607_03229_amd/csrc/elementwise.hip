@@ -430,15 +430,17 @@ __global__ __launch_bounds__(256) void transpose_kernel(TJobs jb) {
   const int li = t / TPR, ci = (t % TPR) * VEC;
   for (int rr = li; rr < 64; rr += LPP) {       // load src rows r0+rr, cols c0+ci..
     const int r = r0 + rr, c = c0 + ci;
+    // the source row whose values land at stored row r
+    const int rs = r < J.perm_rows ? r - r % J.perm_d + rope_component(r % J.perm_d, J.perm_d) : r;
     if constexpr (VEC > 1) {
       if (r < J.rows && c < J.cols) {
-        const uint4 v = *reinterpret_cast<const uint4*>(src + (int64_t)r * J.lds + c);
+        const uint4 v = *reinterpret_cast<const uint4*>(src + (int64_t)rs * J.lds + c);
         const U* e = reinterpret_cast<const U*>(&v);
 #pragma unroll
         for (int k = 0; k < VEC; ++k) tile[rr][ci + k] = e[k];
       }
     } else {
-      if (r < J.rows && c < J.cols) tile[rr][ci] = src[(int64_t)r * J.lds + c];
+      if (r < J.rows && c < J.cols) tile[rr][ci] = src[(int64_t)rs * J.lds + c];
     }
   }
   __syncthreads();
@@ -755,6 +757,9 @@ hipError_t transpose_batch(int dtype, const TJob* jobs, int n, hipStream_t s) {
     const TJob& J = jobs[i];
     if (J.rows <= 0 || J.cols <= 0) continue;
     if (J.lds < J.cols || J.ldd < J.rows) return hipErrorInvalidValue;
+    if (J.perm_rows > 0 && (J.perm_d <= 0 || J.perm_d % 2 || J.perm_rows % J.perm_d ||
+                            J.perm_rows > J.rows))
+      return hipErrorInvalidValue;
     jb.j[jb.n] = J;
     jb.first[jb.n] = tiles;
     tiles += (int64_t)((J.rows + 63) / 64) * ((J.cols + 63) / 64);

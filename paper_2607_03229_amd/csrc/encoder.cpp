@@ -92,7 +92,7 @@ hipError_t run(mpipe_encoder* e, hipStream_t s, const char* cls, double flops, F
 
 const char* gemm_name(int layout, int epi) {
   static const char* L[] = {"NT", "NN", "TN"};
-  static const char* E[] = {"store", "gelu", "resid", "gelubwd", "f32"};
+  static const char* E[] = {"store", "gelu", "resid", "gelubwd", "f32", "storerope"};
   static std::map<int, std::string> names;
   const int key = layout * 8 + epi;
   auto it = names.find(key);
@@ -327,8 +327,12 @@ mpipe_status pad_pe(Ctx& x, const void* patches) {
 // Transposed copies of the [out][in] weights the next GEMMs multiply by, back to back in
 // the workspace: wt[i] = W_i^T ([in][out], row stride out), so that every forward GEMM
 // reads its weight operand K-major (whole 128-byte lines per DMA row).
+// qk_rows > 0: the first weight is the qkv weight, whose first qk_rows output rows (the q
+// and k blocks) are taken pair-interleaved within each head, so that its product comes
+// out in the layout the fused rotary epilogue and the attention kernels work on.
 mpipe_status weights_t(Ctx& x, int n, const void* const* W, const int64_t* out_f,
-                       const int64_t* in_f, const int64_t* ld, const void** wt) {
+                       const int64_t* in_f, const int64_t* ld, const void** wt,
+                       int qk_rows = 0) {
   TJob jobs[kMaxTJobs];
   char* dst = x.ws + x.P.ws_wt;
   for (int i = 0; i < n; ++i) {
@@ -338,6 +342,10 @@ mpipe_status weights_t(Ctx& x, int n, const void* const* W, const int64_t* out_f
     jobs[i].ldd = out_f[i];
     jobs[i].rows = (int)out_f[i];
     jobs[i].cols = (int)in_f[i];
+    if (i == 0 && qk_rows > 0) {
+      jobs[i].perm_rows = qk_rows;
+      jobs[i].perm_d = x.c.d;
+    }
     wt[i] = dst;
     dst += out_f[i] * in_f[i] * x.E;
   }
@@ -396,7 +404,7 @@ mpipe_status forward(Ctx& x, const void* patches, void* merged, char* tape) {
       const void* W[4] = {x.W(blk_param(c, l, B_QKVW)), x.W(blk_param(c, l, B_PROJW)),
                           x.W(blk_param(c, l, B_FC1W)), x.W(blk_param(c, l, B_FC2W))};
       const int64_t of[4] = {3 * h, h, m, h}, inf[4] = {h, h, h, m};
-      MP_RET(weights_t(x, 4, W, of, inf, inf, wt));
+      MP_RET(weights_t(x, 4, W, of, inf, inf, wt, (int)(2 * h)));
     }
     MP_CHECK(run(x.e, x.s, "layernorm", 0, [&] {
       return layernorm_fwd(x.dt, hin, h, N, (int)h, x.W(blk_param(c, l, B_LN1G)),
@@ -405,13 +413,16 @@ mpipe_status forward(Ctx& x, const void* patches, void* merged, char* tape) {
                            reinterpret_cast<float*>(base + S.rstd1), x.s);
     }));
     {
+      // q, k come out pair-interleaved per head with the 2D rotary position applied in
+      // the epilogue; v in plain order
       GemmArgs a = ga(A, h, wt[0], 3 * h, N, 3 * h, h, qkv, 3 * h);
       a.bias = x.W(blk_param(c, l, B_QKVB));
-      MP_RET(gemm_call(x, GEMM_NN, EPI_STORE, a));
+      a.rope_pos = pos;
+      a.rope_tab = reinterpret_cast<const float2*>(freq);
+      a.rope_d = c.d;
+      a.rope_cols = (int)(2 * h);
+      MP_RET(gemm_call(x, GEMM_NN, EPI_STORE_ROPE, a));
     }
-    MP_CHECK(run(x.e, x.s, "rope", 0, [&] {
-      return rope(x.dt, qkv, 3 * h, N, c.heads, c.d, (int)h, pos, freq, 0, x.s);
-    }));
     {
       AttnArgs a = attn_args(x, qkv, false);
       a.out = O;
@@ -628,14 +639,15 @@ mpipe_status backward(Ctx& x, const void* patches, const char* tape, const void*
         a->dk = dqkv + h * x.E;
         a->dv = dqkv + 2 * h * x.E;
         a->ldd = 3 * h;
+        // the tape's q, k are pair-interleaved and rotated: dQ, dK are written rotated
+        // back, in plain column order
+        a->rope_pos = pos;
+        a->rope_tab = reinterpret_cast<const float2*>(freq);
       }
       const double f = 2.0 * c.heads * c.d * (double)P.sum_len2;
       MP_CHECK(run(x.e, x.s, "attn_bwd_dq", f, [&] { return attention_bwd_dq(x.dt, c.d, qa, x.s); }));
       MP_CHECK(run(x.e, x.s, "attn_bwd_dkdv", 3 * f, [&] { return attention_bwd_dkdv(x.dt, c.d, ka, x.s); }));
     }
-    MP_CHECK(run(x.e, x.s, "rope", 0, [&] {
-      return rope(x.dt, dqkv, 3 * h, N, c.heads, c.d, (int)h, pos, freq, 1, x.s);
-    }));
     MP_CHECK(ss.fork());   // dqkv
     MP_RET(dw_gemm(x, dqkv, 3 * h, base + S.a, h, 3 * h, h, N, x.grad(dw, blk_param(c, l, B_QKVW)), h));
     MP_RET(colsum(x, x.dt, dqkv, 3 * h, N, (int)(3 * h), x.grad(dw, blk_param(c, l, B_QKVB))));

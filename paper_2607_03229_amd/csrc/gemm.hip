@@ -199,15 +199,23 @@ __device__ __forceinline__ void epilogue(const GemmArgs& p, int split, int m0, i
   for (int j = 0; j < 4; ++j) {
     const int n = n0 + 16 * j + r;
     if (n >= p.N) continue;
-    const float bv = (bias != nullptr && split == 0) ? to_f(bias[n]) : 0.0f;
+    // rotary columns (q, k) are stored pair-interleaved: bias of the original column
+    const bool rot = EPI == EPI_STORE_ROPE && n < p.rope_cols;
+    const int nb = rot ? n - n % p.rope_d + rope_component(n % p.rope_d, p.rope_d) : n;
+    const float bv = (bias != nullptr && split == 0) ? to_f(bias[nb]) : 0.0f;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
 #pragma unroll
       for (int v = 0; v < 4; ++v) {
         const int m = m0 + 16 * i + 4 * g + v;
         if (m >= p.M) continue;
-        const float x = acc[i][j][v] + bv;
-        if constexpr (EPI == EPI_STORE) {
+        float x = acc[i][j][v] + bv;
+        if constexpr (EPI == EPI_STORE || EPI == EPI_STORE_ROPE) {
+          if (rot) {   // the pair partner (column n ^ 1, same row) is in lane l ^ 1
+            const float y = __shfl_xor(x, 1);
+            const float2 cs = rope_cs(p.rope_pos, p.rope_tab, p.rope_d, m, (n % p.rope_d) >> 1);
+            x = (n & 1) ? rope_second(y, x, cs, false) : rope_first(x, y, cs, false);
+          }
           reinterpret_cast<T*>(p.C)[(int64_t)m * p.ldc + n] = from_f<T>(x);
         } else if constexpr (EPI == EPI_GELU) {
           // GELU and GELU' at the rounded pre-activation u; the backward multiplies by
@@ -322,6 +330,7 @@ template <class T, bool AK, bool BKM>
 hipError_t dispatch_epi(const GemmArgs& a, int epi, hipStream_t s) {
   switch (epi) {
     case EPI_STORE: return launch<T, AK, BKM, EPI_STORE>(a, s);
+    case EPI_STORE_ROPE: return launch<T, AK, BKM, EPI_STORE_ROPE>(a, s);
     case EPI_GELU: return launch<T, AK, BKM, EPI_GELU>(a, s);
     case EPI_RESID: return launch<T, AK, BKM, EPI_RESID>(a, s);
     case EPI_GELU_BWD: return launch<T, AK, BKM, EPI_GELU_BWD>(a, s);

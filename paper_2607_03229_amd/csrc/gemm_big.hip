@@ -144,7 +144,38 @@ __device__ __forceinline__ void aux_fetch(const GemmArgs& p, int split, int m, i
       a.v[0] = *reinterpret_cast<const uint4*>(C);
       a.v[1] = *reinterpret_cast<const uint4*>(C + 4);
     }
+  } else if constexpr (EPI == EPI_STORE_ROPE) {
+    // (cos, sin) of the four rotary pairs of columns n..n+7 at row m: consecutive table
+    // entries (a head's d/4 pairs per axis are a multiple of 4, so they share an axis)
+    if (n < p.rope_cols) {
+      const int q4 = p.rope_d >> 2, j0 = (n % p.rope_d) >> 1;
+      const uint32_t pp = (uint32_t)p.rope_pos[m];
+      const int coord = (int)(j0 < q4 ? (pp >> 16) : (pp & 0xFFFFu));
+      const float2* t = p.rope_tab + coord * q4 + (j0 < q4 ? j0 : j0 - q4);
+      a.v[0] = *reinterpret_cast<const uint4*>(t);
+      a.v[1] = *reinterpret_cast<const uint4*>(t + 2);
+    }
   }
+}
+
+// The bias of a lane's eight columns n..n+7 (zeros when `take` is false).  Columns that
+// get the fused rotary position are stored pair-interleaved, so their bias entries come
+// from the original columns.
+__device__ __forceinline__ void load_bias8(const GemmArgs& p, bool take, int n, float* bias8) {
+#pragma unroll
+  for (int e = 0; e < 8; ++e) bias8[e] = 0.f;
+  if (!take || p.bias == nullptr) return;
+  const bf16* bias = reinterpret_cast<const bf16*>(p.bias);
+  if (p.rope_pos != nullptr && n < p.rope_cols) {   // EPI_STORE_ROPE's q, k columns
+    const int base = n - n % p.rope_d, s0 = n % p.rope_d;   // eight columns of one head
+#pragma unroll
+    for (int e = 0; e < 8; ++e) bias8[e] = (float)bias[base + rope_component(s0 + e, p.rope_d)];
+    return;
+  }
+  const uint4 bb = *reinterpret_cast<const uint4*>(bias + n);
+  const bf16* b8 = reinterpret_cast<const bf16*>(&bb);
+#pragma unroll
+  for (int e = 0; e < 8; ++e) bias8[e] = (float)b8[e];
 }
 
 template <int EPI>
@@ -153,9 +184,17 @@ __device__ __forceinline__ void epi8_vec(const GemmArgs& p, int split, int m, in
                                          float* sum8 = nullptr) {
 #pragma unroll
   for (int e = 0; e < 8; ++e) v[e] += bias8[e];
-  if constexpr (EPI == EPI_STORE || EPI == EPI_GELU || EPI == EPI_GELU_BWD) {
+  if constexpr (EPI == EPI_STORE || EPI == EPI_STORE_ROPE || EPI == EPI_GELU ||
+                EPI == EPI_GELU_BWD) {
     bf16 o[8];
-    if constexpr (EPI == EPI_STORE) {
+    if constexpr (EPI == EPI_STORE || EPI == EPI_STORE_ROPE) {
+      if constexpr (EPI == EPI_STORE_ROPE) {
+        if (n < p.rope_cols) {   // q, k: rotate the four pairs by the prefetched angles
+          const float2* cs = reinterpret_cast<const float2*>(&ax.v[0]);
+#pragma unroll
+          for (int e = 0; e < 8; e += 2) rope_rotate(v[e], v[e + 1], cs[e / 2]);
+        }
+      }
 #pragma unroll
       for (int e = 0; e < 8; ++e) o[e] = (bf16)v[e];
     } else if constexpr (EPI == EPI_GELU) {
@@ -475,16 +514,10 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_big_kernel(GemmArgs p) {
   const int n = n0 + wn * 128 + 8 * cg;   // N % 8 == 0: all eight columns or none in range
   const bool vec = n < p.N;
   float bias8[8];
-#pragma unroll
-  for (int e = 0; e < 8; ++e) bias8[e] = 0.f;
-  if (vec && p.bias != nullptr && split == 0) {
-    const uint4 bb = *reinterpret_cast<const uint4*>(reinterpret_cast<const bf16*>(p.bias) + n);
-    const bf16* b8 = reinterpret_cast<const bf16*>(&bb);
-#pragma unroll
-    for (int e = 0; e < 8; ++e) bias8[e] = (float)b8[e];
-  }
+  load_bias8(p, vec && split == 0, n, bias8);
   auto row_of = [&](int pi, int u) { return m0 + wm * (32 * MT) + 16 * pi + (l >> 4) + 4 * u; };
-  constexpr bool kAux = EPI == EPI_GELU_BWD || EPI == EPI_RESID || EPI == EPI_F32;
+  constexpr bool kAux = EPI == EPI_GELU_BWD || EPI == EPI_RESID || EPI == EPI_F32 ||
+                        EPI == EPI_STORE_ROPE;
   AuxV ax[2][4];
   auto fetch = [&](int pi, AuxV (&dst)[4]) __attribute__((always_inline)) {
     if constexpr (kAux) {
@@ -826,21 +859,15 @@ __global__ __launch_bounds__(NTHR, 2) void gemm_nn_kernel(GemmArgs p) {
   const int n = n0 + wn * 128 + 8 * cg;
   const bool vec = n < p.N;
   float bias8[8];
-#pragma unroll
-  for (int e = 0; e < 8; ++e) bias8[e] = 0.f;
-  if (vec && p.bias != nullptr && split == 0) {
-    const uint4 bb = *reinterpret_cast<const uint4*>(reinterpret_cast<const bf16*>(p.bias) + n);
-    const bf16* b8 = reinterpret_cast<const bf16*>(&bb);
-#pragma unroll
-    for (int e = 0; e < 8; ++e) bias8[e] = (float)b8[e];
-  }
+  load_bias8(p, vec && split == 0, n, bias8);
   auto row_of = [&](int pi, int u) { return m0 + wm * 64 + 16 * pi + (l >> 4) + 4 * u; };
   // GELU-backward column sums over this wave's 64-row band (p.colsum is grid-uniform)
   const bool kSum = EPI == EPI_GELU_BWD && p.colsum != nullptr;
   float cs[8];
 #pragma unroll
   for (int e = 0; e < 8; ++e) cs[e] = 0.f;
-  constexpr bool kAux = EPI == EPI_GELU_BWD || EPI == EPI_RESID || EPI == EPI_F32;
+  constexpr bool kAux = EPI == EPI_GELU_BWD || EPI == EPI_RESID || EPI == EPI_F32 ||
+                        EPI == EPI_STORE_ROPE;
   AuxV ax[2][4];
   auto fetch = [&](int pi, AuxV (&dst)[4]) __attribute__((always_inline)) {
     if constexpr (kAux) {
@@ -921,6 +948,7 @@ hipError_t launch_nn(const GemmArgs& a0, hipStream_t s) {
 hipError_t dispatch_nn(const GemmArgs& a, int epi, hipStream_t s) {
   switch (epi) {
     case EPI_STORE: return launch_nn<EPI_STORE>(a, s);
+    case EPI_STORE_ROPE: return launch_nn<EPI_STORE_ROPE>(a, s);
     case EPI_GELU: return launch_nn<EPI_GELU>(a, s);
     case EPI_RESID: return launch_nn<EPI_RESID>(a, s);
     case EPI_GELU_BWD: return launch_nn<EPI_GELU_BWD>(a, s);

@@ -7,7 +7,8 @@ namespace mpipe {
 
 enum { DT_F32 = 0, DT_BF16 = 1 };
 enum { GEMM_NT = 0, GEMM_NN = 1, GEMM_TN = 2 };
-enum { EPI_STORE = 0, EPI_GELU = 1, EPI_RESID = 2, EPI_GELU_BWD = 3, EPI_F32 = 4 };
+enum { EPI_STORE = 0, EPI_GELU = 1, EPI_RESID = 2, EPI_GELU_BWD = 3, EPI_F32 = 4,
+       EPI_STORE_ROPE = 5 };
 constexpr int ATTN_TILE = 128;   // queries (forward, dQ) or keys (dK/dV) per attention work item
 
 // C[m][n] = sum_k A(m,k) B(n,k) + epilogue.
@@ -19,6 +20,7 @@ constexpr int ATTN_TILE = 128;   // queries (forward, dQ) or keys (dK/dV) per at
 //   EPI_RESID     C(f32) = aux(f32, may alias C, may be null) + acc + bias
 //   EPI_GELU_BWD  C(T)   = acc * aux(T)   (aux = the GELU'(u) the forward stored)
 //   EPI_F32       C(f32) = acc (+ C if beta)
+//   EPI_STORE_ROPE C(T)  = EPI_STORE, then the 2D rotary position on columns < rope_cols
 struct GemmArgs {
   const void* A = nullptr;
   const void* B = nullptr;
@@ -36,6 +38,12 @@ struct GemmArgs {
   // EPI_GELU_BWD on the 128x256 NN kernel only (gemm_fused_colsum says when): column sums
   // of the stored output over each band of 64 rows, colsum[m / 64][n], fp32, row stride N
   float* colsum = nullptr;
+  // EPI_STORE_ROPE: 2D rotary position on output columns n < rope_cols (the q and k
+  // blocks of a qkv product, heads of rope_d columns, stored pair-interleaved as in
+  // common.h); the bias of those columns is indexed by the original column.
+  const int32_t* rope_pos = nullptr;
+  const float2* rope_tab = nullptr;
+  int rope_d = 0, rope_cols = 0;
 };
 hipError_t gemm(int dtype, int layout, int epi, const GemmArgs& a, hipStream_t s);
 // Whether gemm() runs this problem on the NN kernel that can write GemmArgs::colsum.
@@ -66,6 +74,11 @@ struct AttnArgs {
   int heads = 0;
   int64_t N = 0;
   float scale = 0.f;
+  // Backward only: q and k are stored pair-interleaved with the rotary position applied
+  // (the forward's fused qkv epilogue); dQ and dK are then written rotated back and in
+  // the original column order.  Null: plain columns, no rotation.
+  const int32_t* rope_pos = nullptr;
+  const float2* rope_tab = nullptr;
 };
 bool attention_supported(int dtype, int head_dim);
 hipError_t attention_fwd(int dtype, int head_dim, const AttnArgs& a, hipStream_t s);
@@ -105,12 +118,17 @@ hipError_t splitk_reduce(const float* part, int splits, int64_t M, int64_t N, fl
                          int64_t ldo, hipStream_t s);
 // Batched transpose of up to kMaxTJobs matrices in one launch: dst[c][r] = src[r][c]
 // for r < rows, c < cols (row strides lds, ldd in elements; element bits are copied).
+// With perm_rows > 0, source rows r < perm_rows are taken in pair-interleaved order
+// within each block of perm_d rows (common.h): dst[c][s] = src[row of s][c], where s
+// indexes the stored order -- the forward's qkv weight, so that its product comes out
+// with q and k pair-interleaved.
 struct TJob {
   const void* src = nullptr;
   int64_t lds = 0;
   void* dst = nullptr;
   int64_t ldd = 0;
   int rows = 0, cols = 0;
+  int perm_rows = 0, perm_d = 0;
 };
 constexpr int kMaxTJobs = 4;
 hipError_t transpose_batch(int dtype, const TJob* jobs, int n, hipStream_t s);
