@@ -164,6 +164,105 @@ def summarize_pmc(fetch_cal: str, write_cal: str, fetch_db: str, write_db: str, 
     print(json.dumps(rec, indent=1))
 
 
+# ---- rocprofv3 summaries kept under profiles/ ---------------------------------------
+SQ_PASS1 = ("SQ_VALU_MFMA_BUSY_CYCLES SQ_INSTS_MFMA SQ_INSTS_VALU SQ_ACTIVE_INST_VALU "
+            "SQ_LDS_BANK_CONFLICT SQ_ACTIVE_INST_LDS SQ_WAVE_CYCLES SQ_WAIT_ANY GRBM_GUI_ACTIVE")
+SQ_PASS2 = ("SQ_VALU_MFMA_COEXEC_CYCLES SQ_INSTS_LDS SQ_WAIT_INST_LDS SQ_INSTS_VALU_TRANS_F32 "
+            "SQ_INSTS_SALU GRBM_GUI_ACTIVE")
+N_XCD, N_CU, N_SIMD = 8, 256, 1024
+
+
+def summarize_trace(db: str, bench_json: str, cmds: str, out: str):
+    """rocprofv3 --kernel-trace --stats database -> markdown table of the top kernels, with
+    the library's class of each and the bench line of the same run."""
+    import sqlite3
+    c = sqlite3.connect(db)
+    rows = list(c.execute("select name, total_calls, total_duration, average, percentage "
+                          "from top_kernels order by total_duration desc"))
+    r = json.loads(open(bench_json).read().strip().splitlines()[-1])
+    L = [f"# Kernel trace: encoder training step, {r['config']['workload']} (seed {r['config']['seed']})",
+         "", "Command (on the MI355X box):", "", "```", cmds, "```", "",
+         "| kernel [library class] | calls | total ms | avg us | % of kernel time |",
+         "|---|---:|---:|---:|---:|"]
+    for name, n, tot, avg, pct in rows[:28]:
+        cls = kernel_class(name)
+        short = name if len(name) < 90 else name[:87] + "..."
+        L.append(f"| `{short}`{' [' + cls + ']' if cls else ''} | {n} | {tot / 1e3:.1f} | "
+                 f"{avg:.1f} | {pct:.1f} |")
+    L += ["", f"Bench line of the same run: {r['ms_per_step']} ms/step, {r['value']:,} patch-tokens/s, "
+              f"{r['model_tflop_per_step']} model TFLOP/step = {r['achieved_tflops']} TFLOP/s = "
+              f"{r['mfma_pct_of_peak']} % of the {PEAK_BF16_TFLOPS} TFLOP/s bf16 dense peak "
+              f"(hardware FLOPs: {r['hw_mfma_pct_of_peak']} %)."]
+    for key in ("roofline", "roofline_largest_class"):
+        roof = r.get(key)
+        if not roof:
+            continue
+        tr = [x for x in rows if kernel_class(x[0]) == roof["kernel"]]
+        if tr:
+            n = sum(x[1] for x in tr)
+            tot = sum(x[2] for x in tr)
+            L.append(f"`{key}` class `{roof['kernel']}` ({roof['stream']} stream): the library's "
+                     f"HIP events give avg {roof['avg_ms'] * 1e3:.1f} us over {roof['launches']} "
+                     f"launches; the trace gives avg {tot / n:.1f} us over {n} dispatches "
+                     f"(the trace also covers the warmup step and the per-kernel pass).")
+    open(out, "w").write("\n".join(L) + "\n")
+    print("\n".join(L))
+
+
+def summarize_sq(db1: str, db2: str, cmds: str, out: str):
+    """Two rocprofv3 --pmc passes of SQ counters over one step -> per kernel class averages
+    and the derived per-SIMD / per-CU fractions (formulas in the table header)."""
+    per = {}
+    for db, names in ((db1, SQ_PASS1.split()), (db2, SQ_PASS2.split())):
+        for counter in names:
+            vals = _pmc_by_dispatch(db, counter)
+            for (d, n), v in vals.items():
+                cls = kernel_class(n) or ("layernorm_bwd" if "ln_bwd_kernel" in n else
+                                          "layernorm" if "ln_fwd_kernel" in n else None)
+                if cls is None:
+                    continue
+                e = per.setdefault(cls, {}).setdefault(counter, {})
+                e[(db, d)] = v
+    L = [f"# SQ counters per kernel class: encoder training step (c4_qwen2vl_trained, seed 0)", "",
+         "Two `rocprofv3 --pmc` passes of one bench step (kernels are serialized while counters",
+         "are taken, so these are each kernel's own figures, without the side-stream overlap).",
+         "Commands (on the MI355X box):", "", "```", cmds, "```", "",
+         f"Per dispatch: `cyc` = GRBM_GUI_ACTIVE / {N_XCD} (GPU-active cycles of one XCD); "
+         f"MFMA busy = SQ_VALU_MFMA_BUSY_CYCLES / (cyc x {N_SIMD} SIMDs); MFMA+VALU co-issue = "
+         f"SQ_VALU_MFMA_COEXEC_CYCLES / (cyc x {N_SIMD}); VALU active = 4 SQ_ACTIVE_INST_VALU / "
+         f"(cyc x {N_SIMD}); LDS bank-conflict = SQ_LDS_BANK_CONFLICT / (cyc x {N_CU} CUs); "
+         "waiting = SQ_WAIT_ANY / SQ_WAVE_CYCLES; waves/SIMD = 4 SQ_WAVE_CYCLES / "
+         f"(cyc x {N_SIMD}).  Instruction counts are per SIMD per dispatch.", "",
+         "| class | dispatches | MFMA busy | co-issue | VALU active | LDS bank-conflict | waiting "
+         "| waves/SIMD | MFMA inst | VALU inst | trans inst | LDS inst |",
+         "|---|---:|---:|---:|---:|---:|---:|---:|---:|---:|---:|---:|"]
+
+    def avg(e, c):
+        v = list(e.get(c, {}).values())
+        return sum(v) / len(v) if v else float("nan")
+
+    rows = []
+    for cls, e in per.items():
+        cyc = avg(e, "GRBM_GUI_ACTIVE") / N_XCD
+        if not cyc or cyc != cyc:
+            continue
+        nd = len(e.get("SQ_INSTS_MFMA", {}))
+        rows.append((avg(e, "SQ_VALU_MFMA_BUSY_CYCLES") * nd, cls, [
+            nd, avg(e, "SQ_VALU_MFMA_BUSY_CYCLES") / (cyc * N_SIMD),
+            avg(e, "SQ_VALU_MFMA_COEXEC_CYCLES") / (cyc * N_SIMD),
+            4 * avg(e, "SQ_ACTIVE_INST_VALU") / (cyc * N_SIMD),
+            avg(e, "SQ_LDS_BANK_CONFLICT") / (cyc * N_CU),
+            avg(e, "SQ_WAIT_ANY") / max(avg(e, "SQ_WAVE_CYCLES"), 1.0),
+            4 * avg(e, "SQ_WAVE_CYCLES") / (cyc * N_SIMD),
+            avg(e, "SQ_INSTS_MFMA") / N_SIMD, avg(e, "SQ_INSTS_VALU") / N_SIMD,
+            avg(e, "SQ_INSTS_VALU_TRANS_F32") / N_SIMD, avg(e, "SQ_INSTS_LDS") / N_SIMD]))
+    for _, cls, v in sorted(rows, reverse=True):
+        L.append(f"| `{cls}` | {v[0]} | {v[1]:.3f} | {v[2]:.3f} | {v[3]:.3f} | {v[4]:.3f} | "
+                 f"{v[5]:.3f} | {v[6]:.2f} | {v[7]:,.0f} | {v[8]:,.0f} | {v[9]:,.0f} | {v[10]:,.0f} |")
+    open(out, "w").write("\n".join(L) + "\n")
+    print("\n".join(L))
+
+
 def stored_traffic(cls: str):
     try:
         with open(TRAFFIC_FILE) as fh:
@@ -387,11 +486,21 @@ def main():
     ap.add_argument("--summarize-pmc", nargs=4, metavar=("FETCH_CAL", "WRITE_CAL", "FETCH", "WRITE"),
                     help="rocprofv3 PMC databases -> profiles/hbm_traffic.json")
     ap.add_argument("--pmc-commands", default="", help="commands recorded with --summarize-pmc")
+    ap.add_argument("--summarize-trace", nargs=3, metavar=("DB", "BENCH_JSON", "OUT_MD"),
+                    help="rocprofv3 kernel-trace database -> a markdown summary")
+    ap.add_argument("--summarize-sq", nargs=3, metavar=("PASS1_DB", "PASS2_DB", "OUT_MD"),
+                    help="two rocprofv3 SQ-counter databases -> a markdown summary")
     ap.add_argument("--gemm-vs-library", action="store_true",
                     help="only time the step's GEMM shapes alone, against torch.mm (hipBLASLt)")
     args = ap.parse_args()
     if args.summarize_pmc:
         summarize_pmc(*args.summarize_pmc, args.pmc_commands)
+        return
+    if args.summarize_trace:
+        summarize_trace(*args.summarize_trace[:2], args.pmc_commands, args.summarize_trace[2])
+        return
+    if args.summarize_sq:
+        summarize_sq(*args.summarize_sq[:2], args.pmc_commands, args.summarize_sq[2])
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one MI355X only: the encoder step runs on one GPU "
