@@ -447,16 +447,17 @@ __global__ __launch_bounds__(64 * (8 / NS), NS == 2 ? 2 : 1) void attn_bwd_dkdv_
         const float4 lq = *reinterpret_cast<const float4*>(lse_s + q4);
         const float4 eq = *reinterpret_cast<const float4*>(del_s + q4);
         const float nl[4] = {-lq.x * kLog2e, -lq.y * kLog2e, -lq.z * kLog2e, -lq.w * kLog2e};
-        const float de[4] = {eq.x, eq.y, eq.z, eq.w};
+        const f32x4 mde = {eq.x, eq.y, eq.z, eq.w};   // -delta as stored
 #pragma unroll
         for (int ks = 0; ks < NS; ++ks) {
           f32x4 s = dot_d<D>(q_s, qb16, r, kf[ks], g, f32x4{0.f, 0.f, 0.f, 0.f});
-          f32x4 dp = dot_d<D>(do_s, qb16, r, vf[ks], g, f32x4{0.f, 0.f, 0.f, 0.f});
+          // the dP accumulator starts at -delta, so the products leave dP - delta
+          f32x4 dpd = dot_d<D>(do_s, qb16, r, vf[ks], g, mde);
 #pragma unroll
           for (int v = 0; v < 4; ++v) {
             const float pp = fast_exp2(fmaf(s[v], sl2, nl[v]));
             P[h2][ks][v] = pp;
-            dS[h2][ks][v] = pp * (dp[v] - de[v]);
+            dS[h2][ks][v] = pp * dpd[v];
           }
         }
         if (qb + 64 > s1) {   // ragged last tile: queries past the segment contribute nothing
@@ -562,7 +563,8 @@ __global__ __launch_bounds__(64 * (8 / NS), NS == 2 ? 3 : 1) void attn_bwd_dq_ke
 
   RowFrag<D> qf[NS], dof[NS];
   int qrow[NS];
-  float lse2[NS], del[NS];
+  float lse2[NS];
+  f32x4 mdel[NS];   // -delta of the lane's query, in every element
 #pragma unroll
   for (int qs = 0; qs < NS; ++qs) {
     qrow[qs] = q0 + RW * w + 16 * qs + r;
@@ -581,8 +583,8 @@ __global__ __launch_bounds__(64 * (8 / NS), NS == 2 ? 3 : 1) void attn_bwd_dq_ke
       for (int e = 0; e < 8; ++e) dl += (float)of.f[f][e] * (float)dof[qs].f[f][e];
     dl += __shfl_xor(dl, 16);
     dl += __shfl_xor(dl, 32);
-    del[qs] = dl;
-    if (g == 0 && qrow[qs] < s1) p.delta_out[(int64_t)head * p.N + qrow[qs]] = dl;
+    mdel[qs] = f32x4{-dl, -dl, -dl, -dl};
+    if (g == 0 && qrow[qs] < s1) p.delta_out[(int64_t)head * p.N + qrow[qs]] = -dl;
   }
   f32x4 dq[NS][NDT];
 #pragma unroll
@@ -616,11 +618,12 @@ __global__ __launch_bounds__(64 * (8 / NS), NS == 2 ? 3 : 1) void attn_bwd_dq_ke
 #pragma unroll
       for (int qs = 0; qs < NS; ++qs) {
         f32x4 sv = dot_d<D>(k_s, 16 * kq, r, qf[qs], g, f32x4{0.f, 0.f, 0.f, 0.f});
-        f32x4 dp = dot_d<D>(v_s, 16 * kq, r, dof[qs], g, f32x4{0.f, 0.f, 0.f, 0.f});
+        // the dP accumulator starts at -delta, so the products leave dP - delta
+        f32x4 dpd = dot_d<D>(v_s, 16 * kq, r, dof[qs], g, mdel[qs]);
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
           const float pp = fast_exp2(fmaf(sv[v], sl2, -lse2[qs]));
-          ds[kq][qs][v] = pp * (dp[v] - del[qs]);
+          ds[kq][qs][v] = pp * dpd[v];
         }
       }
     if (kb + 64 > s1) {   // ragged last tile: keys past the segment contribute nothing
@@ -706,7 +709,7 @@ __global__ __launch_bounds__(64 * (8 / NS), NS == 2 ? 3 : 1) void attn_bwd_dq_ke
   }
 }
 
-// ---- delta = rowsum(dO o O) per (head, query) ----------------------------------------
+// ---- -delta = -rowsum(dO o O) per (head, query), stored negated --------------------------
 
 template <class T>
 __global__ void attn_delta_kernel(const T* O, const T* dO, int64_t ldo, int64_t N, int heads,
@@ -718,7 +721,7 @@ __global__ void attn_delta_kernel(const T* O, const T* dO, int64_t ldo, int64_t 
   float s = 0.f;
   for (int e = 0; e < d; ++e)
     s += to_f(O[q * ldo + hd * d + e]) * to_f(dO[q * ldo + hd * d + e]);
-  delta[(int64_t)hd * N + q] = s;
+  delta[(int64_t)hd * N + q] = -s;
 }
 
 // ---- fp32 kernels: one thread per query (forward, dQ) or per key (dK, dV) -------------
@@ -769,14 +772,14 @@ __global__ void attn_bwd_dq_f32_kernel(AttnArgs p) {
     dov[e] = dO[(int64_t)q * p.ldo + e];
     dq[e] = 0.f;
   }
-  const float L = p.lse[(int64_t)head * p.N + q], del = p.delta_out[(int64_t)head * p.N + q];
+  const float L = p.lse[(int64_t)head * p.N + q], mdel = p.delta_out[(int64_t)head * p.N + q];
   for (int k = s0; k < s1; ++k) {
     float s = 0.f, dp = 0.f;
     for (int e = 0; e < D; ++e) {
       s += qv[e] * K[(int64_t)k * p.ld + e];
       dp += dov[e] * V[(int64_t)k * p.ld + e];
     }
-    const float ds = expf(s * p.scale - L) * (dp - del);
+    const float ds = expf(s * p.scale - L) * (dp + mdel);
     for (int e = 0; e < D; ++e) dq[e] += ds * K[(int64_t)k * p.ld + e];
   }
   float* dQ = reinterpret_cast<float*>(p.dq) + head * D + (int64_t)q * p.ldd;
@@ -815,7 +818,7 @@ __global__ void attn_bwd_dkdv_f32_kernel(AttnArgs p) {
       dp += dO[(int64_t)q * p.ldo + e] * vv[e];
     }
     const float pp = expf(s * p.scale - p.lse[(int64_t)head * p.N + q]);
-    const float ds = pp * (dp - p.delta[(int64_t)head * p.N + q]);
+    const float ds = pp * (dp + p.delta[(int64_t)head * p.N + q]);
     for (int e = 0; e < D; ++e) {
       dv[e] += pp * dO[(int64_t)q * p.ldo + e];
       dk[e] += ds * Q[(int64_t)q * p.ld + e];

@@ -67,8 +67,10 @@ struct AttnArgs {
   void* dv = nullptr;
   int64_t ldd = 0;
   float* lse = nullptr;        // [heads][N], natural log
-  const float* delta = nullptr;  // [heads][N] rowsum(dO o O), read by the dK/dV kernel
-  float* delta_out = nullptr;     // [heads][N], written by the dQ kernel
+  // [heads][N] -rowsum(dO o O), stored negated so that the bf16 kernels can start their
+  // dP accumulators with it: written by the dQ kernel, read by the dK/dV kernel
+  const float* delta = nullptr;
+  float* delta_out = nullptr;
   const int4* work = nullptr;  // (tile start row, segment start, segment end, 0)
   int n_work = 0;
   int heads = 0;
