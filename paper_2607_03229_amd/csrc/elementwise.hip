@@ -140,8 +140,9 @@ __device__ __forceinline__ void combine_waves(const float4* red, int nc, float* 
   }
 }
 
-template <class T, int MC>
-__global__ __launch_bounds__(256) void ln_bwd_kernel(const float* dY, int64_t ldd, const float* X,
+// DY: the type of dY (fp32, or bf16 as the encoder's bf16 input-gradient GEMMs store it)
+template <class T, int MC, class DY>
+__global__ __launch_bounds__(256) void ln_bwd_kernel(const DY* dY, int64_t ldd, const float* X,
                                                      int64_t ldx, const float* mean,
                                                      const float* rstd, const T* gam, int64_t rows,
                                                      int n, int64_t rows_per_block,
@@ -167,7 +168,7 @@ __global__ __launch_bounds__(256) void ln_bwd_kernel(const float* dY, int64_t ld
       const int c = l + 64 * i;
       if (c < nc) {
         x[i] = V4<float>::load(X + row * ldx + 4 * c);
-        dy[i] = V4<float>::load(dY + row * ldd + 4 * c);
+        dy[i] = V4<DY>::load(dY + row * ldd + 4 * c);
       }
     }
     float s1 = 0.f, s2 = 0.f;
@@ -632,11 +633,11 @@ int64_t layernorm_bwd_partial_rows(int64_t rows) {
   return b < LN_BWD_MAX_BLOCKS ? b : LN_BWD_MAX_BLOCKS;
 }
 
-hipError_t layernorm_bwd_partials(int dtype, const float* dY, int64_t ldd, const float* X,
-                                  int64_t ldx, const float* mean, const float* rstd, const void* g,
-                                  int64_t rows, int n, const float* dres, float* dX, void* dXt,
-                                  float* part_g, float* part_b, float* part_c, int64_t* blocks,
-                                  hipStream_t s) {
+hipError_t layernorm_bwd_partials(int dtype, const void* dY, int dy_dtype, int64_t ldd,
+                                  const float* X, int64_t ldx, const float* mean, const float* rstd,
+                                  const void* g, int64_t rows, int n, const float* dres, float* dX,
+                                  void* dXt, float* part_g, float* part_b, float* part_c,
+                                  int64_t* blocks, hipStream_t s) {
   *blocks = 0;
   if (rows == 0) return hipSuccess;
   // one round of resident blocks (never more than the partial rows the caller sized)
@@ -645,16 +646,18 @@ hipError_t layernorm_bwd_partials(int dtype, const float* dY, int64_t ldd, const
   float* pc = dX ? part_c : nullptr;
   auto go = [&](auto MCc) {
     constexpr int MC = decltype(MCc)::value;
-    auto launch = [&](auto kern, auto gptr, auto dxt) {
+    auto launch = [&](auto kern, auto dy, auto gptr, auto dxt) {
       nblk = std::min(layernorm_bwd_partial_rows(rows), resident_blocks<MC>(kern, 256));
       const int64_t rpb = (rows + nblk - 1) / nblk;
-      hipLaunchKernelGGL(kern, dim3((unsigned)nblk), dim3(256), 0, s, dY, ldd, X, ldx, mean, rstd,
+      hipLaunchKernelGGL(kern, dim3((unsigned)nblk), dim3(256), 0, s, dy, ldd, X, ldx, mean, rstd,
                          gptr, rows, n, rpb, dres, dX, dxt, part_g, part_b, pc);
     };
-    if (dtype == DT_BF16)
-      launch(ln_bwd_kernel<bf16, MC>, (const bf16*)g, (bf16*)dXt);
+    if (dtype == DT_BF16 && dy_dtype == DT_BF16)
+      launch(ln_bwd_kernel<bf16, MC, bf16>, (const bf16*)dY, (const bf16*)g, (bf16*)dXt);
+    else if (dtype == DT_BF16)
+      launch(ln_bwd_kernel<bf16, MC, float>, (const float*)dY, (const bf16*)g, (bf16*)dXt);
     else
-      launch(ln_bwd_kernel<float, MC>, (const float*)g, (float*)dXt);
+      launch(ln_bwd_kernel<float, MC, float>, (const float*)dY, (const float*)g, (float*)dXt);
   };
   if (!dispatch_mc(mc, go)) return hipErrorInvalidValue;
   *blocks = nblk;
@@ -680,8 +683,8 @@ hipError_t layernorm_bwd(int dtype, const float* dY, int64_t ldd, const float* X
                          hipStream_t s) {
   if (!dX || !grad_c) part_c = grad_c = nullptr;
   int64_t nb = 0;
-  hipError_t r = layernorm_bwd_partials(dtype, dY, ldd, X, ldx, mean, rstd, g, rows, n, dres, dX,
-                                        dXt, part_g, part_b, part_c, &nb, s);
+  hipError_t r = layernorm_bwd_partials(dtype, dY, DT_F32, ldd, X, ldx, mean, rstd, g, rows, n,
+                                        dres, dX, dXt, part_g, part_b, part_c, &nb, s);
   if (r != hipSuccess) return r;
   return layernorm_bwd_reduce(part_g, grad_g, part_b, grad_b, part_c, grad_c, nb, n, s);
 }

@@ -503,7 +503,10 @@ mpipe_status backward(Ctx& x, const void* patches, const char* tape, const void*
   char* dht = x.ws + P.ws_dht;
   float* dhm = reinterpret_cast<float*>(x.ws + P.ws_dhm);
   char* dhmt = x.ws + P.ws_dhmt;
-  float* dx32 = reinterpret_cast<float*>(x.ws + P.ws_dx32);
+  // input gradient of each LayerNorm: bf16 for a bf16 encoder (the GEMM stores it with the
+  // plain epilogue), fp32 for the fp32 one
+  void* dxln = x.ws + P.ws_dxln;
+  const int epi_dxln = x.dt == DT_BF16 ? EPI_STORE : EPI_F32;
   char* du = x.ws + P.ws_du;
   char* dO = x.ws + P.ws_do;
   float* delta = reinterpret_cast<float*>(x.ws + P.ws_delta);
@@ -528,7 +531,7 @@ mpipe_status backward(Ctx& x, const void* patches, const char* tape, const void*
   // stream (x.s2), which forks off after each gradient buffer is produced; the caller's
   // stream waits for a buffer's side readers only before it overwrites that buffer.
   SideSync ss{x, x.s2 != x.s};
-  // LayerNorm backward of dx32 on the caller's stream; its partial sums are reduced into
+  // LayerNorm backward of dxln on the caller's stream; its partial sums are reduced into
   // the gain, shift and bias gradients on the side stream (nothing in the backward reads
   // them).  The partial buffers alternate, so a call waits only for the reduction of the
   // call two back before overwriting its buffer.
@@ -543,7 +546,7 @@ mpipe_status backward(Ctx& x, const void* patches, const char* tape, const void*
     MP_CHECK(ss.acquire(FREE_LNP0 + k));
     int64_t nb = 0;
     MP_CHECK(run(x.e, x.s, "layernorm_bwd", 0, [&] {
-      return layernorm_bwd_partials(x.dt, dx32, h, X_, h, reinterpret_cast<const float*>(mean_),
+      return layernorm_bwd_partials(x.dt, dxln, x.dt, h, X_, h, reinterpret_cast<const float*>(mean_),
                                     reinterpret_cast<const float*>(rstd_), g_, N, (int)h, dres_,
                                     dX_, dXt_, pg, pb, pc, &nb, x.s);
     }));
@@ -576,8 +579,8 @@ mpipe_status backward(Ctx& x, const void* patches, const char* tape, const void*
                : colsum(x, x.dt, du, 4 * h, Tm, (int)(4 * h), x.grad(dw, merger_param(c, M_FC1B))));
   MP_CHECK(ss.release(FREE_DU));
   {
-    GemmArgs a = ga(du, 4 * h, x.W(merger_param(c, M_FC1W)), 4 * h, Tm, 4 * h, 4 * h, dx32, 4 * h);
-    MP_RET(gemm_call(x, GEMM_NN, EPI_F32, a));
+    GemmArgs a = ga(du, 4 * h, x.W(merger_param(c, M_FC1W)), 4 * h, Tm, 4 * h, 4 * h, dxln, 4 * h);
+    MP_RET(gemm_call(x, GEMM_NN, epi_dxln, a));
   }
   MP_RET(ln_bwd(reinterpret_cast<const float*>(base + MS.hfin), base + MS.meanz, base + MS.rstdz,
                 x.W(merger_param(c, M_LNG)), nullptr, merger_only ? nullptr : dh,
@@ -609,8 +612,8 @@ mpipe_status backward(Ctx& x, const void* patches, const char* tape, const void*
                  : colsum(x, x.dt, du, m, N, (int)m, x.grad(dw, blk_param(c, l, B_FC1B))));
     MP_CHECK(ss.release(FREE_DU));
     {
-      GemmArgs a = ga(du, m, x.W(blk_param(c, l, B_FC1W)), h, N, h, m, dx32, h);
-      MP_RET(gemm_call(x, GEMM_NN, EPI_F32, a));
+      GemmArgs a = ga(du, m, x.W(blk_param(c, l, B_FC1W)), h, N, h, m, dxln, h);
+      MP_RET(gemm_call(x, GEMM_NN, epi_dxln, a));
     }
     MP_CHECK(ss.acquire(FREE_DHM));
     MP_RET(ln_bwd(hmid, base + S.mean2, base + S.rstd2, x.W(blk_param(c, l, B_LN2G)), dh, dhm,
@@ -653,8 +656,8 @@ mpipe_status backward(Ctx& x, const void* patches, const char* tape, const void*
     MP_RET(colsum(x, x.dt, dqkv, 3 * h, N, (int)(3 * h), x.grad(dw, blk_param(c, l, B_QKVB))));
     MP_CHECK(ss.release(FREE_DQKV));
     {
-      GemmArgs a = ga(dqkv, 3 * h, x.W(blk_param(c, l, B_QKVW)), h, N, h, 3 * h, dx32, h);
-      MP_RET(gemm_call(x, GEMM_NN, EPI_F32, a));
+      GemmArgs a = ga(dqkv, 3 * h, x.W(blk_param(c, l, B_QKVW)), h, N, h, 3 * h, dxln, h);
+      MP_RET(gemm_call(x, GEMM_NN, epi_dxln, a));
     }
     MP_CHECK(ss.acquire(FREE_DH));
     MP_RET(ln_bwd(hin, base + S.mean1, base + S.rstd1, x.W(blk_param(c, l, B_LN1G)), dhm, dh, dht,

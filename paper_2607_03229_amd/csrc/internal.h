@@ -105,11 +105,12 @@ hipError_t layernorm_bwd(int dtype, const float* dY, int64_t ldd, const float* X
 // The two halves of layernorm_bwd, for callers that reduce on another stream: the kernel
 // (part_c written when both it and dX are non-null; *blocks = the partial rows written)
 // and the deterministic reduction of those partial rows into the (nullable) targets.
-hipError_t layernorm_bwd_partials(int dtype, const float* dY, int64_t ldd, const float* X,
-                                  int64_t ldx, const float* mean, const float* rstd, const void* g,
-                                  int64_t rows, int n, const float* dres, float* dX, void* dXt,
-                                  float* part_g, float* part_b, float* part_c, int64_t* blocks,
-                                  hipStream_t s);
+// dY is fp32, or bf16 (dy_dtype DT_BF16, with a bf16 layer only)
+hipError_t layernorm_bwd_partials(int dtype, const void* dY, int dy_dtype, int64_t ldd,
+                                  const float* X, int64_t ldx, const float* mean, const float* rstd,
+                                  const void* g, int64_t rows, int n, const float* dres, float* dX,
+                                  void* dXt, float* part_g, float* part_b, float* part_c,
+                                  int64_t* blocks, hipStream_t s);
 hipError_t layernorm_bwd_reduce(float* part_g, float* grad_g, float* part_b, float* grad_b,
                                 float* part_c, float* grad_c, int64_t blocks, int n,
                                 hipStream_t s);

@@ -313,7 +313,7 @@ int build_plan(const Cfg& c, const int32_t* cu, int n_seg, const int32_t* thw, i
     p.ws_dht = ws.take((size_t)N * h * E);
     p.ws_dhm = ws.take((size_t)N * h * 4);
     p.ws_dhmt = ws.take((size_t)N * h * E);
-    p.ws_dx32 = ws.take((size_t)N * h * 4);
+    p.ws_dxln = ws.take((size_t)N * h * E);   // LayerNorm input gradient, activation dtype
     p.ws_du = ws.take((size_t)N * std::max<int64_t>(m, h) * E);
     p.ws_do = ws.take((size_t)N * h * E);
     p.ws_delta = ws.take((size_t)N * nh * 4);
