@@ -53,11 +53,11 @@ struct mpipe_encoder {
   std::vector<Rec> recs;
   std::vector<hipEvent_t> pool;
   // Weight-gradient side stream of the backward (default priority) and its sync events:
-  // 0 fork (caller -> side), 1..6 buffer-free signals (side -> caller), 7 join.
+  // 0 fork (caller -> side), 1..7 buffer-free signals (side -> caller), 8 join.
   bool side_on = true;
   hipStream_t side = nullptr;
   int side_dev = -1;
-  hipEvent_t sync[8] = {};
+  hipEvent_t sync[9] = {};
 
   hipEvent_t event() {
     if (!pool.empty()) {
@@ -210,7 +210,7 @@ mpipe_status colsum(Ctx& x, int dtype_in, const void* X, int64_t ld, int64_t row
 struct SideSync {
   Ctx& x;
   bool on;
-  bool recorded[8] = {};
+  bool recorded[9] = {};
   hipError_t fork() {
     if (!on) return hipSuccess;
     hipError_t r = hipEventRecord(x.e->sync[0], x.s);
@@ -227,11 +227,12 @@ struct SideSync {
   }
   hipError_t join() {
     if (!on) return hipSuccess;
-    hipError_t r = hipEventRecord(x.e->sync[7], x.s2);
-    return r != hipSuccess ? r : hipStreamWaitEvent(x.s, x.e->sync[7], 0);
+    hipError_t r = hipEventRecord(x.e->sync[8], x.s2);
+    return r != hipSuccess ? r : hipStreamWaitEvent(x.s, x.e->sync[8], 0);
   }
 };
-enum { FREE_DU = 1, FREE_DH = 2, FREE_DHM = 3, FREE_DQKV = 4, FREE_LNP0 = 5, FREE_LNP1 = 6 };
+enum { FREE_DU = 1, FREE_DH = 2, FREE_DHM = 3, FREE_DQKV = 4, FREE_LNP0 = 5, FREE_LNP1 = 6,
+       FREE_DQKV1 = 7 };
 
 // Creates the side stream and its events on the current device (once per device).
 hipError_t ensure_side(mpipe_encoder* e) {
@@ -510,7 +511,7 @@ mpipe_status backward(Ctx& x, const void* patches, const char* tape, const void*
   char* du = x.ws + P.ws_du;
   char* dO = x.ws + P.ws_do;
   float* delta = reinterpret_cast<float*>(x.ws + P.ws_delta);
-  char* dqkv = x.ws + P.ws_dqkv;
+  char* const dqkvb[2] = {x.ws + P.ws_dqkv, x.ws + P.ws_dqkv2};
   // LayerNorm-backward partials: two buffers of three sets (gain, shift, and the column sums
   // of the residual-stream gradient it writes, which is the next bias gradient), each
   // kPartialRowsMax x h floats
@@ -590,6 +591,15 @@ mpipe_status backward(Ctx& x, const void* patches, const char* tape, const void*
                 merger_only ? nullptr : x.grad(dw, blk_param(c, c.layers - 1, B_FC2B))));
   if (merger_only) return MPIPE_OK;
 
+  int pending_qkv = -1;   // block whose qkv weight gradient is still to be launched
+  auto qkv_dw = [&](int lq) -> mpipe_status {
+    char* const dq_ = dqkvb[lq & 1];
+    MP_RET(dw_gemm(x, dq_, 3 * h, base + P.tape_act[lq].a, h, 3 * h, h, N,
+                   x.grad(dw, blk_param(c, lq, B_QKVW)), h));
+    MP_RET(colsum(x, x.dt, dq_, 3 * h, N, (int)(3 * h), x.grad(dw, blk_param(c, lq, B_QKVB))));
+    MP_CHECK(ss.release((lq & 1) ? FREE_DQKV1 : FREE_DQKV));
+    return MPIPE_OK;
+  };
   for (int l = c.layers - 1; l >= 0; --l) {
     const ActSet& S = P.tape_act[l];
     const float* hin = reinterpret_cast<const float*>(base + S.hin);
@@ -617,6 +627,8 @@ mpipe_status backward(Ctx& x, const void* patches, const char* tape, const void*
     // (same-call A/B of this order against forking each GEMM as soon as its operand
     // exists: 281.2 -> 277.1 ms per step)
     MP_CHECK(ss.fork());   // dh, dht, du and its band sums
+    if (pending_qkv >= 0) MP_RET(qkv_dw(pending_qkv));
+    pending_qkv = -1;
     MP_RET(dw_gemm(x, dht, h, base + S.g, m, h, m, N, x.grad(dw, blk_param(c, l, B_FC2W)), m));
     MP_CHECK(ss.release(FREE_DH));
     MP_RET(dw_gemm(x, du, m, base + S.b, h, m, h, N, x.grad(dw, blk_param(c, l, B_FC1W)), h));
@@ -631,7 +643,8 @@ mpipe_status backward(Ctx& x, const void* patches, const char* tape, const void*
       GemmArgs a = ga(dhmt, h, x.W(blk_param(c, l, B_PROJW)), h, N, h, h, dO, h);
       MP_RET(gemm_call(x, GEMM_NN, EPI_STORE, a));
     }
-    MP_CHECK(ss.acquire(FREE_DQKV));
+    char* const dqkv = dqkvb[l & 1];
+    MP_CHECK(ss.acquire((l & 1) ? FREE_DQKV1 : FREE_DQKV));
     {
       const char* qkv = base + S.qkv;
       AttnArgs qa = attn_args(x, qkv, false), ka = attn_args(x, qkv, true);
@@ -663,14 +676,13 @@ mpipe_status backward(Ctx& x, const void* patches, const char* tape, const void*
     MP_RET(ln_bwd(hin, base + S.mean1, base + S.rstd1, x.W(blk_param(c, l, B_LN1G)), dhm, dh, dht,
                   x.grad(dw, blk_param(c, l, B_LN1G)), x.grad(dw, blk_param(c, l, B_LN1B)),
                   x.grad(dw, l > 0 ? blk_param(c, l - 1, B_FC2B) : P_PE_B)));
-    // qkv's weight gradient likewise waits for the LayerNorm backward
-    MP_CHECK(ss.fork());   // dqkv
-    MP_RET(dw_gemm(x, dqkv, 3 * h, base + S.a, h, 3 * h, h, N, x.grad(dw, blk_param(c, l, B_QKVW)), h));
-    MP_RET(colsum(x, x.dt, dqkv, 3 * h, N, (int)(3 * h), x.grad(dw, blk_param(c, l, B_QKVB))));
-    MP_CHECK(ss.release(FREE_DQKV));
+    // qkv's weight gradient runs beside the next block's attention (its dqkv buffer
+    // alternates with the next block's)
+    pending_qkv = l;
   }
   // patch embedding (the trainable source: nothing goes upstream unless asked)
   MP_CHECK(ss.fork());   // dh, dht
+  if (pending_qkv >= 0) MP_RET(qkv_dw(pending_qkv));
   MP_RET(dw_gemm(x, dht, h, Xp, ldx, h, c.kpe, N, x.grad(dw, P_PE_W), c.kpe));
   if (d_patches) {
     GemmArgs a = ga(dht, h, Wpe, ldx, N, c.kpe, h, d_patches, c.kpe);

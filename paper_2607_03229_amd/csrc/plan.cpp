@@ -318,6 +318,7 @@ int build_plan(const Cfg& c, const int32_t* cu, int n_seg, const int32_t* thw, i
     p.ws_do = ws.take((size_t)N * h * E);
     p.ws_delta = ws.take((size_t)N * nh * 4);
     p.ws_dqkv = ws.take((size_t)N * 3 * h * E);
+    p.ws_dqkv2 = mode == MODE_TRAINED ? ws.take((size_t)N * 3 * h * E) : 0;
     const int64_t widest = std::max({3 * h, m, 4 * h, H, (int64_t)c.kpe});
     // LayerNorm-backward partials (two buffers of three sets: gain, shift and the column
     // sums of the residual-stream gradient, h columns each) and bias column-sum partials

@@ -101,7 +101,7 @@ struct Plan {
   ActSet ws_act{};                 // frozen forward activations
   MergerSet ws_mrg{};
   size_t ws_dh = 0, ws_dht = 0, ws_dhm = 0, ws_dhmt = 0, ws_dxln = 0, ws_du = 0, ws_do = 0,
-         ws_delta = 0, ws_dqkv = 0, ws_part = 0, ws_cpart = 0, ws_dwpart = 0,
+         ws_delta = 0, ws_dqkv = 0, ws_dqkv2 = 0, ws_part = 0, ws_cpart = 0, ws_dwpart = 0,
          ws_gpart = 0;
   size_t ws_bytes = 0;
   std::vector<Region> ws_regions;   // every range a kernel may write, in layout order
