@@ -479,6 +479,8 @@ def main():
                          "(about 15 minutes on 16 cores) instead of at 0 and 1 blocks")
     ap.add_argument("--cpu-baseline-only", action="store_true",
                     help="only time the CPU oracle sample and print its JSON object")
+    ap.add_argument("--no-alone-pass", action="store_true",
+                    help="skip the per-kernel pass with the side stream off (figures *_alone)")
     ap.add_argument("--no-profile", action="store_true",
                     help="skip the per-kernel event timing (roofline figures)")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -573,7 +575,7 @@ def main():
     log(f"timed {args.steps} steps: {elapsed * 1e3 / args.steps:.1f} ms/step")
     # Per-kernel figures from a separate pass: every launch bracketed by a HIP event pair
     # on the stream it is launched on (the caller's, or the backward's side stream)
-    kern = {}
+    kern, kern_alone = {}, {}
     prof_steps = min(args.steps, 5)
     if profile:
         enc.profile(True)
@@ -586,6 +588,17 @@ def main():
             f"{(time.perf_counter() - t1) * 1e3 / prof_steps:.1f} ms/step with events")
         kern = enc.profile_read(stream)
         enc.profile(False)
+        if int(trainable) == 1 and not args.no_alone_pass:
+            # the same pass with the weight-gradient work on the caller's stream: each
+            # kernel then runs alone, so its event time is its own, without CU sharing
+            enc.set_side_stream(False)
+            enc.profile(True)
+            for _ in range(prof_steps):
+                step()
+            torch.cuda.synchronize()
+            kern_alone = enc.profile_read(stream)
+            enc.profile(False)
+            enc.set_side_stream(True)
 
     # scatter bandwidth, timed on its own
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -618,17 +631,26 @@ def main():
                             "ms_avg": round(ms / max(n, 1), 4),
                             "tflops": round(fl / (ms * 1e-3) / 1e12, 1) if ms > 0 and fl > 0 else None,
                             "stream": "side" if side else "caller"}
+            if cls in kern_alone:   # the same class with every kernel alone on one stream
+                na, msa, _ = kern_alone[cls]
+                kernels[cls]["ms_avg_alone"] = round(msa / max(na, 1), 4)
         def roof(cls):
             key = cls if cls in kern else cls + "@side"
             n, ms, fl = kern[key]
             ach = fl / n / (ms / n * 1e-3) / 1e12
-            return {"kernel": cls, "bound": "mfma", "achieved": round(ach, 1), "peak": peak,
-                    "unit": "TFLOP/s", "frac": round(ach / peak, 4),
-                    "traffic": stored_traffic(cls),
-                    "traffic_counter": TRAFFIC_NOTE,
-                    "launches": n, "avg_ms": round(ms / n, 4),
-                    "flop_per_launch": fl / n, "stream": kernels[cls]["stream"],
-                    "timed_over_steps": prof_steps}
+            r = {"kernel": cls, "bound": "mfma", "achieved": round(ach, 1), "peak": peak,
+                 "unit": "TFLOP/s", "frac": round(ach / peak, 4),
+                 "traffic": stored_traffic(cls),
+                 "traffic_counter": TRAFFIC_NOTE,
+                 "launches": n, "avg_ms": round(ms / n, 4),
+                 "flop_per_launch": fl / n, "stream": kernels[cls]["stream"],
+                 "timed_over_steps": prof_steps}
+            if cls in kern_alone:   # the pass with every kernel alone on one stream
+                na, msa, fla = kern_alone[cls]
+                acha = fla / na / (msa / na * 1e-3) / 1e12
+                r.update({"achieved_alone": round(acha, 1), "frac_alone": round(acha / peak, 4),
+                          "avg_ms_alone": round(msa / na, 4)})
+            return r
 
         # the roofline kernel: the largest MFMA class on the caller's (critical) stream;
         # beside it, the largest class of the whole trace when that is another one
