@@ -263,6 +263,69 @@ def summarize_sq(db1: str, db2: str, cmds: str, out: str):
     print("\n".join(L))
 
 
+MEM_PASS1 = ("SQ_LDS_IDX_ACTIVE SQ_LDS_BANK_CONFLICT SQ_VALU_MFMA_BUSY_CYCLES SQ_BUSY_CU_CYCLES "
+             "GRBM_GUI_ACTIVE")
+MEM_PASS2 = ("TA_TA_BUSY TD_TD_BUSY TD_TC_STALL TCP_PENDING_STALL_CYCLES TCP_TCC_READ_REQ_LATENCY "
+             "TCP_TCC_READ_REQ GRBM_GUI_ACTIVE")
+
+
+def summarize_memory(db1: str, db2: str, cmds: str, out: str):
+    """Two rocprofv3 --pmc passes of LDS and vector-memory-path counters over one step ->
+    per kernel class: how busy the LDS, the texture address (TA) and data (TD) units are,
+    how often the L1 waits on the L2, and the mean L1->L2 read latency."""
+    per = {}
+    for db, names in ((db1, MEM_PASS1.split()), (db2, MEM_PASS2.split())):
+        for counter in names:
+            for (d, n), v in _pmc_by_dispatch(db, counter).items():
+                cls = kernel_class(n) or ("layernorm_bwd" if "ln_bwd_kernel" in n else
+                                          "layernorm" if "ln_fwd_kernel" in n else None)
+                if cls is None:
+                    continue
+                per.setdefault(cls, {}).setdefault(counter, {})[(db, d)] = v
+    L = ["# LDS and vector-memory-path counters per kernel class: encoder training step "
+         "(c4_qwen2vl_trained, seed 0)", "",
+         "Two `rocprofv3 --pmc` passes of one bench step (kernels are serialized while counters",
+         "are taken: each kernel's own figures).  Commands (on the MI355X box):", "", "```", cmds,
+         "```", "",
+         f"Per dispatch: `cyc` = GRBM_GUI_ACTIVE / {N_XCD}; LDS active = SQ_LDS_IDX_ACTIVE / "
+         f"(cyc x {N_CU} CUs); LDS bank-conflict = SQ_LDS_BANK_CONFLICT / (cyc x {N_CU}); MFMA busy "
+         f"= SQ_VALU_MFMA_BUSY_CYCLES / (cyc x {N_SIMD} SIMDs); CU busy = SQ_BUSY_CU_CYCLES / "
+         f"(cyc x {N_CU}); TA, TD busy = TA_TA_BUSY, TD_TD_BUSY / (cyc x {N_CU}); TD waits on L2 "
+         f"= TD_TC_STALL / (cyc x {N_CU}); L1 pending on L2 = TCP_PENDING_STALL_CYCLES / (cyc x "
+         f"{N_CU}); L2 read latency = TCP_TCC_READ_REQ_LATENCY / TCP_TCC_READ_REQ (cycles).", "",
+         "| class | dispatches | LDS active | LDS bank-conflict | MFMA busy | CU busy | TA busy "
+         "| TD busy | TD waits on L2 | L1 pending on L2 | L2 read latency |",
+         "|---|---:|---:|---:|---:|---:|---:|---:|---:|---:|---:|"]
+
+    def avg(e, c):
+        v = list(e.get(c, {}).values())
+        return sum(v) / len(v) if v else float("nan")
+
+    rows = []
+    for cls, e in per.items():
+        c1 = [v for (db, _), v in e.get("GRBM_GUI_ACTIVE", {}).items() if db == db1]
+        c2 = [v for (db, _), v in e.get("GRBM_GUI_ACTIVE", {}).items() if db == db2]
+        if not c1 or not c2:
+            continue
+        cyc1, cyc2 = sum(c1) / len(c1) / N_XCD, sum(c2) / len(c2) / N_XCD
+        nd = len(c1)
+        req = avg(e, "TCP_TCC_READ_REQ")
+        rows.append((avg(e, "SQ_VALU_MFMA_BUSY_CYCLES") * nd + cyc1 * nd * 1e-3, cls, [
+            nd, avg(e, "SQ_LDS_IDX_ACTIVE") / (cyc1 * N_CU),
+            avg(e, "SQ_LDS_BANK_CONFLICT") / (cyc1 * N_CU),
+            avg(e, "SQ_VALU_MFMA_BUSY_CYCLES") / (cyc1 * N_SIMD),
+            avg(e, "SQ_BUSY_CU_CYCLES") / (cyc1 * N_CU),
+            avg(e, "TA_TA_BUSY") / (cyc2 * N_CU), avg(e, "TD_TD_BUSY") / (cyc2 * N_CU),
+            avg(e, "TD_TC_STALL") / (cyc2 * N_CU),
+            avg(e, "TCP_PENDING_STALL_CYCLES") / (cyc2 * N_CU),
+            avg(e, "TCP_TCC_READ_REQ_LATENCY") / req if req else float("nan")]))
+    for _, cls, v in sorted(rows, reverse=True):
+        L.append(f"| `{cls}` | {v[0]} | {v[1]:.3f} | {v[2]:.3f} | {v[3]:.3f} | {v[4]:.3f} | "
+                 f"{v[5]:.3f} | {v[6]:.3f} | {v[7]:.3f} | {v[8]:.3f} | {v[9]:.0f} |")
+    open(out, "w").write("\n".join(L) + "\n")
+    print("\n".join(L))
+
+
 def stored_traffic(cls: str):
     try:
         with open(TRAFFIC_FILE) as fh:
@@ -490,6 +553,8 @@ def main():
     ap.add_argument("--pmc-commands", default="", help="commands recorded with --summarize-pmc")
     ap.add_argument("--summarize-trace", nargs=3, metavar=("DB", "BENCH_JSON", "OUT_MD"),
                     help="rocprofv3 kernel-trace database -> a markdown summary")
+    ap.add_argument("--summarize-memory", nargs=3, metavar=("PASS1_DB", "PASS2_DB", "OUT_MD"),
+                    help="LDS / TA / TD / TCP counter passes -> profiles markdown")
     ap.add_argument("--summarize-sq", nargs=3, metavar=("PASS1_DB", "PASS2_DB", "OUT_MD"),
                     help="two rocprofv3 SQ-counter databases -> a markdown summary")
     ap.add_argument("--gemm-vs-library", action="store_true",
@@ -503,6 +568,9 @@ def main():
         return
     if args.summarize_sq:
         summarize_sq(*args.summarize_sq[:2], args.pmc_commands, args.summarize_sq[2])
+        return
+    if args.summarize_memory:
+        summarize_memory(*args.summarize_memory[:2], args.pmc_commands, args.summarize_memory[2])
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one MI355X only: the encoder step runs on one GPU "
@@ -600,7 +668,11 @@ def main():
             enc.profile(False)
             enc.set_side_stream(True)
 
-    # scatter bandwidth, timed on its own
+    # scatter bandwidth, timed on its own, after a few untimed calls (the step leaves the
+    # caches full of its dirty lines, whose write-back would be charged to the first ones)
+    for _ in range(5):
+        mp.merge_scatter(merged, idx, emb)
+    torch.cuda.synchronize()
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     reps = 20
     ev0.record(stream)
