@@ -326,6 +326,42 @@ def summarize_memory(db1: str, db2: str, cmds: str, out: str):
     print("\n".join(L))
 
 
+def summarize_workloads(out: str, files, cmds: str):
+    """Bench lines of several workloads (one JSON file each) -> one markdown table."""
+    import subprocess
+    try:
+        tree = subprocess.run(["git", "-C", ROOT, "rev-parse", "--short", "HEAD"], check=True,
+                              capture_output=True, text=True).stdout.strip()
+    except (OSError, subprocess.CalledProcessError):
+        tree = "unknown"
+    mode_name = {"trained": "trained", "merger": "merger-trained", "frozen": "frozen"}
+    rows = []
+    for f in files:
+        with open(f) as fh:
+            d = json.load(fh)
+        c = d["config"]
+        rows.append("| `%s` | %s | %s | %d | %s | %.3f | %.3f | %.3f | %s | %.3f | %.2f | %.2f | %s |" % (
+            c["workload"], mode_name.get(c["mode"], c["mode"]), d["dtype"], c["n_items"],
+            f"{c['n_patches']:,}", d["ms_per_step"], d["ms_per_step_median"], d["ms_per_step_min"],
+            f"{d['value']:,.0f}", d["model_tflop_per_step"], d["mfma_pct_of_peak"],
+            d["hw_mfma_pct_of_peak"], f"{d['scatter_GBps']:,.0f}"))
+    lines = [
+        "# Bench lines of every workload (seed 0): encoder step on one MI355X", "",
+        f"Commands (on the MI355X box), one run per workload, tree at commit `{tree}`, then the "
+        "table from the JSON lines:", "", "```", cmds.strip(), "```", "",
+        "Trained = forward with tape + merge scatter + merge gather + backward; merger-trained = "
+        "the same with only the merger trainable (its backward only); frozen = forward + scatter.",
+        "ms columns: mean over the timed steps (host clock), and the median / minimum of per-step "
+        "HIP events.  MFMA % = model FLOPs / time / 2516.6 TFLOP/s; hw % counts the attention "
+        "recompute and head-dim padding.", "",
+        "| workload | mode | dtype | items | patches | ms/step | median | min | patch-tokens/s | "
+        "model TFLOP | MFMA % | hw MFMA % | scatter GB/s |",
+        "|---|---|---|---:|---:|---:|---:|---:|---:|---:|---:|---:|---:|"] + rows
+    with open(out, "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+    print(f"wrote {out}")
+
+
 def stored_traffic(cls: str):
     try:
         with open(TRAFFIC_FILE) as fh:
@@ -557,6 +593,8 @@ def main():
                     help="LDS / TA / TD / TCP counter passes -> profiles markdown")
     ap.add_argument("--summarize-sq", nargs=3, metavar=("PASS1_DB", "PASS2_DB", "OUT_MD"),
                     help="two rocprofv3 SQ-counter databases -> a markdown summary")
+    ap.add_argument("--summarize-workloads", nargs="+", metavar=("OUT_MD", "JSON"),
+                    help="bench JSON lines of several workloads -> a markdown table")
     ap.add_argument("--gemm-vs-library", action="store_true",
                     help="only time the step's GEMM shapes alone, against torch.mm (hipBLASLt)")
     args = ap.parse_args()
@@ -568,6 +606,10 @@ def main():
         return
     if args.summarize_sq:
         summarize_sq(*args.summarize_sq[:2], args.pmc_commands, args.summarize_sq[2])
+        return
+    if args.summarize_workloads:
+        summarize_workloads(args.summarize_workloads[0], args.summarize_workloads[1:],
+                            args.pmc_commands)
         return
     if args.summarize_memory:
         summarize_memory(*args.summarize_memory[:2], args.pmc_commands, args.summarize_memory[2])
