@@ -388,7 +388,7 @@ def copy_calibration():
     print(json.dumps({"copy_read_bytes": CAL_READ, "copy_write_bytes": CAL_WRITE}), flush=True)
 
 
-def gemm_vs_library(workload: str, seed: int):
+def gemm_vs_library(workload: str, seed: int, out_md: str = ""):
     """The encoder step's GEMM shapes, each run alone: the library's kernels against
     torch.mm (hipBLASLt on ROCm) on the same bf16 operands, HIP-event timed.  The
     weight gradients run the step's four-way K split (fp32 partials, the reduction
@@ -416,12 +416,18 @@ def gemm_vs_library(workload: str, seed: int):
     def rnd(*shape):
         return (torch.randn(*shape, device=dev, generator=g) * 0.5).to(torch.bfloat16)
 
-    def line(name, M, N, K, ours, lib):
+    def line(name, M, N, K, ours, lib, lib_nt=None):
         fl = 2.0 * M * N * K
-        print(json.dumps({"gemm": name, "M": M, "N": N, "K": K,
-                          "ours_ms": round(ours, 3), "ours_tflops": round(fl / ours / 1e9, 1),
-                          "hipblaslt_ms": round(lib, 3), "hipblaslt_tflops": round(fl / lib / 1e9, 1)}),
-              flush=True)
+        rec = {"gemm": name, "M": M, "N": N, "K": K,
+               "ours_ms": round(ours, 3), "ours_tflops": round(fl / ours / 1e9, 1),
+               "hipblaslt_ms": round(lib, 3), "hipblaslt_tflops": round(fl / lib / 1e9, 1)}
+        if lib_nt is not None:   # the same product with B given as [N][K] (hipBLASLt NT)
+            rec.update({"hipblaslt_nt_ms": round(lib_nt, 3),
+                        "hipblaslt_nt_tflops": round(fl / lib_nt / 1e9, 1)})
+        print(json.dumps(rec), flush=True)
+        recs.append(rec)
+
+    recs = []
 
     # forward and input-gradient products: C[M][N] = A[M][K] B[K][N], bf16 out
     for name, M, N, K in [("qkv_fwd", T, 3 * h, h), ("proj_fwd", T, h, h), ("fc1_fwd", T, f, h),
@@ -431,8 +437,10 @@ def gemm_vs_library(workload: str, seed: int):
         bias = torch.zeros(N, dtype=torch.bfloat16, device=dev)
         ours = tm(lambda: mp.op_gemm(mp.BF16, 1, 0, M, N, K, A, K, B, N, C, N, bias=bias))
         lib = tm(lambda: torch.mm(A, B, out=C))
-        line(name, M, N, K, ours, lib)
-        del A, B, C
+        Bt = B.t().contiguous()
+        lib_nt = tm(lambda: torch.mm(A, Bt.t(), out=C))
+        line(name, M, N, K, ours, lib, lib_nt)
+        del A, B, Bt, C
     # weight gradients: C[M][N] = sum over tokens of A[k][M] B[k][N]
     for name, M, N in [("qkv_wgrad", h, 3 * h), ("proj_wgrad", h, h), ("fc1_wgrad", h, f),
                        ("fc2_wgrad", f, h)]:
@@ -446,6 +454,38 @@ def gemm_vs_library(workload: str, seed: int):
         lib = tm(lambda: torch.mm(At, B, out=Cb))
         line(name, M, N, T, ours, lib)
         del A, B, C, Cb
+    if out_md:
+        fwd = [r for r in recs if "hipblaslt_nt_ms" in r]
+        wg = [r for r in recs if "hipblaslt_nt_ms" not in r]
+        rows = []
+        for r in recs:
+            nt = (f"{r['hipblaslt_nt_ms']:.3f} | {r['hipblaslt_nt_tflops']:.1f}"
+                  if "hipblaslt_nt_ms" in r else "— | —")
+            rows.append(f"| {r['gemm']} | {r['M']:,} | {r['N']:,} | {r['K']:,} | {r['ours_ms']:.3f} | "
+                        f"{r['ours_tflops']:.1f} | {r['hipblaslt_ms']:.3f} | {r['hipblaslt_tflops']:.1f} | {nt} |")
+        lines = [
+            f"# Library GEMM kernels vs hipBLASLt on the encoder step's shapes ({workload}, seed {seed})",
+            "", "Command (on the MI355X box; the table it writes is copied to `profiles/`):", "",
+            "```",
+            f"python3 bench.py --gemm-vs-library --workload {workload} --gemm-vs-library-out {out_md}",
+            "```", "",
+            "Each product runs alone on the default stream, HIP-event timed over 10 calls after one "
+            "warm call, on random bf16 operands (scale 0.5). The library runs the NN kernel with a "
+            "bias epilogue, and the TN weight-gradient kernel with a four-way K split into fp32 "
+            "partials (the reduction not timed). hipBLASLt is `torch.mm` with bf16 output: NN with "
+            "the weight as [K][N], and NT with the same weight stored [N][K]. In the step the weight "
+            "gradients run on a side stream beside the input-gradient products, so in-step durations "
+            "(the kernel trace) are longer than these.", "",
+            "| product | M | N | K | library ms | library TFLOP/s | hipBLASLt NN ms | TFLOP/s | "
+            "hipBLASLt NT ms | TFLOP/s |",
+            "|---|---:|---:|---:|---:|---:|---:|---:|---:|---:|"] + rows + [
+            "", "Sums: forward and input-gradient shapes %.3f ms (library) vs %.3f ms (hipBLASLt NN), "
+            "%.3f ms (hipBLASLt NT); weight gradients %.3f vs %.3f ms." % (
+                sum(r["ours_ms"] for r in fwd), sum(r["hipblaslt_ms"] for r in fwd),
+                sum(r["hipblaslt_nt_ms"] for r in fwd), sum(r["ours_ms"] for r in wg),
+                sum(r["hipblaslt_ms"] for r in wg))]
+        with open(out_md, "w") as fh:
+            fh.write("\n".join(lines) + "\n")
 
 
 def _prefix_sample(min_patches: int = 4096):
@@ -597,6 +637,8 @@ def main():
                     help="bench JSON lines of several workloads -> a markdown table")
     ap.add_argument("--gemm-vs-library", action="store_true",
                     help="only time the step's GEMM shapes alone, against torch.mm (hipBLASLt)")
+    ap.add_argument("--gemm-vs-library-out", default="",
+                    help="with --gemm-vs-library: also write the table as markdown here")
     args = ap.parse_args()
     if args.summarize_pmc:
         summarize_pmc(*args.summarize_pmc, args.pmc_commands)
@@ -626,7 +668,7 @@ def main():
         copy_calibration()
         return
     if args.gemm_vs_library:
-        gemm_vs_library(args.workload, args.seed)
+        gemm_vs_library(args.workload, args.seed, args.gemm_vs_library_out)
         return
     import torch
     import paper_2607_03229_amd as mp
