@@ -3,13 +3,14 @@
 // C[M,N] = sum_k A(m,k) B(n,k) with the same operand layouts and epilogues as the
 // general kernel (NT forward, NN input gradient, TN weight gradient).
 //
-// Two kernels, both 256 threads = 4 wave64 in a 2x2 grid of v_mfma_f32_32x32x16_bf16
+// Three kernels, all 256 threads = 4 wave64 in a 2x2 grid of v_mfma_f32_32x32x16_bf16
 // accumulators with the same K order, so a given output element gets bitwise the same
-// value from either:
-//   gemm_big_kernel (NT, TN): block tile 256x256, each wave 128x128 (4x4 accumulators,
+// value from any of them:
+//   gemm_big_kernel (TN): block tile 256x256, each wave 128x128 (4x4 accumulators,
 //     256 AGPRs), a 4-stage ring (128 KB of LDS), one block per CU.  A 128x128 wave tile
 //     keeps the LDS traffic (fragment reads + tile fills) well under what the LDS
 //     delivers at the full MFMA rate.
+//   gemm_nt64_kernel (NT, described with it below): the same block with 64-deep K stages.
 //   gemm_nn_kernel (NN, described with it below): block tile 128x256, two blocks per CU.
 //
 // Operand tiles (rows x 32 k) are filled by 16-byte global->LDS DMA (global_load_lds)
@@ -566,6 +567,263 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_big_kernel(GemmArgs p) {
   }
 }
 
+// ---- NT kernel: 256x256 tiles, 64-deep K stages ---------------------------------------
+//
+// Both operands K-contiguous ([M][K] activations, [N][K] weight).  A K tile is 64 deep, so
+// every operand row of a stage is one whole 128-byte line: DMA instruction q of a 32 KB
+// operand tile fetches rows 8q..8q+7, lane l row 8q + l/8 at physical chunk l%8, which
+// holds logical chunk (l%8) ^ f8(row), f8(row) = (row >> 1) & 7.  A fragment read (32
+// rows at one logical chunk per lane half) then covers 16 distinct 16-byte bank groups in
+// every 16-lane group.  Two stages (2 x 64 KB): the DMA of tile t+2 goes out right after
+// the barrier in the middle of tile t (stage t%2 fully read by then), so at every wait
+// the only DMAs pending are tile t+1's, and one barrier covers 2048 MFMA cycles per wave.
+// Waves 2x2 of 128x128 with 4x4 32x32x16 accumulators in the same K order as the other
+// kernels, so an output element gets bitwise the same value from any of them.
+constexpr int BK64 = 64;
+constexpr int T64_U4 = 256 * BK64 * 2 / 16;   // 16-byte slots of a 256 x 64 operand tile (2048)
+constexpr int I64 = 8;                        // DMA instructions per wave per operand tile
+constexpr int NT64_LDS_U4 = 2 * 2 * T64_U4;   // two stages of A and B: 128 KB
+
+__device__ __forceinline__ int f8(int r) { return (r >> 1) & 7; }
+// source of instruction q of a 256-row, 64-deep K-contiguous tile (rows r0.., k from k0)
+__device__ __forceinline__ const bf16* src_kc64(const bf16* X, int64_t ld, int rows, int r0,
+                                                int k0, int kend, int q) {
+  const int l = threadIdx.x & 63;
+  const int row = 8 * q + (l >> 3);
+  int k = k0 + 8 * ((l & 7) ^ f8(row));
+  k = k < kend ? k : kend - 8;
+  int gr = r0 + row;
+  gr = gr < rows ? gr : rows - 1;
+  return X + (int64_t)gr * ld + k;
+}
+
+template <int EPI>
+__global__ __launch_bounds__(NTHR, 1) void gemm_nt64_kernel(GemmArgs p) {
+  __shared__ uint4 smem[NT64_LDS_U4];
+  static_assert(4 * 16 * SP * 4 <= NT64_LDS_U4 * 16, "epilogue staging must fit in the ring");
+
+  const int ntiles = p.tiles_m * p.tiles_n;
+  const int nb = gridDim.x;
+  const int b = blockIdx.x;
+  const int pid = (b % 8) * (nb / 8) + (b / 8);
+  if (pid >= ntiles) return;
+  const int group = pid / (GROUP_M * p.tiles_n);
+  const int first_m = group * GROUP_M;
+  const int gsize = min(p.tiles_m - first_m, GROUP_M);
+  const int tm = first_m + (pid % gsize);
+  const int tn = (pid % (GROUP_M * p.tiles_n)) / gsize;
+  const int split = blockIdx.y;
+  const int m0 = tm * 256, n0 = tn * 256;
+  const int kbeg = split * p.kps;
+  const int kend = min(p.K, kbeg + p.kps);
+  const int nk = kend > kbeg ? (kend - kbeg + BK64 - 1) / BK64 : 0;
+  const int nfull = kend > kbeg ? (kend - kbeg) / BK64 : 0;   // tiles t < nfull are whole
+  const bf16* A = reinterpret_cast<const bf16*>(p.A);
+  const bf16* B = reinterpret_cast<const bf16*>(p.B);
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), l = threadIdx.x & 63;
+  const int wm = w >> 1, wn = w & 1;
+
+  f32x16 acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+
+  auto stage_a = [&](int s) { return smem + s * T64_U4; };
+  auto stage_b = [&](int s) { return smem + (2 + s) * T64_U4; };
+  const bf16* sA[I64];
+  const bf16* sB[I64];
+#pragma unroll
+  for (int i = 0; i < I64; ++i) {
+    sA[i] = src_kc64(A, p.lda, p.M, m0, kbeg, kend, I64 * w + i);
+    sB[i] = src_kc64(B, p.ldb, p.N, n0, kbeg, kend, I64 * w + i);
+  }
+  // DMA d (0..15: A instructions, then B) of tile t into stage s; a whole tile adds t*64
+  auto dm1 = [&](int s, int t, int d) __attribute__((always_inline)) {
+    if (d < I64) dma16(sA[d] + t * BK64, stage_a(s), I64 * w + d);
+    else dma16(sB[d - I64] + t * BK64, stage_b(s), I64 * w + (d - I64));
+  };
+  auto dma_tile = [&](int s, int t) __attribute__((always_inline)) {
+    if (t < nfull) {
+#pragma unroll
+      for (int d = 0; d < 2 * I64; ++d) dm1(s, t, d);
+    } else {   // ragged last tile: clamped sources
+      const int k0 = kbeg + t * BK64;
+#pragma unroll
+      for (int i = 0; i < I64; ++i) {
+        dma16(src_kc64(A, p.lda, p.M, m0, k0, kend, I64 * w + i), stage_a(s), I64 * w + i);
+        dma16(src_kc64(B, p.ldb, p.N, n0, k0, kend, I64 * w + i), stage_b(s), I64 * w + i);
+      }
+    }
+  };
+
+  // lane offset of a fragment read in a 32-row block: row l%32, logical chunk 2h + l/32 of
+  // K step h at physical chunk (2h + l/32) ^ f8(l%32) -> kc ^ 32h
+  const int kc = 128 * (l & 31) + 16 * ((l >> 5) ^ f8(l & 31));
+  auto frag = [&](const uint4* t, int rb, int h) __attribute__((always_inline)) -> bf16x8 {
+    const char* base = reinterpret_cast<const char*>(t) + rb * 128;
+    const uint4 v = *reinterpret_cast<const uint4*>(base + (kc ^ (32 * h)));
+    return *reinterpret_cast<const bf16x8*>(&v);
+  };
+  // fragment read k (0..7) of K step h, in first-use order A0, B0..B3, A1..A3
+  auto rd1 = [&](int s, int h, int k, bf16x8 (&a)[4], bf16x8 (&bb)[4]) __attribute__((always_inline)) {
+    const bool isb = k >= 1 && k <= 4;
+    const int i = k == 0 ? 0 : isb ? k - 1 : k - 4;
+    if (isb) bb[i] = frag(stage_b(s), wn * 128 + 32 * i, h);
+    else a[i] = frag(stage_a(s), wm * 128 + 32 * i, h);
+  };
+  // ragged tile t: zero this lane's A elements of K step h past kend
+  auto mask_a = [&](int t, int h, bf16x8 (&a)[4]) __attribute__((always_inline)) {
+    if (t >= nfull) {
+      const int kr = kend - (kbeg + t * BK64) - 16 * h - 8 * (l >> 5);
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          if (e >= kr) a[i][e] = (bf16)0.f;
+    }
+  };
+  auto mf1 = [&](int n, const bf16x8 (&a)[4], const bf16x8 (&bb)[4]) __attribute__((always_inline)) {
+    acc[n >> 2][n & 3] =
+        __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[n >> 2], bb[n & 3], acc[n >> 2][n & 3], 0, 0, 0);
+  };
+  bf16x8 fa[2][4], fb[2][4];
+  // tile t in stage S = t % 2; fa[0] / fb[0] hold its K step 0 on entry and tile t+1's on
+  // exit.  FULL: tiles t, t+1 and t+2 whole (no guard splits the fenced schedule).
+  auto body = [&](auto S, auto FULL, int t) __attribute__((always_inline)) {
+    constexpr int s = decltype(S)::value, sn = 1 - s;
+    constexpr bool full = decltype(FULL)::value;
+#pragma unroll
+    for (int h = 0; h < 3; ++h) {
+      bf16x8 (&an)[4] = fa[(h + 1) & 1];
+      bf16x8 (&bn)[4] = fb[(h + 1) & 1];
+#pragma unroll
+      for (int n = 0; n < 16; ++n) {
+        if ((n & 1) == 0) {
+          rd1(s, h + 1, n >> 1, an, bn);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+        mf1(n, fa[h & 1], fb[h & 1]);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      if constexpr (!full) mask_a(t, h + 1, an);
+    }
+    wait_vm<0>();   // tile t+1 landed (the only DMAs pending)
+    lds_barrier();  // every wave is done with stage s
+    if constexpr (full) {
+#pragma unroll
+      for (int n = 0; n < 16; ++n) {
+        dm1(s, t + 2, n);
+        __builtin_amdgcn_sched_barrier(0);
+        mf1(n, fa[1], fb[1]);
+        __builtin_amdgcn_sched_barrier(0);
+        if ((n & 1) == 0) {
+          rd1(sn, 0, n >> 1, fa[0], fb[0]);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      }
+    } else {
+      if (t + 2 < nk) dma_tile(s, t + 2);
+#pragma unroll
+      for (int n = 0; n < 16; ++n) mf1(n, fa[1], fb[1]);
+      if (t + 1 < nk) {
+#pragma unroll
+        for (int k = 0; k < 8; ++k) rd1(sn, 0, k, fa[0], fb[0]);
+        mask_a(t + 1, 0, fa[0]);
+      }
+    }
+  };
+
+  using S0 = std::integral_constant<int, 0>;
+  using S1 = std::integral_constant<int, 1>;
+  using F0 = std::integral_constant<bool, false>;
+  using F1 = std::integral_constant<bool, true>;
+  if (nk > 0) {
+    dma_tile(0, 0);
+    if (nk > 1) {
+      dma_tile(1, 1);
+      wait_vm<2 * I64>();   // tile 0 landed; tile 1 may stay pending
+    } else {
+      wait_vm<0>();
+    }
+    lds_barrier();
+#pragma unroll
+    for (int k = 0; k < 8; ++k) rd1(0, 0, k, fa[0], fb[0]);
+    mask_a(0, 0, fa[0]);
+    int t = 0;
+    // steady state: tiles t, t+1 and the DMA'd tile t+2 all whole
+    for (; t + 4 <= nfull; t += 2) {
+      body(S0{}, F1{}, t);
+      body(S1{}, F1{}, t + 1);
+    }
+    for (; t < nk; t += 2) {   // the last (at most five) tiles, guarded
+      body(S0{}, F0{}, t);
+      if (t + 1 < nk) body(S1{}, F0{}, t + 1);
+    }
+  }
+  wait_vm<0>();
+
+  // epilogue (as in the 256x256 kernel above)
+  __syncthreads();
+  float* stage = reinterpret_cast<float*>(smem) + w * 16 * SP;
+  const int cg = l & 15;
+  const int n = n0 + wn * 128 + 8 * cg;
+  const bool vec = n < p.N;
+  float bias8[8];
+  load_bias8(p, vec && split == 0, n, bias8);
+  auto row_of = [&](int pi, int u) { return m0 + wm * 128 + 16 * pi + (l >> 4) + 4 * u; };
+  constexpr bool kAux = EPI == EPI_GELU_BWD || EPI == EPI_RESID || EPI == EPI_F32 ||
+                        EPI == EPI_STORE_ROPE;
+  AuxV ax[2][4];
+  auto fetch = [&](int pi, AuxV (&dst)[4]) __attribute__((always_inline)) {
+    if constexpr (kAux) {
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int m = row_of(pi, u);
+        if (vec && m < p.M) aux_fetch<EPI>(p, split, m, n, dst[u]);
+      }
+    }
+  };
+  fetch(0, ax[0]);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh) {
+      const int pi = 2 * i + hh;
+      if (pi + 1 < 8) fetch(pi + 1, ax[(pi + 1) & 1]);
+      lds_wave_fence();
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int e = 8 * hh; e < 8 * hh + 8; ++e) {
+          const int rr = 8 * ((e >> 2) & 1) + 4 * (l >> 5) + (e & 3);
+          stage[rr * SP + 32 * j + (l & 31)] = acc[i][j][e];
+        }
+      lds_wave_fence();
+      auto out_row = [&](int u, const AuxV& a) __attribute__((always_inline)) {
+        const int rr = (l >> 4) + 4 * u;
+        const int m = row_of(pi, u);
+        if (m >= p.M || n >= p.N) return;
+        float v[8];
+        const float4 x0 = *reinterpret_cast<const float4*>(stage + rr * SP + 8 * cg);
+        const float4 x1 = *reinterpret_cast<const float4*>(stage + rr * SP + 8 * cg + 4);
+        v[0] = x0.x; v[1] = x0.y; v[2] = x0.z; v[3] = x0.w;
+        v[4] = x1.x; v[5] = x1.y; v[6] = x1.z; v[7] = x1.w;
+        epi8_vec<EPI>(p, split, m, n, v, bias8, a);
+      };
+      if constexpr (kAux) {
+#pragma unroll
+        for (int u = 0; u < 4; ++u) out_row(u, ax[pi & 1][u]);
+      } else {
+#pragma unroll 1
+        for (int u = 0; u < 4; ++u) out_row(u, ax[0][0]);
+      }
+    }
+  }
+}
+
 // ---- NN kernel: 128x256 tiles, paired A stages ---------------------------------------
 //
 // The input-gradient and forward products (A = activations [M][K], B = weight [K][N]).  A
@@ -971,6 +1229,32 @@ hipError_t launch_big(const GemmArgs& a0, hipStream_t s) {
   return hipGetLastError();
 }
 
+template <int EPI>
+hipError_t launch_nt64(const GemmArgs& a0, hipStream_t s) {
+  GemmArgs a = a0;
+  a.tiles_m = (a.M + 255) / 256;
+  a.tiles_n = (a.N + 255) / 256;
+  const int nt = a.tiles_m * a.tiles_n;
+  const int nb = (nt + 7) / 8 * 8;
+  int splits = a.kps > 0 ? (a.K + a.kps - 1) / a.kps : 1;
+  if (a.kps <= 0) a.kps = a.K;
+  if (splits < 1) splits = 1;
+  hipLaunchKernelGGL((gemm_nt64_kernel<EPI>), dim3(nb, splits), dim3(NTHR), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t dispatch_nt64(const GemmArgs& a, int epi, hipStream_t s) {
+  switch (epi) {
+    case EPI_STORE: return launch_nt64<EPI_STORE>(a, s);
+    case EPI_STORE_ROPE: return launch_nt64<EPI_STORE_ROPE>(a, s);
+    case EPI_GELU: return launch_nt64<EPI_GELU>(a, s);
+    case EPI_RESID: return launch_nt64<EPI_RESID>(a, s);
+    case EPI_GELU_BWD: return launch_nt64<EPI_GELU_BWD>(a, s);
+    case EPI_F32: return launch_nt64<EPI_F32>(a, s);
+  }
+  return hipErrorInvalidValue;
+}
+
 template <bool AK, bool BKM>
 hipError_t dispatch_big(const GemmArgs& a, int epi, hipStream_t s) {
   switch (epi) {
@@ -987,11 +1271,12 @@ hipError_t dispatch_big(const GemmArgs& a, int epi, hipStream_t s) {
 
 // Kernel per layout, from timings of the encoder's products on MI355X: NN (the forward
 // with transposed weights, and the input gradient) runs faster on the 128x256 kernel at
-// every encoder shape; NT and the weight gradient (TN, split over K to fill the chip)
-// take the 256x256 kernel.
+// every encoder shape; NT takes the 256x256 kernel with 64-deep stages (a few per cent
+// faster than with 32-deep ones) and the weight gradient (TN, split over K to fill the
+// chip) the 256x256 kernel.
 hipError_t gemm_big(int layout, int epi, const GemmArgs& a, hipStream_t s) {
   switch (layout) {
-    case GEMM_NT: return dispatch_big<false, false>(a, epi, s);
+    case GEMM_NT: return dispatch_nt64(a, epi, s);
     case GEMM_NN: return dispatch_nn(a, epi, s);
     case GEMM_TN: return dispatch_big<true, true>(a, epi, s);
   }
