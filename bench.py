@@ -164,6 +164,36 @@ def summarize_pmc(fetch_cal: str, write_cal: str, fetch_db: str, write_db: str, 
     print(json.dumps(rec, indent=1))
 
 
+def summarize_traffic_md(out: str, workload: str = "c4_qwen2vl_trained", seed: int = 0):
+    """profiles/hbm_traffic.json (written by --summarize-pmc) -> its markdown table."""
+    with open(TRAFFIC_FILE) as fh:
+        rec = json.load(fh)
+    c = rec["calibration"]
+    rows = sorted(rec["per_launch"].items(), key=lambda kv: -kv[1]["bytes"])
+    lines = [
+        f"# L2<->fabric traffic per launch: encoder training step ({workload}, seed {seed})", "",
+        "Two `rocprofv3 --pmc` runs of one bench step (FETCH_SIZE, then WRITE_SIZE), each scaled "
+        "by what the same counter reads for a plain copy of known size: the library's row gather "
+        "with identity indices, 32768 rows x 3584 bf16 (`bench.py --copy-calibration`).  The TCC "
+        "counters count bytes between the L2 and the data fabric, including reads the 256 MB "
+        "Infinity Cache serves, so they bound HBM traffic from above.", "",
+        "Commands (on the MI355X box; this table: `python3 bench.py --summarize-traffic-md "
+        f"{out}`):", "", "```", rec.get("commands", "").strip(), "```", "",
+        f"Calibration: the copy reads {c['copy_read_bytes']:,} B and writes "
+        f"{c['copy_write_bytes']:,} B; FETCH_SIZE read {c['fetch_kib']:,.0f} KiB (scale "
+        f"{c['fetch_scale']:.3f}), WRITE_SIZE {c['write_kib']:,.0f} KiB (scale {c['write_scale']:.3f}).",
+        "", f"Source digest of the kernels measured: `{rec['digest']}` (bench.py reports the traffic "
+        "only while the tree's kernel sources hash to it).", "",
+        "| kernel class | dispatches | fetch MB/launch | write MB/launch | total MB/launch |",
+        "|---|---:|---:|---:|---:|"]
+    for k, v in rows:
+        lines.append(f"| `{k}` | {v['dispatches']} | {v['fetch_bytes'] / 1e6:,.1f} | "
+                     f"{v['write_bytes'] / 1e6:,.1f} | {v['bytes'] / 1e6:,.1f} |")
+    with open(out, "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+    print(f"wrote {out}")
+
+
 # ---- rocprofv3 summaries kept under profiles/ ---------------------------------------
 SQ_PASS1 = ("SQ_VALU_MFMA_BUSY_CYCLES SQ_INSTS_MFMA SQ_INSTS_VALU SQ_ACTIVE_INST_VALU "
             "SQ_LDS_BANK_CONFLICT SQ_ACTIVE_INST_LDS SQ_WAVE_CYCLES SQ_WAIT_ANY GRBM_GUI_ACTIVE")
@@ -633,6 +663,8 @@ def main():
                     help="LDS / TA / TD / TCP counter passes -> profiles markdown")
     ap.add_argument("--summarize-sq", nargs=3, metavar=("PASS1_DB", "PASS2_DB", "OUT_MD"),
                     help="two rocprofv3 SQ-counter databases -> a markdown summary")
+    ap.add_argument("--summarize-traffic-md", metavar="OUT_MD",
+                    help="profiles/hbm_traffic.json -> its markdown table")
     ap.add_argument("--summarize-workloads", nargs="+", metavar=("OUT_MD", "JSON"),
                     help="bench JSON lines of several workloads -> a markdown table")
     ap.add_argument("--gemm-vs-library", action="store_true",
@@ -648,6 +680,9 @@ def main():
         return
     if args.summarize_sq:
         summarize_sq(*args.summarize_sq[:2], args.pmc_commands, args.summarize_sq[2])
+        return
+    if args.summarize_traffic_md:
+        summarize_traffic_md(args.summarize_traffic_md, args.workload, args.seed)
         return
     if args.summarize_workloads:
         summarize_workloads(args.summarize_workloads[0], args.summarize_workloads[1:],
