@@ -1,10 +1,11 @@
 """Host-side models of the large GEMM kernels' K-tile schedules (gemm_big.hip).
 
-The 256x256 kernel fills an NST-stage LDS ring by DMA (NST = 4): the prologue issues
-tiles 0..NST-1, the steady-state passes (entered while t + 2 NST + 1 <= nk) issue tile
-t + NST from unclamped sources and read fragments without the ragged-K mask, and the
-tail bodies issue tile t + NST through the clamping path.  The 128x256 NN kernel fills
-A two K tiles at a time into two pair stages and B into three stages.  These models
+The 256x256 weight-gradient kernel fills an NST-stage LDS ring by DMA (NST = 4): the
+prologue issues tiles 0..NST-1, the steady-state passes (entered while t + 2 NST + 1 <= nk)
+issue tile t + NST from unclamped sources and read fragments without the ragged-K mask,
+and the tail bodies issue tile t + NST through the clamping path.  The 128x256 NN kernel
+fills A two K tiles at a time into two pair stages and B into three stages.  The NT kernel
+takes 64-deep tiles in two stages and issues tile t + 2 after the barrier in tile t.  These models
 replay the control flow for many K ranges and split sizes and check that every tile
 is filled exactly once, that no unclamped source or unmasked read ever touches the
 last, ragged tile, that each wait leaves only later DMAs pending and that no stage is
@@ -187,3 +188,97 @@ def test_nn_model_flags_a_loose_wait():
     pair unfinished; the model must see that."""
     assert _nn_schedule(0, 40 * BK) == []
     assert ("wait does not cover tile", 2) in _nn_schedule(0, 40 * BK, widen_odd_wait=4)
+
+
+def _nt64_schedule(kbeg, kend, steady_bound=4):
+    """The NT kernel with 64-deep K tiles: tile t in stage t % 2, 8 A + 8 B DMA
+    instructions per wave per tile.  The prologue issues tiles 0 and 1 and waits for tile
+    0; body t reads K steps 1..3 of tile t, waits for every DMA issued (tile t+1), passes
+    the barrier, issues tile t+2 into stage t % 2 and reads K step 0 of tile t+1.  Bodies
+    run fenced and unguarded ("full") while t + steady_bound <= nfull, two at a time, and
+    guarded after that.  steady_bound lets the model check itself (the kernel uses 4)."""
+    BK64 = 64
+    nk = (kend - kbeg + BK64 - 1) // BK64 if kend > kbeg else 0
+    nfull = (kend - kbeg) // BK64 if kend > kbeg else 0
+    problems = []
+    stage = {}                  # stage -> tile it holds
+    landed, pending = set(), set()
+    reads_left = {}             # tile -> K steps not yet read
+    filled = []
+    def dma(t, unclamped):
+        if unclamped and t >= nfull:
+            problems.append(("unclamped DMA of a ragged tile", t))
+        s = t % 2
+        old = stage.get(s)
+        if old is not None and reads_left.get(old, 0) > 0:
+            problems.append(("stage refilled before its last read", t))
+        stage[s] = t
+        pending.add(t)
+        reads_left[t] = 4
+        filled.append(t)
+    def wait_all():
+        landed.update(pending)
+        pending.clear()
+    def read(t, step, masked):
+        if stage.get(t % 2) != t or t not in landed:
+            problems.append(("read of a tile not landed in its stage", (t, step)))
+        if not masked and t >= nfull:
+            problems.append(("unmasked read of a ragged tile", t))
+        reads_left[t] -= 1
+    def body(t, full):
+        if full and not (t + 2 < nfull):
+            problems.append(("unguarded body without a whole tile t+2", t))
+        for step in (1, 2, 3):
+            read(t, step, not full)
+        wait_all()
+        if full:
+            dma(t + 2, True)
+        elif t + 2 < nk:
+            dma(t + 2, t + 2 < nfull)
+        if full or t + 1 < nk:
+            read(t + 1, 0, not full)
+    if nk == 0:
+        return problems
+    dma(0, 0 < nfull)
+    if nk > 1:
+        dma(1, 1 < nfull)
+        pending.discard(0)          # wait_vm<16>: tile 0 landed, tile 1 may stay pending
+        landed.add(0)
+    else:
+        wait_all()
+    read(0, 0, True)
+    t = 0
+    while t + steady_bound <= nfull:
+        body(t, True)
+        body(t + 1, True)
+        t += 2
+    while t < nk:
+        body(t, False)
+        if t + 1 < nk:
+            body(t + 1, False)
+        t += 2
+    if sorted(filled) != list(range(nk)):
+        problems.append(("tiles not filled exactly once", filled))
+    if any(v != 0 for v in reads_left.values()):
+        problems.append(("a tile not read in full", reads_left))
+    return problems
+
+
+@pytest.mark.parametrize("K", list(range(8, 1200, 8)) + [1280, 3840, 5120, 42944])
+def test_nt64_schedule(K):
+    assert _nt64_schedule(0, K) == []
+
+
+@pytest.mark.parametrize("K,kps", [(1000, 256), (42944, 2688), (5000, 64), (1000, 320),
+                                   (300, 128), (4096, 1024)])
+def test_nt64_schedule_split(K, kps):
+    for s in range((K + kps - 1) // kps):
+        assert _nt64_schedule(s * kps, min(K, (s + 1) * kps)) == [], (K, kps, s)
+
+
+def test_nt64_model_flags_a_loose_steady_bound():
+    """Entering the unguarded bodies while t + 3 <= nfull would issue tile t+2 unclamped
+    from the second body of the pair at K = 5 * 64 + 32 (the last tile ragged)."""
+    assert _nt64_schedule(0, 5 * 64 + 32) == []
+    bad = _nt64_schedule(0, 5 * 64 + 32, steady_bound=3)
+    assert any(p[0] == "unguarded body without a whole tile t+2" for p in bad), bad
