@@ -50,7 +50,8 @@ hipError_t gemm(int dtype, int layout, int epi, const GemmArgs& a, hipStream_t s
 bool gemm_fused_colsum(int dtype, int layout, int epi, const GemmArgs& a);
 // out[c] += sum of part[r][c] over r < rows, in a fixed order (two stages).
 hipError_t partials_reduce(float* part, float* out, int64_t rows, int n, hipStream_t s);
-// 256x256-tile bf16 kernel (M >= 512, N >= 256), same contract as gemm()
+// large-tile bf16 kernels (M >= 512, N >= 256): 128x256 NN, 256x256 NT (64-deep K
+// stages) and TN; same contract as gemm()
 hipError_t gemm_big(int layout, int epi, const GemmArgs& a, hipStream_t s);
 
 struct AttnArgs {
