@@ -52,11 +52,14 @@ def model_flops(cfg, n_patches: int, sum_len2: int, trainable: int) -> float:
 def hardware_flops(cfg, n_patches: int, sum_len2: int, trainable: bool) -> float:
     """MFMA work the kernels actually issue: the model FLOPs plus the attention backward's
     recompute (the dQ kernel recomputes S and dP, the dK/dV kernel S: 6 h d sum L^2 per
-    layer) and the head-dim padding of the products over d (d rounded up to 32 for S and
-    dP: one in the forward, four in the backward).  Ragged GEMM tile edges are not counted."""
+    layer), the head-dim padding of the products over d (d rounded up to 32 for S and
+    dP: one in the forward, four in the backward) and the forward's row sums of P, taken
+    by MFMAs with a ones operand (32 FLOP per query-key pair and head).  Ragged tile edges
+    are not counted (the issued-FLOP counter in profiles/ measures them: about 1 % more)."""
     h, d, L = cfg.hidden, cfg.hidden // cfg.heads, cfg.layers
     dpad = (d + 31) // 32 * 32
     extra = 2.0 * h * sum_len2 * (dpad - d) / d      # one S-type product, padding only
+    extra += 32.0 * (h // d) * sum_len2              # forward row sums of P
     per_layer = extra
     if int(trainable) == 1:
         per_layer += 6.0 * h * sum_len2 + 4 * (2.0 * h * sum_len2 * dpad / d)
@@ -162,6 +165,42 @@ def summarize_pmc(fetch_cal: str, write_cal: str, fetch_db: str, write_db: str, 
     with open(TRAFFIC_FILE, "w") as fh:
         json.dump(rec, fh, indent=1)
     print(json.dumps(rec, indent=1))
+
+
+def summarize_mfma_flops(db: str, out: str, cmds: str, workload: str = "c4_qwen2vl_trained",
+                         seed: int = 0):
+    """One rocprofv3 --pmc pass of SQ_INSTS_VALU_MFMA_MOPS_BF16 over one bench step: the bf16
+    MFMA FLOPs the kernels issued (the counter counts multiply-add operations / 512), per
+    kernel class and in total, against the analytic model and hardware FLOPs."""
+    import workload as W
+    wl = W.make_workload(workload, seed)
+    n, s2 = wl.n_patches, int(np.sum(np.diff(wl.cu_seqlens).astype(np.int64) ** 2))
+    mf = model_flops(wl.cfg, n, s2, wl.trainable)
+    hw = hardware_flops(wl.cfg, n, s2, wl.trainable)
+    per = {}
+    for (d, name), v in _pmc_by_dispatch(db, "SQ_INSTS_VALU_MFMA_MOPS_BF16").items():
+        cls = kernel_class(name) or name.split("(")[0][-48:]
+        e = per.setdefault(cls, [0, 0.0])
+        e[0] += 1
+        e[1] += v * 512.0
+    total = sum(v for _, v in per.values())
+    lines = [
+        f"# bf16 MFMA FLOPs issued in one training step ({workload}, seed {seed})", "",
+        "One `rocprofv3 --pmc` pass of one bench step; `SQ_INSTS_VALU_MFMA_MOPS_BF16` counts the "
+        "MFMA multiply-add operations / 512 (the profiler's own `MfmaFlopsBF16` = counter x 512). "
+        "Commands (on the MI355X box):", "", "```", cmds.strip(), "```", "",
+        f"Measured: **{total / 1e12:.3f} TFLOP** per step.  Model FLOPs (bench.py `model_flops`): "
+        f"{mf / 1e12:.3f} TFLOP; hardware model (`hardware_flops`: plus the attention backward's "
+        f"recompute and the head-dim padding): {hw / 1e12:.3f} TFLOP "
+        f"(measured / hardware model = {total / hw:.4f}).", "",
+        "| kernel class | dispatches | TFLOP per step | share |", "|---|---:|---:|---:|"]
+    for cls, (nd, v) in sorted(per.items(), key=lambda kv: -kv[1][1]):
+        if v <= 0:
+            continue
+        lines.append(f"| `{cls}` | {nd} | {v / 1e12:.3f} | {100 * v / total:.1f} % |")
+    with open(out, "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+    print(f"wrote {out}: measured {total / 1e12:.3f} TFLOP, hardware model {hw / 1e12:.3f}")
 
 
 def summarize_traffic_md(out: str, workload: str = "c4_qwen2vl_trained", seed: int = 0):
@@ -663,6 +702,8 @@ def main():
                     help="LDS / TA / TD / TCP counter passes -> profiles markdown")
     ap.add_argument("--summarize-sq", nargs=3, metavar=("PASS1_DB", "PASS2_DB", "OUT_MD"),
                     help="two rocprofv3 SQ-counter databases -> a markdown summary")
+    ap.add_argument("--summarize-mfma-flops", nargs=2, metavar=("DB", "OUT_MD"),
+                    help="rocprofv3 SQ_INSTS_VALU_MFMA_MOPS_BF16 pass -> issued MFMA FLOPs")
     ap.add_argument("--summarize-traffic-md", metavar="OUT_MD",
                     help="profiles/hbm_traffic.json -> its markdown table")
     ap.add_argument("--summarize-workloads", nargs="+", metavar=("OUT_MD", "JSON"),
@@ -680,6 +721,10 @@ def main():
         return
     if args.summarize_sq:
         summarize_sq(*args.summarize_sq[:2], args.pmc_commands, args.summarize_sq[2])
+        return
+    if args.summarize_mfma_flops:
+        summarize_mfma_flops(*args.summarize_mfma_flops, args.pmc_commands, args.workload,
+                             args.seed)
         return
     if args.summarize_traffic_md:
         summarize_traffic_md(args.summarize_traffic_md, args.workload, args.seed)
