@@ -191,7 +191,7 @@ def summarize_mfma_flops(db: str, out: str, cmds: str, workload: str = "c4_qwen2
         "Commands (on the MI355X box):", "", "```", cmds.strip(), "```", "",
         f"Measured: **{total / 1e12:.3f} TFLOP** per step.  Model FLOPs (bench.py `model_flops`): "
         f"{mf / 1e12:.3f} TFLOP; hardware model (`hardware_flops`: plus the attention backward's "
-        f"recompute and the head-dim padding): {hw / 1e12:.3f} TFLOP "
+        f"recompute, the head-dim padding and the forward's row-sum MFMAs): {hw / 1e12:.3f} TFLOP "
         f"(measured / hardware model = {total / hw:.4f}).", "",
         "| kernel class | dispatches | TFLOP per step | share |", "|---|---:|---:|---:|"]
     for cls, (nd, v) in sorted(per.items(), key=lambda kv: -kv[1][1]):
